@@ -1,0 +1,453 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: a closed
+form, a library routine (torch softmax / scaled_dot_product_attention in
+float64), an invariant implied by the definitions, or brute force over explicit
+index sets.  They are chosen so that a dropped term, a wrong sign or index, or a
+transposed operand in any oracle stage fails at least one of them.
+
+Stage -> pins:
+  proxy attention (Alg. 2)        P3 causal rows, P3 n == b equals dense softmax, P4 flat closed form, P5
+  C_struct (Sec. 3.2)             P3 brute force over the anchor set, P3 limits, P4 closed form
+  route (Alg. 2)                  P4 flat head routes PE; sink head routes VS; tie rule
+  a_v / a_s / p (Alg. 3)          P5 closed form for p_v, brute-force diagonal walk for a_s, P8 identities
+  floor and top-k (Alg. 3, Sec. 4.3)  P5 exact set, P6 exact sets at alpha 0.5 / 2, P7 metamorphic
+  PE scores and cutoff (Alg. 4)   P4 closed-form A_tilde and K*, brute-force cutoff, P7 gamma monotone
+  block sets                      P9 structure, slash geometry walk
+  sparse attention (Eq. 1)        P1 all blocks == dense SDPA, P2 explicit-mask softmax
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import crisp_oracle as O
+from tests.helpers import bf16_round, random_head, sink_head
+
+S128 = 1.0 / math.sqrt(128)
+
+
+# ---------------------------------------------------------------- P1, P2 (Eq. 1)
+
+def _sdpa_causal(q, k, v, scale):
+    out = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None, None], torch.from_numpy(k)[None, None], torch.from_numpy(v)[None, None],
+        is_causal=True, scale=scale)
+    return out[0, 0].numpy()
+
+
+@pytest.mark.parametrize("n,block", [(512, 128), (300, 64), (1000, 128), (96, 128)])
+@pytest.mark.parametrize("kind", ["vs", "pe"])
+def test_p1_all_blocks_is_dense(n, block, kind):
+    """k_min = N_b (VS) or gamma = 1 (PE) selects every causal pair, so Eq. 1 is dense causal attention."""
+    if kind == "vs":
+        q, k, v = sink_head(n, beta=6.0, seed=1)
+        q = q + bf16_round(np.random.default_rng(2).standard_normal(q.shape) * 0.3)
+    else:
+        q, k, v = random_head(n, seed=3, scale=0.05)
+    nb = O.n_blocks(n, block)
+    # tau = 0 forces VS, tau > 1 forces PE (C_struct lies in [0, 1])
+    p = O.Params(k_min_blocks=nb, gamma=1.0, tau_proxy=0.0 if kind == "vs" else 1.5)
+    r = O.crisp_head(q, k, v, block, p)
+    assert r.route == (O.ROUTE_VS if kind == "vs" else O.ROUTE_PE)
+    assert r.sets == O.dense_causal_sets(nb)
+    ref = _sdpa_causal(q, k, v, S128)
+    assert np.max(np.abs(r.out - ref)) < 1e-12
+
+
+def test_p2_masked_softmax_identity():
+    """Eq. 1 with the explicit n x n mask M_S (0 on selected, -inf elsewhere) equals the oracle's
+    blockwise attention on the same sets."""
+    n, block = 256, 32
+    q, k, v = random_head(n, seed=5, scale=0.3)
+    nb = O.n_blocks(n, block)
+    rng = np.random.default_rng(6)
+    sets = []
+    for qb in range(nb):
+        s = {0, qb} | {int(x) for x in rng.choice(qb + 1, size=min(qb + 1, 3), replace=False)}
+        sets.append(sorted(s))
+    out = O.sparse_attention(q, k, v, sets, block, S128)
+    M = np.full((n, n), -np.inf)
+    for i in range(n):
+        for j in range(i + 1):
+            if (j // block) in sets[i // block]:
+                M[i, j] = 0.0
+    logits = torch.from_numpy(q @ k.T * S128 + M)
+    ref = (torch.softmax(logits, dim=-1) @ torch.from_numpy(v)).numpy()
+    assert np.max(np.abs(out - ref)) < 1e-12
+
+
+def test_p2_sampled_query_blocks_match_full():
+    n, block = 640, 128
+    q, k, v = random_head(n, seed=7)
+    sets = O.dense_causal_sets(O.n_blocks(n, block))
+    full = O.sparse_attention(q, k, v, sets, block, S128)
+    part = O.sparse_attention(q, k, v, sets, block, S128, qbs=[1, 4])
+    assert np.array_equal(part[128:256], full[128:256]) and np.array_equal(part[512:], full[512:])
+    assert not part[:128].any()
+
+
+# ---------------------------------------------------------------- P3 (Alg. 2, C_struct)
+
+@pytest.mark.parametrize("n,block", [(700, 128), (4096, 128), (50, 64)])
+def test_p3_proxy_rows(n, block):
+    q, k, _ = random_head(n, seed=11)
+    A = O.proxy_attention(q, k, block, S128)
+    b = min(block, n)
+    assert A.shape == (b, n)
+    assert np.allclose(A.sum(axis=1), 1.0, atol=1e-13)
+    for r in range(b):
+        assert not A[r, n - b + r + 1:].any()
+        assert (A[r, : n - b + r + 1] > 0).all()
+
+
+def test_p3_proxy_equals_dense_softmax_when_n_equals_b():
+    n = 128
+    q, k, _ = random_head(n, seed=12)
+    A = O.proxy_attention(q, k, 128, S128)
+    z = torch.from_numpy(q @ k.T * S128)
+    z = z.masked_fill(torch.triu(torch.ones(n, n, dtype=torch.bool), 1), float("-inf"))
+    assert np.max(np.abs(A - torch.softmax(z, -1).numpy())) < 1e-14
+
+
+def test_p3_c_struct_brute_force_and_limits():
+    n, block = 200, 64
+    q, k, _ = random_head(n, seed=13, scale=0.5)
+    A = O.proxy_attention(q, k, block, S128)
+    for ws, wl in [(16, 16), (64, 64), (0, 10), (10, 0), (150, 100), (0, 0), (200, 0), (0, 200)]:
+        anchors = set(range(min(ws, n))) | set(range(max(0, n - wl), n))
+        brute = 0.0
+        for r in range(A.shape[0]):
+            for j in anchors:
+                brute += A[r, j]
+        brute /= A.shape[0]
+        cs = O.c_struct(A, n, ws, wl)
+        assert abs(cs - brute) < 1e-13
+        assert -1e-15 <= cs <= 1 + 1e-12
+        if ws + wl >= n or ws >= n or wl >= n:
+            assert abs(cs - 1.0) < 1e-12
+        if ws == 0 and wl == 0:
+            assert cs == 0.0
+
+
+def test_route_tie_and_sides():
+    assert O.route(0.2, 0.2) == O.ROUTE_VS          # ">=" in Alg. 2
+    assert O.route(np.nextafter(np.float32(0.2), np.float32(0)), 0.2) == O.ROUTE_PE
+    q, k, _ = sink_head(1024, beta=20.0)
+    assert O.crisp_head(q, k, None, 128, O.Params(), attend=False).route == O.ROUTE_VS
+
+
+# ---------------------------------------------------------------- P4 (flat head, closed forms)
+
+def test_p4_flat_head_proxy_and_c_struct():
+    n, block = 4096, 128
+    q = np.zeros((n, 128))
+    k = bf16_round(np.random.default_rng(20).standard_normal((n, 128)))
+    A = O.proxy_attention(q, k, block, S128)
+    b = block
+    for r in (0, 57, 127):
+        i = n - b + r
+        assert np.allclose(A[r, : i + 1], 1.0 / (i + 1), rtol=0, atol=1e-16)
+    closed = sum((128 + r + 1) / (n - b + r + 1) for r in range(b)) / b
+    assert abs(closed - 0.047657) < 5e-7
+    assert abs(O.c_struct(A, n, 128, 128) - closed) < 1e-14
+    assert O.route(closed, 0.2) == O.ROUTE_PE
+
+
+def _flat_kstar(nb, gamma):
+    """Closed form for a flat head: A_tilde[qb, kb] = 1 / (N_b (qb + 1)); whole rows are taken in
+    order until the remainder fits into part of the next row (Alg. 4 with descending order)."""
+    g = float(np.float32(gamma))
+    m = 0
+    while (m + 1) / nb < g:
+        m += 1
+    rest = g - m / nb
+    part = math.ceil(rest * nb * (m + 1) - 1e-9)
+    return m, part, m * (m + 1) // 2 + part
+
+
+@pytest.mark.parametrize("nb,expected", [(512, 118536), (1024, 473657), (32, None), (7, None)])
+def test_p4_flat_head_pe_closed_form(nb, expected):
+    block = 128
+    n = nb * block
+    q = np.zeros((n, 128))
+    k = bf16_round(np.random.default_rng(21).standard_normal((n, 128)))
+    At = O.pe_scores(q, k, block, S128)
+    qb, kb = np.tril_indices(nb)
+    assert np.allclose(At[qb, kb], 1.0 / (nb * (qb + 1)), rtol=1e-14, atol=0)
+    assert not At[np.triu_indices(nb, 1)].any()
+    pairs, kstar, _ = O.pe_select(At, 0.95)
+    m, part, ks = _flat_kstar(nb, 0.95)
+    if expected is not None:
+        assert ks == expected
+    assert kstar == ks
+    want = {(a, c) for a in range(m) for c in range(a + 1)} | {(m, c) for c in range(part)}
+    assert set(pairs) == want
+
+
+def test_pe_cutoff_brute_force():
+    """K* = min{k : sum of the k largest >= gamma} by exhaustive prefix search on a tiny matrix."""
+    rng = np.random.default_rng(22)
+    for trial in range(20):
+        nb = int(rng.integers(1, 9))
+        L = rng.standard_normal((nb, nb)) * rng.uniform(0.1, 4)
+        L[np.triu_indices(nb, 1)] = -np.inf
+        E = np.exp(L - L.max(1, keepdims=True))
+        A = E / E.sum(1, keepdims=True)
+        At = A / A.sum()
+        gamma = float(rng.uniform(0.3, 1.0))
+        items = [(float(np.float32(At[a, c])), a * nb + c, (a, c)) for a in range(nb) for c in range(a + 1)]
+        items.sort(key=lambda t: (-t[0], t[1]))
+        total, want = 0.0, []
+        for val, _, pair in items:
+            if total >= float(np.float32(gamma)):
+                break
+            total += val
+            want.append(pair)
+        pairs, kstar, _ = O.pe_select(At, gamma)
+        assert pairs == want and kstar == len(want)
+
+
+def test_pe_gamma_one_takes_everything():
+    rng = np.random.default_rng(23)
+    nb = 12
+    L = rng.standard_normal((nb, nb))
+    L[np.triu_indices(nb, 1)] = -np.inf
+    E = np.exp(L - L.max(1, keepdims=True))
+    At = (E / E.sum(1, keepdims=True)) / nb
+    _, kstar, _ = O.pe_select(At, 1.0)
+    assert kstar == nb * (nb + 1) // 2
+
+
+# ---------------------------------------------------------------- P5 (mass cliff, App. C)
+
+def _cliff_inputs(n, a_sink, a_col, cols, d=128):
+    q = np.zeros((n, d))
+    k = np.zeros((n, d))
+    k[:4, 0] = 8.0
+    for c in cols:
+        k[c, 1] = 8.0
+    q[:, 0] = a_sink
+    q[:, 1] = a_col
+    return q, k
+
+
+def test_p5_app_c_background_mass():
+    """Last proxy row with k signal keys at logit Delta above n - k background keys:
+    each background key carries eps = e^-Delta / (k + (n - k) e^-Delta) (App. C)."""
+    n = 2048
+    q, k = _cliff_inputs(n, 14.0, 0.0, [])
+    A = O.proxy_attention(q, k, 128, S128)
+    delta = 8 * 14.0 * S128
+    eps = math.exp(-delta) / (4 + (n - 4) * math.exp(-delta))
+    assert abs(A[-1, 100] - eps) < 1e-18 and abs(A[-1, 2000] - eps) < 1e-18
+    assert abs(A[-1, 0] - (1 - (n - 4) * eps) / 4) < 1e-15
+
+
+def test_p5_cliff_closed_form_scores_and_selection():
+    n, block = 2048, 128
+    cols = [5 * 128 + 17, 11 * 128 + 90]
+    q, k = _cliff_inputs(n, 14.0, 6.0, cols)
+    ds, dc = 8 * 14.0 * S128, 8 * 6.0 * S128
+    b, nb = block, n // block
+    # closed form of p_v per block
+    p_v = np.zeros(nb)
+    for r in range(b):
+        i = n - b + r
+        Z = 4 * math.exp(ds) + 2 * math.exp(dc) + (i + 1 - 6)
+        for J in range(nb):
+            lo, hi = J * block, min((J + 1) * block, i + 1)
+            if hi <= lo:
+                continue
+            w = hi - lo
+            if J == 0:
+                w += 4 * (math.exp(ds) - 1)
+            w += sum(math.exp(dc) - 1 for c in cols if lo <= c < hi)
+            p_v[J] += w / Z / b
+    r_ = O.crisp_head(q, k, None, block, O.Params(k_min_blocks=1), attend=False)
+    assert np.allclose(r_.p_v, p_v, rtol=1e-12, atol=1e-18)
+    assert r_.route == O.ROUTE_VS
+    assert r_.S_v == [0, 5, 11]
+    # with a very large alpha only the top k_min blocks survive
+    assert O.vs_select(r_.p_v, 1e6, 3) == [0, 5, 11]
+    assert O.vs_select(r_.p_v, 1e6, 1) == [0]
+
+
+def test_diagonal_scores_by_brute_force_walk():
+    """a_s[j] is the mass on the diagonal through (last proxy row, key j): walk every proxy
+    entry (r, key), take its query-key offset o = i_r - key and the diagonal's key on the last
+    row n - 1 - o, and accumulate -- independent of the oracle's shifted-row sum."""
+    for n, block in [(300, 64), (256, 128), (77, 32)]:
+        q, k, _ = random_head(n, seed=31, scale=0.7)
+        A = O.proxy_attention(q, k, block, S128)
+        b = A.shape[0]
+        a_s = np.zeros(n)
+        a_v = np.zeros(n)
+        for r in range(b):
+            i = n - b + r
+            for key in range(i + 1):
+                o = i - key
+                a_s[n - 1 - o] += A[r, key] / b
+                a_v[key] += A[r, key] / b
+        av, as_, pv, ps = O.vs_scores(A, n, block)
+        assert np.allclose(as_, a_s, rtol=1e-12, atol=1e-17)
+        assert np.allclose(av, a_v, rtol=1e-12, atol=1e-17)
+        for J in range(O.n_blocks(n, block)):
+            assert abs(ps[J] - a_s[J * block:(J + 1) * block].sum()) < 1e-14
+
+
+# ---------------------------------------------------------------- P6 (noise exactly at the floor)
+
+def test_p6_noise_at_floor():
+    n, block = 4096, 128
+    q, k, _ = sink_head(n, beta=math.log(n / 4))
+    r = O.crisp_head(q, k, None, block, O.Params(), attend=False)
+    assert r.route == O.ROUTE_VS
+    nb = n // block
+    mids = r.p_v[1:nb - 1]
+    assert np.all(mids == mids[0])                        # exactly tied middle blocks
+    # alpha = 0.5: every middle block is above half the mean, and so is the last block, whose
+    # rows see on average (B + 1) / 2 of its B keys: mass (B + 1) / (2B) of a middle block
+    assert O.vs_select(r.p_v, 0.5, 8) == list(range(nb))
+    # alpha = 2: only the sink block passes; k_min tops up with the lowest-index ties
+    assert O.vs_select(r.p_v, 2.0, 8) == list(range(8))
+    # alpha = 1: every middle block sits within 1e-4 of the floor (the exemption band)
+    _, _, thr = O.vs_floor(r.p_v, 1.0)
+    assert np.all(np.abs(mids - thr) <= 1e-4 * thr)
+
+
+def test_degenerate_residual_sink_collapse():
+    n = 8192
+    q, k, _ = sink_head(n, beta=40.0)
+    r = O.crisp_head(q, k, None, 128, O.Params(), attend=False)
+    rr, mu, thr = O.vs_floor(r.p_v, 1.0)
+    assert r.route == O.ROUTE_VS and rr == 0.0 and thr == 0.0
+    assert sum(r.p_v[1:-1]) < 2 ** -20
+
+
+# ---------------------------------------------------------------- P7 (metamorphic)
+
+def _structured(n, seed):
+    rng = np.random.default_rng(seed)
+    q, k, v = sink_head(n, beta=float(rng.uniform(5, 9)), seed=seed)
+    cols = rng.choice(np.arange(8, n - 256), size=4, replace=False)
+    for i, c in enumerate(cols):
+        k[c, 1 + i] = 8.0
+        q[:, 1 + i] = bf16_round(np.array([rng.uniform(0.5, 1.2) * math.log(n) * math.sqrt(128) / 8]))[0]
+    q = q + bf16_round(rng.standard_normal(q.shape) * 0.4)
+    return q, k, v
+
+
+@pytest.mark.parametrize("seed", [40, 41, 42])
+def test_p7_alpha_monotone_and_budget(seed):
+    n, block = 4096, 128
+    q, k, _ = _structured(n, seed)
+    A = O.proxy_attention(q, k, block, S128)
+    _, _, pv, ps = O.vs_scores(A, n, block)
+    for p in (pv, ps):
+        prev = None
+        for alpha in (0.25, 0.5, 1.0, 1.5, 2.0, 4.0):
+            for km in (1, 8, 40):
+                S = O.vs_select(p, alpha, km)
+                assert len(S) >= min(km, len(p))
+                _, _, thr = O.vs_floor(p, alpha)
+                above = {J for J in range(len(p)) if np.float32(p[J]) > thr}
+                assert above <= set(S)
+            S1 = set(O.vs_select(p, alpha, 1))
+            if prev is not None:
+                assert S1 <= prev
+            prev = S1
+
+
+def test_p7_gamma_monotone():
+    rng = np.random.default_rng(43)
+    nb = 40
+    L = rng.standard_normal((nb, nb)) * 2
+    L[np.triu_indices(nb, 1)] = -np.inf
+    E = np.exp(L - L.max(1, keepdims=True))
+    At = (E / E.sum(1, keepdims=True)) / nb
+    prev = set()
+    for g in (0.1, 0.5, 0.8, 0.9, 0.95, 0.99, 1.0):
+        cur = set(O.pe_select(At, g)[0])
+        assert prev <= cur
+        prev = cur
+
+
+# ---------------------------------------------------------------- P8 (mass identities)
+
+@pytest.mark.parametrize("n,block", [(4096, 128), (1000, 64), (333, 128)])
+def test_p8_mass_identities(n, block):
+    q, k, _ = _structured(max(n, 600), 44)
+    q, k = q[:n], k[:n]
+    A = O.proxy_attention(q, k, block, S128)
+    av, as_, pv, ps = O.vs_scores(A, n, block)
+    assert abs(av.sum() - 1) < 1e-12 and abs(as_.sum() - 1) < 1e-12
+    assert abs(pv.sum() - 1) < 1e-12 and abs(ps.sum() - 1) < 1e-12
+    assert (pv >= 0).all() and (ps >= 0).all()
+    nb = len(pv)
+    for p in (pv, ps):
+        assert abs(max(1 - p[0] - p[nb - 1], 0) - p[1:nb - 1].sum()) < 1e-12
+
+
+# ---------------------------------------------------------------- P9 (block sets)
+
+def _check_structure(sets, nb):
+    assert len(sets) == nb
+    for qb, s in enumerate(sets):
+        assert s == sorted(set(s)) and s[0] == 0 and s[-1] == qb
+        assert all(0 <= kb <= qb for kb in s)
+
+
+def test_p9_structure_vs_and_pe():
+    n, block = 4096, 128
+    nb = n // block
+    q, k, v = _structured(n, 45)
+    r = O.crisp_head(q, k, None, block, O.Params(), attend=False)
+    assert r.route == O.ROUTE_VS
+    _check_structure(r.sets, nb)
+    q2, k2, _ = random_head(n, seed=46, scale=0.05)
+    r2 = O.crisp_head(q2, k2, None, block, O.Params(), attend=False)
+    assert r2.route == O.ROUTE_PE
+    _check_structure(r2.sets, nb)
+    assert sum(len(s) for s in r2.sets) >= r2.pe_info["kstar"]
+
+
+def test_p9_slash_geometry_walk():
+    """A selected slash block J holds the diagonals with last-row key j in block J.  Walked from
+    the last row of each query block qb, each such diagonal must land in a key block of S(qb)."""
+    nb, block = 24, 64
+    n = nb * block
+    rng = np.random.default_rng(47)
+    S_s = sorted(int(x) for x in rng.choice(nb, size=6, replace=False))
+    S_v = sorted(int(x) for x in rng.choice(nb, size=4, replace=False))
+    sets = O.vs_block_sets(S_v, S_s, nb)
+    for qb in range(nb):
+        i = (qb + 1) * block - 1
+        for J in S_s:
+            for j in range(J * block, (J + 1) * block):
+                o = n - 1 - j
+                key = i - o
+                if key >= 0:
+                    assert key // block in sets[qb]
+        for J in S_v:
+            if J <= qb:
+                assert J in sets[qb]
+        extra = set(sets[qb]) - {0, qb} - {J for J in S_v if J <= qb} - {qb - (nb - 1 - J) for J in S_s}
+        assert not extra
+
+
+def test_p9_mass_accounting_brute_force():
+    """For each query row, the dense softmax mass inside its selected blocks, counted key by key,
+    equals one minus the mass outside, counted block by block."""
+    n, block = 512, 64
+    q, k, _ = _structured(n, 48)
+    r = O.crisp_head(q, k, None, block, O.Params(k_min_blocks=2), attend=False)
+    z = q @ k.T * S128
+    for i in range(0, n, 37):
+        row = np.exp(z[i, : i + 1] - z[i, : i + 1].max())
+        row /= row.sum()
+        inside = sum(row[j] for j in range(i + 1) if (j // block) in r.sets[i // block])
+        outside = sum(row[J * block: min((J + 1) * block, i + 1)].sum()
+                      for J in range(i // block + 1) if J not in r.sets[i // block])
+        assert abs(inside + outside - 1) < 1e-12
