@@ -1,0 +1,82 @@
+"""Builds libcrisp.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+
+    python -m paper_2609_01925_amd.build
+
+Sources are compiled in parallel into _build/ and linked in-tree next to this
+file, so the library travels with the source tree.
+"""
+from __future__ import annotations
+
+import concurrent.futures as cf
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+BUILD = os.path.join(ROOT, "_build")
+LIB = os.path.join(PKG, "libcrisp.so")
+ARCH = "gfx950"
+
+# Packed fp32 VALU forms are kept out of every kernel: the compiler would
+# otherwise form them from ordinary float code.
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall", "-Wno-unused-function"]
+
+
+def hipcc() -> str:
+    for cand in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("hipcc not found (ROCm is required to build libcrisp)")
+
+
+def sources():
+    hip = sorted(f for f in os.listdir(CSRC) if f.endswith(".hip"))
+    cpp = sorted(f for f in os.listdir(CSRC) if f.endswith(".cpp"))
+    return hip, cpp
+
+
+def _run(cmd):
+    p = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    out = "\n".join(line for line in p.stdout.splitlines()
+                    if "packed-fp32-ops' is not a recognized feature" not in line)
+    return p.returncode, " ".join(cmd), out
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source and link libcrisp.so; returns its path.  Raises on failure."""
+    cc = hipcc()
+    os.makedirs(BUILD, exist_ok=True)
+    hip, cpp = sources()
+    jobs = []
+    for f in hip:
+        obj = os.path.join(BUILD, f[:-4] + ".o")
+        jobs.append([cc, f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS, "-c", os.path.join(CSRC, f), "-o", obj])
+    for f in cpp:
+        obj = os.path.join(BUILD, f[:-4] + ".o")
+        jobs.append([cc, f"--offload-arch={ARCH}", *COMMON, "-c", os.path.join(CSRC, f), "-o", obj])
+    workers = min(len(jobs), max(1, min(8, os.cpu_count() or 1)))
+    with cf.ThreadPoolExecutor(workers) as ex:
+        results = list(ex.map(_run, jobs))
+    bad = [(cmd, out) for rc, cmd, out in results if rc != 0]
+    if verbose or bad:
+        for rc, cmd, out in results:
+            if out.strip():
+                print(out, file=sys.stderr)
+    if bad:
+        raise RuntimeError("libcrisp compile failed:\n" + "\n".join(f"$ {c}\n{o}" for c, o in bad))
+    objs = [j[-1] for j in jobs]
+    tmp = LIB + ".tmp"
+    rc, cmd, out = _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
+    if rc != 0:
+        raise RuntimeError(f"libcrisp link failed:\n$ {cmd}\n{out}")
+    os.replace(tmp, LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    print(build(verbose="-v" in sys.argv))

@@ -1,0 +1,102 @@
+// Device-side building blocks shared by the libcrisp kernels (gfx950 / CDNA4).
+//
+// MFMA operand layouts used throughout (v_mfma_f32_32x32x16_bf16, wave64,
+// lane l):
+//   A (32 x 16, M x K): lane l holds row l % 32, k = 8 * (l / 32) + [0, 8)
+//   B (16 x 32, K x N): lane l holds col l % 32, k = 8 * (l / 32) + [0, 8)
+//   C (32 x 32):        lane l holds col l % 32; register i holds
+//                       row 8 * (i / 4) + 4 * (l / 32) + (i % 4)
+// Attention scores are computed transposed (S^T = K Q^T: keys on M, queries on
+// N), so each lane owns one query column and the softmax row reductions stay
+// inside a lane plus one exchange with lane l ^ 32.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "crisp_internal.h"
+
+namespace crisp {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
+
+constexpr int kWave = 64;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kNumXcd = 8;  // MI355X: 8 XCDs; workgroup i runs on XCD i % 8
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// Value held by lane l ^ 32.
+__device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32); }
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// LDS tile swizzle: a row of 128 bf16 is 16 chunks of 16 bytes; chunk c of row r
+// is stored at chunk c ^ swz(r).  swz spreads 16 consecutive rows over 16
+// distinct chunks (conflict-free 16-byte column reads) and 4 consecutive rows
+// over 4 distinct groups of 4 chunks (the 4-row reads of the transposing load).
+__device__ __forceinline__ int swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+
+// Byte offset of element (r, d) in a swizzled [rows][128] bf16 LDS tile.
+__device__ __forceinline__ int lds_off(int r, int d) {
+  return r * 256 + ((((d >> 3) ^ swz(r)) & 15) << 4) + ((d & 7) << 1);
+}
+
+__device__ __forceinline__ bf16x8 lds_read16(const char* base, int off) {
+  return *reinterpret_cast<const bf16x8*>(base + off);
+}
+
+// ds_read_b64_tr_b16: within each group of 16 lanes, lane i receives element i%4
+// of the 8-byte chunks addressed by lanes i/4, 4 + i/4, 8 + i/4, 12 + i/4.
+__device__ __forceinline__ bf16x4 lds_read_tr(const char* base, int off) {
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(base + off));
+  return __builtin_bit_cast(bf16x4, v);
+}
+
+__device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {
+  bf16x8 r;
+  r[0] = a[0]; r[1] = a[1]; r[2] = a[2]; r[3] = a[3];
+  r[4] = b[0]; r[5] = b[1]; r[6] = b[2]; r[7] = b[3];
+  return r;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+__device__ __forceinline__ int div_up(int a, int b) { return (a + b - 1) / b; }
+
+// Wave-wide sums.
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+__device__ __forceinline__ int wave_sum_i(int x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+}  // namespace crisp

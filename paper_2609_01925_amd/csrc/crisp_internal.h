@@ -1,0 +1,44 @@
+// Internal launch interface between the C ABI layer (api.cpp) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace crisp {
+
+constexpr int kHeadDim = 128;
+
+// Shape-derived sizes shared by host and kernels.
+struct Dims {
+  int hq, hkv, G, n, B, nb, b;  // b = min(B, n) proxy rows
+  int64_t cap;                  // nb * (nb + 1) / 2
+};
+
+// Estimator work split: each workgroup owns `bps` whole key blocks.
+struct EstSplit {
+  int bps;
+  int splits;
+};
+EstSplit est_split(const Dims& d);
+
+// Workspace layout (byte offsets; every region 256-byte aligned).
+struct WsLayout {
+  size_t rowstat, rowfinal, parts, masks, qbar, kbar, atil, rhist, rstate, rowinfo, total;
+};
+WsLayout ws_layout(const Dims& d);
+
+hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                       const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, bool dense,
+                       uint16_t* o, hipStream_t stream);
+
+hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, const uint16_t* q,
+                           const uint16_t* k, float* c_struct, float* p_v, float* p_s, char* ws,
+                           hipStream_t stream);
+
+hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, float gamma, int k_min,
+                         const uint16_t* q, const uint16_t* k, const float* c_struct, const float* p_v,
+                         const float* p_s, int8_t* route, int32_t* row_ptr, int32_t* col_idx,
+                         int64_t col_cap, uint8_t* dir_mask, char* ws, hipStream_t stream);
+
+}  // namespace crisp

@@ -1,0 +1,608 @@
+// Stage 3: route each head (Alg. 2), select its key blocks (Alg. 3 with the
+// sink-aware noise floor of Sec. 4.3 for VS heads, Alg. 4 for PE heads) and
+// emit the per-head CSR block lists consumed by the attention kernel.
+//
+// Every kernel reads the route from device memory, so the host never waits on
+// the GPU; kernels for the other route exit on entry.
+//
+// VS, per (head, direction), one workgroup:
+//   floor  r = max((1 - p[0]) - p[N_b-1], 0), mu = r / (N_b - 2), thr = alpha * mu
+//   count  c = #{p > thr};  k = min(max(c, k_min), N_b)
+//   if k > c: radix-select the k-th largest value t on the float bit pattern
+//   (p >= 0, so bit order is value order) and keep ties at t in block order.
+// PE, per head:
+//   pool     mean of Q (PE heads) and K (their KV groups) per block, fp32
+//   logits   pooled Q . K^T * scale * log2(e), block-causal, 64 x 64 tiles
+//   softmax  per row, divided by N_b (the sum of N_b row-normalised rows)
+//   cutoff   the gamma prefix of the descending order is found without a sort:
+//            a radix select over the float bit patterns weighted by mass
+//            (11 + 11 + 10 bits), masses in 2^-60 fixed point so the
+//            cumulative sums are exact and order-independent.  It yields the
+//            value t* of the last pair taken and how many pairs equal to t*
+//            (in flat order qb * N_b + kb) complete the gamma mass.
+// CSR: count per row -> per-head scan -> fill, one wave per row, ballots for
+// compaction; rows always hold the sink block 0 and the diagonal block qb.
+#include "crisp_device.h"
+#include "crisp_internal.h"
+
+namespace crisp {
+
+namespace {
+
+struct RState {
+  uint32_t prefix;   // bits of t* found so far
+  uint32_t all;      // 1: the total mass never reaches gamma, keep every pair
+  unsigned long long need;  // mass (2^-60 units) still to cover below the current prefix
+  unsigned long long ceq;   // pairs equal to t* to take, in flat order
+  unsigned long long pad;
+};
+
+struct SelArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const float* c_struct;
+  const float* p_v;
+  const float* p_s;
+  int8_t* route;
+  int32_t* row_ptr;
+  int32_t* col_idx;
+  int64_t col_cap;
+  uint8_t* dir_mask;
+  int n, nb, B, hq, hkv, G;
+  float c2;  // softmax scale * log2(e)
+  float alpha, tau, gamma;
+  int k_min;
+  int64_t cap;  // nb * (nb + 1) / 2
+  uint8_t* masks;
+  float* qbar;
+  float* kbar;
+  float* atil;
+  unsigned long long* rhist;
+  RState* rstate;
+  int4* rowinfo;
+};
+
+constexpr int kRadixBins = 2048;
+constexpr double kFix = 1152921504606846976.0;  // 2^60
+
+__device__ __forceinline__ uint32_t fbits(float x) {
+  uint32_t b = __float_as_uint(x);
+  return (b & 0x80000000u) ? 0u : b;  // negatives (and -0) rank as 0
+}
+
+__device__ __forceinline__ unsigned long long fixed_mass(uint32_t bits) {
+  return (unsigned long long)((double)__uint_as_float(bits) * kFix);
+}
+
+__device__ __forceinline__ uint64_t lanemask_lt() {
+  const int l = lane_id();
+  return l == 0 ? 0ull : (~0ull >> (64 - l));
+}
+
+// Exclusive prefix count of `flag` over a 1024-thread block; *total gets the block total.
+__device__ int block_scan_1024(int flag, int* wtot, int* total) {
+  const int tid = threadIdx.x, w = tid >> 6;
+  const uint64_t bal = __ballot(flag);
+  const int within = __popcll(bal & lanemask_lt());
+  if ((tid & 63) == 0) wtot[w] = __popcll(bal);
+  __syncthreads();
+  int before = 0, all = 0;
+  for (int i = 0; i < 16; ++i) {
+    const int t = wtot[i];
+    if (i < w) before += t;
+    all += t;
+  }
+  __syncthreads();
+  *total = all;
+  return before + within;
+}
+
+__device__ int block_sum_1024(int x, int* wtot) {
+  x = wave_sum_i(x);
+  const int tid = threadIdx.x;
+  if ((tid & 63) == 0) wtot[tid >> 6] = x;
+  __syncthreads();
+  int s = 0;
+  for (int i = 0; i < 16; ++i) s += wtot[i];
+  __syncthreads();
+  return s;
+}
+
+// k-th largest bit pattern (k >= 1) among fbits(p[0..nb)).
+__device__ uint32_t kth_largest(const float* p, int nb, int k, uint32_t* hist, int* sh) {
+  const int tid = threadIdx.x;
+  uint32_t prefix = 0, pmask = 0;
+  int rem = k;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int i = tid; i < 256; i += 1024) hist[i] = 0;
+    __syncthreads();
+    for (int J = tid; J < nb; J += 1024) {
+      const uint32_t b = fbits(p[J]);
+      if ((b & pmask) == prefix) atomicAdd(&hist[(b >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int cum = 0, d = 255;
+      for (; d > 0; --d) {
+        if (cum + (int)hist[d] >= rem) break;
+        cum += hist[d];
+      }
+      sh[0] = d;
+      sh[1] = rem - cum;
+    }
+    __syncthreads();
+    prefix |= (uint32_t)sh[0] << shift;
+    pmask |= 255u << shift;
+    rem = sh[1];
+    __syncthreads();
+  }
+  return prefix;
+}
+
+// Route (Alg. 2) and VS selection per direction (Alg. 3).  grid (hq, 2), 1024 threads.
+__global__ __launch_bounds__(1024) void sel_route_vs(SelArgs a) {
+  __shared__ uint32_t hist[256];
+  __shared__ int wtot[16];
+  __shared__ int sh[2];
+  const int h = blockIdx.x, dir = blockIdx.y, tid = threadIdx.x;
+  const bool vs = a.c_struct[h] >= a.tau;
+  if (dir == 0 && tid == 0) a.route[h] = vs ? 0 : 1;
+  const int nb = a.nb;
+  const float* p = (dir == 0 ? a.p_v : a.p_s) + (size_t)h * nb;
+  uint8_t* m = a.masks + ((size_t)h * 2 + dir) * nb;
+  uint8_t* dm = a.dir_mask ? a.dir_mask + ((size_t)h * 2 + dir) * nb : nullptr;
+  if (!vs || nb <= 2) {
+    for (int J = tid; J < nb; J += 1024) {
+      m[J] = 0;
+      if (dm) dm[J] = 0;
+    }
+    return;
+  }
+  const float r = fmaxf((1.0f - p[0]) - p[nb - 1], 0.0f);
+  const float mu = r / (float)(nb - 2);
+  const float thr = a.alpha * mu;
+  int c = 0;
+  for (int J = tid; J < nb; J += 1024) c += p[J] > thr;
+  c = block_sum_1024(c, wtot);
+  int kd = c > a.k_min ? c : a.k_min;
+  kd = kd < nb ? kd : nb;
+  if (kd == c) {
+    for (int J = tid; J < nb; J += 1024) {
+      const uint8_t s = p[J] > thr;
+      m[J] = s;
+      if (dm) dm[J] = s;
+    }
+    return;
+  }
+  const uint32_t t = kth_largest(p, nb, kd, hist, sh);
+  int ngt = 0;
+  for (int J = tid; J < nb; J += 1024) ngt += fbits(p[J]) > t;
+  ngt = block_sum_1024(ngt, wtot);
+  const int need = kd - ngt;
+  int running = 0;
+  for (int base = 0; base < nb; base += 1024) {
+    const int J = base + tid;
+    const uint32_t b = J < nb ? fbits(p[J]) : 0u;
+    const int eq = J < nb && b == t;
+    int tot;
+    const int rank = running + block_scan_1024(eq, wtot, &tot);
+    if (J < nb) {
+      const uint8_t s = (b > t) || (eq && rank < need);
+      m[J] = s;
+      if (dm) dm[J] = s;
+    }
+    running += tot;
+  }
+}
+
+// Mean-pool Q of PE heads and K of KV groups with a PE head (Alg. 4).  grid (nb, hq + hkv), 256 threads.
+__global__ __launch_bounds__(256) void sel_pool(SelArgs a) {
+  __shared__ float red[16][128];
+  const int J = blockIdx.x, y = blockIdx.y, tid = threadIdx.x;
+  const uint16_t* src;
+  float* dst;
+  if (y < a.hq) {
+    if (a.route[y] != 1) return;
+    src = a.q + (size_t)y * a.n * kHeadDim;
+    dst = a.qbar + ((size_t)y * a.nb + J) * kHeadDim;
+  } else {
+    const int g = y - a.hq;
+    bool any = false;
+    for (int i = 0; i < a.G; ++i) any |= a.route[g * a.G + i] == 1;
+    if (!any) return;
+    src = a.k + (size_t)g * a.n * kHeadDim;
+    dst = a.kbar + ((size_t)g * a.nb + J) * kHeadDim;
+  }
+  const int r0 = J * a.B;
+  const int r1 = r0 + a.B < a.n ? r0 + a.B : a.n;
+  const int c = tid & 15, rg = tid >> 4;
+  float acc[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  for (int r = r0 + rg; r < r1; r += 16) {
+    const u32x4 raw = *reinterpret_cast<const u32x4*>(src + (size_t)r * kHeadDim + 8 * c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[2 * e] += __uint_as_float(raw[e] << 16);
+      acc[2 * e + 1] += __uint_as_float(raw[e] & 0xffff0000u);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) red[rg][8 * c + e] = acc[e];
+  __syncthreads();
+  if (tid < 128) {
+    float s = 0.f;
+    for (int i = 0; i < 16; ++i) s += red[i][tid];
+    dst[tid] = s / (float)(r1 - r0);
+  }
+}
+
+// Pooled logits (log2 domain), 64 x 64 tiles of the block-causal triangle.  grid (ntri, hq), 256 threads.
+__global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
+  __shared__ float Qs[128][64];
+  __shared__ float Ks[128][64];
+  const int h = blockIdx.y, tid = threadIdx.x;
+  if (a.route[h] != 1) return;
+  const int t = blockIdx.x;
+  int qt = (int)((sqrtf(8.f * (float)t + 1.f) - 1.f) * 0.5f);
+  while ((qt + 1) * (qt + 2) / 2 <= t) ++qt;
+  while (qt * (qt + 1) / 2 > t) --qt;
+  const int kt = t - qt * (qt + 1) / 2;
+  const int qb0 = qt * 64, kb0 = kt * 64;
+  const float* Qb = a.qbar + (size_t)h * a.nb * kHeadDim;
+  const float* Kb = a.kbar + (size_t)(h / a.G) * a.nb * kHeadDim;
+  for (int idx = tid; idx < 64 * 32; idx += 256) {
+    const int row = idx >> 5, d4 = idx & 31;
+    float4 qv = make_float4(0.f, 0.f, 0.f, 0.f), kv = qv;
+    if (qb0 + row < a.nb) qv = *reinterpret_cast<const float4*>(Qb + (size_t)(qb0 + row) * kHeadDim + 4 * d4);
+    if (kb0 + row < a.nb) kv = *reinterpret_cast<const float4*>(Kb + (size_t)(kb0 + row) * kHeadDim + 4 * d4);
+    Qs[4 * d4 + 0][row] = qv.x; Qs[4 * d4 + 1][row] = qv.y; Qs[4 * d4 + 2][row] = qv.z; Qs[4 * d4 + 3][row] = qv.w;
+    Ks[4 * d4 + 0][row] = kv.x; Ks[4 * d4 + 1][row] = kv.y; Ks[4 * d4 + 2][row] = kv.z; Ks[4 * d4 + 3][row] = kv.w;
+  }
+  __syncthreads();
+  const int tx = tid & 15, ty = tid >> 4;
+  float acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+  for (int d = 0; d < kHeadDim; ++d) {
+    const float4 qa = *reinterpret_cast<const float4*>(&Qs[d][4 * ty]);
+    const float4 ka = *reinterpret_cast<const float4*>(&Ks[d][4 * tx]);
+    const float qv[4] = {qa.x, qa.y, qa.z, qa.w};
+    const float kv[4] = {ka.x, ka.y, ka.z, ka.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_fmaf(qv[i], kv[j], acc[i][j]);
+  }
+  float* At = a.atil + (size_t)h * a.cap;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int qb = qb0 + 4 * ty + i;
+    if (qb >= a.nb) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int kb = kb0 + 4 * tx + j;
+      if (kb <= qb) At[(int64_t)qb * (qb + 1) / 2 + kb] = acc[i][j] * a.c2;
+    }
+  }
+}
+
+// Row softmax of the pooled logits, divided by N_b.  grid (nb, hq), 256 threads.
+__global__ __launch_bounds__(256) void sel_pe_softmax(SelArgs a) {
+  __shared__ float red[256];
+  const int qb = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+  if (a.route[h] != 1) return;
+  float* row = a.atil + (size_t)h * a.cap + (int64_t)qb * (qb + 1) / 2;
+  const int len = qb + 1;
+  float mx = -__builtin_inff();
+  for (int i = tid; i < len; i += 256) mx = fmaxf(mx, row[i]);
+  red[tid] = mx;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) red[tid] = fmaxf(red[tid], red[tid + s]);
+    __syncthreads();
+  }
+  mx = red[0];
+  __syncthreads();
+  float sum = 0.f;
+  for (int i = tid; i < len; i += 256) sum += fast_exp2(row[i] - mx);
+  red[tid] = sum;
+  __syncthreads();
+  for (int s = 128; s > 0; s >>= 1) {
+    if (tid < s) red[tid] += red[tid + s];
+    __syncthreads();
+  }
+  sum = red[0];
+  const float inv_nb = 1.f / (float)a.nb;
+  for (int i = tid; i < len; i += 256) row[i] = fast_exp2(row[i] - mx) / sum * inv_nb;
+}
+
+// Radix state init: need = ceil(gamma * 2^60), histogram cleared.  grid hq, 256 threads.
+__global__ __launch_bounds__(256) void sel_radix_init(SelArgs a) {
+  const int h = blockIdx.x, tid = threadIdx.x;
+  if (a.route[h] != 1) return;
+  for (int i = tid; i < kRadixBins; i += 256) a.rhist[(size_t)h * kRadixBins + i] = 0ull;
+  if (tid == 0) {
+    RState s;
+    s.prefix = 0;
+    s.all = 0;
+    s.need = (unsigned long long)ceil((double)a.gamma * kFix);
+    if (s.need == 0) s.need = 1;
+    s.ceq = 0;
+    s.pad = 0;
+    a.rstate[h] = s;
+  }
+}
+
+__device__ __forceinline__ void radix_digit(int pass, int& shift, int& nbits) {
+  shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
+  nbits = pass == 2 ? 10 : 11;
+}
+
+// Mass histogram of one digit over the pairs whose higher digits match the prefix.
+// grid (chunks, hq), 256 threads.
+__global__ __launch_bounds__(256) void sel_radix_hist(SelArgs a, int pass) {
+  __shared__ unsigned long long lh[kRadixBins];
+  const int h = blockIdx.y, tid = threadIdx.x;
+  if (a.route[h] != 1) return;
+  const RState st = a.rstate[h];
+  if (st.all) return;
+  int shift, nbits;
+  radix_digit(pass, shift, nbits);
+  const int hi = shift + nbits;
+  const uint64_t want = (uint64_t)st.prefix >> hi;
+  for (int i = tid; i < kRadixBins; i += 256) lh[i] = 0ull;
+  __syncthreads();
+  const float* At = a.atil + (size_t)h * a.cap;
+  const int64_t per = (a.cap + gridDim.x - 1) / gridDim.x;
+  const int64_t lo = (int64_t)blockIdx.x * per;
+  const int64_t up = lo + per < a.cap ? lo + per : a.cap;
+  const uint32_t dmask = (1u << nbits) - 1u;
+  for (int64_t i = lo + tid; i < up; i += 256) {
+    const uint32_t b = fbits(At[i]);
+    if (((uint64_t)b >> hi) == want) atomicAdd(&lh[(b >> shift) & dmask], fixed_mass(b));
+  }
+  __syncthreads();
+  for (int i = tid; i < kRadixBins; i += 256)
+    if (lh[i]) atomicAdd(&a.rhist[(size_t)h * kRadixBins + i], lh[i]);
+}
+
+// Picks the digit where the descending cumulative mass reaches `need`.  grid hq, 256 threads.
+__global__ __launch_bounds__(256) void sel_radix_scan(SelArgs a, int pass) {
+  __shared__ unsigned long long part[256];
+  const int h = blockIdx.x, tid = threadIdx.x;
+  if (a.route[h] != 1) return;
+  RState st = a.rstate[h];
+  if (st.all) return;
+  int shift, nbits;
+  radix_digit(pass, shift, nbits);
+  const int nbins = 1 << nbits;
+  unsigned long long* H = a.rhist + (size_t)h * kRadixBins;
+  // thread tid owns bins [top - 8 tid - 7, top - 8 tid] (descending)
+  const int per = nbins / 256;
+  unsigned long long s = 0;
+  for (int i = 0; i < per; ++i) s += H[nbins - 1 - (tid * per + i)];
+  part[tid] = s;
+  __syncthreads();
+  if (tid == 0) {
+    unsigned long long cum = 0;
+    int t = 0;
+    for (; t < 256; ++t) {
+      if (cum + part[t] >= st.need) break;
+      cum += part[t];
+    }
+    if (t == 256) {
+      st.all = 1;  // total mass below gamma: keep every pair
+      st.ceq = ~0ull;
+    } else {
+      int bin = nbins - 1 - t * per;
+      for (int i = 0; i < per; ++i, --bin) {
+        if (cum + H[bin] >= st.need) break;
+        cum += H[bin];
+      }
+      st.need -= cum;
+      st.prefix |= (uint32_t)bin << shift;
+      if (pass == 2) {
+        const unsigned long long ft = fixed_mass(st.prefix);
+        st.ceq = ft ? (st.need + ft - 1) / ft : ~0ull;
+      }
+    }
+    a.rstate[h] = st;
+  }
+  __syncthreads();
+  for (int i = tid; i < kRadixBins; i += 256) H[i] = 0ull;
+}
+
+// Per-row counts.  VS: x = row size.  PE: x = #(> t*), y = #(== t*), z = flags
+// (1: block 0 > t*, 2: block 0 == t*, 4: block qb > t*, 8: block qb == t*).
+// grid (ceil(nb / 4), hq), 256 threads, one wave per row.
+__global__ __launch_bounds__(256) void sel_csr_count(SelArgs a) {
+  const int h = blockIdx.y, w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int qb = blockIdx.x * 4 + w;
+  if (qb >= a.nb) return;
+  const int nb = a.nb;
+  int4 info = make_int4(0, 0, 0, 0);
+  if (a.route[h] == 0) {
+    const uint8_t* vm = a.masks + (size_t)h * 2 * nb;
+    const uint8_t* sm = vm + nb;
+    int cnt = 0;
+    for (int base = 0; base <= qb; base += 64) {
+      const int kb = base + l;
+      const bool sel = kb <= qb && (kb == 0 || kb == qb || vm[kb] || sm[nb - 1 - qb + kb]);
+      cnt += __popcll(__ballot(sel));
+    }
+    info.x = cnt;
+  } else {
+    const RState st = a.rstate[h];
+    const float* row = a.atil + (size_t)h * a.cap + (int64_t)qb * (qb + 1) / 2;
+    int ngt = 0, neq = 0, flags = 0;
+    for (int base = 0; base <= qb; base += 64) {
+      const int kb = base + l;
+      const uint32_t b = kb <= qb ? fbits(row[kb]) : 0u;
+      const bool gt = kb <= qb && (st.all || b > st.prefix);
+      const bool eq = kb <= qb && !st.all && b == st.prefix;
+      ngt += __popcll(__ballot(gt));
+      neq += __popcll(__ballot(eq));
+      int f = 0;
+      if (kb == 0) f |= (gt ? 1 : 0) | (eq ? 2 : 0);
+      if (kb == qb) f |= (gt ? 4 : 0) | (eq ? 8 : 0);
+      f = wave_sum_i(f);  // at most two lanes contribute, with disjoint bits
+      flags |= f;
+    }
+    info = make_int4(ngt, neq, flags, 0);
+  }
+  if (l == 0) a.rowinfo[(size_t)h * nb + qb] = info;
+}
+
+// Ties taken per PE row, row sizes and the exclusive scan into row_ptr.  grid hq, 1024 threads.
+__global__ __launch_bounds__(1024) void sel_csr_scan(SelArgs a) {
+  __shared__ long long wtot[16];
+  const int h = blockIdx.x, tid = threadIdx.x, w = tid >> 6;
+  const int nb = a.nb;
+  const bool pe = a.route[h] == 1;
+  const RState st = pe ? a.rstate[h] : RState{};
+  int4* info = a.rowinfo + (size_t)h * nb;
+  int32_t* rp = a.row_ptr + (size_t)h * (nb + 1);
+  long long tie_carry = 0, row_carry = 0;
+  for (int base = 0; base < nb; base += 1024) {
+    const int qb = base + tid;
+    int4 in = qb < nb ? info[qb] : make_int4(0, 0, 0, 0);
+    // inclusive scans (ties, then row sizes) by waves + wave totals
+    long long cnt = 0;
+    if (pe) {
+      long long x = in.y, incl = x;
+      for (int o = 1; o < 64; o <<= 1) {
+        const long long y = __shfl_up(incl, o);
+        if ((tid & 63) >= o) incl += y;
+      }
+      if ((tid & 63) == 63) wtot[w] = incl;
+      __syncthreads();
+      long long before = 0, all = 0;
+      for (int i = 0; i < 16; ++i) {
+        if (i < w) before += wtot[i];
+        all += wtot[i];
+      }
+      __syncthreads();
+      const long long tie_prefix = tie_carry + before + incl - x;
+      tie_carry += all;
+      long long take = 0;
+      if (qb < nb) {
+        const unsigned long long ceq = st.ceq;
+        if (ceq > (unsigned long long)tie_prefix) {
+          const unsigned long long left = ceq - (unsigned long long)tie_prefix;
+          take = left < (unsigned long long)in.y ? (long long)left : (long long)in.y;
+        }
+        const bool z_sel = (in.z & 1) || ((in.z & 2) && take >= 1);
+        const bool d_sel = (in.z & 4) || ((in.z & 8) && take == in.y);
+        cnt = in.x + take + (z_sel ? 0 : 1) + ((qb > 0 && !d_sel) ? 1 : 0);
+        in.w = (int)take;
+        info[qb] = in;
+      }
+    } else if (qb < nb) {
+      cnt = in.x;
+    }
+    long long incl = cnt;
+    for (int o = 1; o < 64; o <<= 1) {
+      const long long y = __shfl_up(incl, o);
+      if ((tid & 63) >= o) incl += y;
+    }
+    if ((tid & 63) == 63) wtot[w] = incl;
+    __syncthreads();
+    long long before = 0, all = 0;
+    for (int i = 0; i < 16; ++i) {
+      if (i < w) before += wtot[i];
+      all += wtot[i];
+    }
+    __syncthreads();
+    if (qb < nb) rp[qb] = (int32_t)(row_carry + before + incl - cnt);
+    row_carry += all;
+  }
+  if (tid == 0) rp[nb] = (int32_t)row_carry;
+}
+
+// Write the block lists.  grid (ceil(nb / 4), hq), 256 threads, one wave per row.
+__global__ __launch_bounds__(256) void sel_csr_fill(SelArgs a) {
+  const int h = blockIdx.y, w = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int qb = blockIdx.x * 4 + w;
+  if (qb >= a.nb) return;
+  const int nb = a.nb;
+  int32_t* out = a.col_idx + (size_t)h * a.col_cap + a.row_ptr[(size_t)h * (nb + 1) + qb];
+  const uint64_t lt = lanemask_lt();
+  int pos = 0;
+  if (a.route[h] == 0) {
+    const uint8_t* vm = a.masks + (size_t)h * 2 * nb;
+    const uint8_t* sm = vm + nb;
+    for (int base = 0; base <= qb; base += 64) {
+      const int kb = base + l;
+      const bool sel = kb <= qb && (kb == 0 || kb == qb || vm[kb] || sm[nb - 1 - qb + kb]);
+      const uint64_t bal = __ballot(sel);
+      if (sel) out[pos + __popcll(bal & lt)] = kb;
+      pos += __popcll(bal);
+    }
+  } else {
+    const RState st = a.rstate[h];
+    const int take = a.rowinfo[(size_t)h * nb + qb].w;
+    const float* row = a.atil + (size_t)h * a.cap + (int64_t)qb * (qb + 1) / 2;
+    int eq_seen = 0;
+    for (int base = 0; base <= qb; base += 64) {
+      const int kb = base + l;
+      const uint32_t b = kb <= qb ? fbits(row[kb]) : 0u;
+      const bool gt = kb <= qb && (st.all || b > st.prefix);
+      const bool eq = kb <= qb && !st.all && b == st.prefix;
+      const uint64_t eb = __ballot(eq);
+      const int eq_rank = eq_seen + __popcll(eb & lt);
+      eq_seen += __popcll(eb);
+      const bool sel = kb <= qb && (gt || (eq && eq_rank < take) || kb == 0 || kb == qb);
+      const uint64_t bal = __ballot(sel);
+      if (sel) out[pos + __popcll(bal & lt)] = kb;
+      pos += __popcll(bal);
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, float gamma, int k_min,
+                         const uint16_t* q, const uint16_t* k, const float* c_struct, const float* p_v,
+                         const float* p_s, int8_t* route, int32_t* row_ptr, int32_t* col_idx,
+                         int64_t col_cap, uint8_t* dir_mask, char* ws, hipStream_t stream) {
+  if (d.n == 0 || d.hq == 0) return hipSuccess;
+  const WsLayout L = ws_layout(d);
+  SelArgs a;
+  a.q = q; a.k = k; a.c_struct = c_struct; a.p_v = p_v; a.p_s = p_s;
+  a.route = route; a.row_ptr = row_ptr; a.col_idx = col_idx; a.col_cap = col_cap; a.dir_mask = dir_mask;
+  a.n = d.n; a.nb = d.nb; a.B = d.B; a.hq = d.hq; a.hkv = d.hkv; a.G = d.G;
+  a.c2 = scale * kLog2e;
+  a.alpha = alpha; a.tau = tau; a.gamma = gamma; a.k_min = k_min;
+  a.cap = d.cap;
+  a.masks = reinterpret_cast<uint8_t*>(ws + L.masks);
+  a.qbar = reinterpret_cast<float*>(ws + L.qbar);
+  a.kbar = reinterpret_cast<float*>(ws + L.kbar);
+  a.atil = reinterpret_cast<float*>(ws + L.atil);
+  a.rhist = reinterpret_cast<unsigned long long*>(ws + L.rhist);
+  a.rstate = reinterpret_cast<RState*>(ws + L.rstate);
+  a.rowinfo = reinterpret_cast<int4*>(ws + L.rowinfo);
+  const int nb = d.nb;
+  hipLaunchKernelGGL(sel_route_vs, dim3(d.hq, 2), dim3(1024), 0, stream, a);
+  hipLaunchKernelGGL(sel_pool, dim3(nb, d.hq + d.hkv), dim3(256), 0, stream, a);
+  const int nt = (nb + 63) / 64;
+  hipLaunchKernelGGL(sel_pe_logits, dim3(nt * (nt + 1) / 2, d.hq), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(sel_pe_softmax, dim3(nb, d.hq), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(sel_radix_init, dim3(d.hq), dim3(256), 0, stream, a);
+  int64_t chunks = (d.cap + 16383) / 16384;
+  if (chunks > 1024) chunks = 1024;
+  if (chunks < 1) chunks = 1;
+  for (int pass = 0; pass < 3; ++pass) {
+    hipLaunchKernelGGL(sel_radix_hist, dim3((unsigned)chunks, d.hq), dim3(256), 0, stream, a, pass);
+    hipLaunchKernelGGL(sel_radix_scan, dim3(d.hq), dim3(256), 0, stream, a, pass);
+  }
+  const int rows_grid = (nb + 3) / 4;
+  hipLaunchKernelGGL(sel_csr_count, dim3(rows_grid, d.hq), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(sel_csr_scan, dim3(d.hq), dim3(1024), 0, stream, a);
+  hipLaunchKernelGGL(sel_csr_fill, dim3(rows_grid, d.hq), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace crisp

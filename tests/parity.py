@@ -1,0 +1,130 @@
+"""GPU-vs-oracle parity rules for CRISP.
+
+Integer results (routes, block sets, CSR lists) must match exactly, except for
+decisions whose deciding value lies within 1e-4 (relative) of the threshold in
+the oracle's own arithmetic, where a different rounding order may legitimately
+flip them:
+  E1  VS floor band:   |p_d[J] - alpha mu_d| <= 1e-4 alpha mu_d
+  E2  VS top-up band:  when fewer than k_min blocks pass the floor, blocks with
+                       |p_d[J] - t| <= 1e-4 t, t = the k_min-th largest p_d
+  E3  degenerate residual: r_d < 2^-20 (below float32 resolution next to 1):
+                       only the forced blocks and the invariants are checked
+  E4  PE cutoff band:  pairs with |A~ - t*| <= 1e-4 t*, t* = A~ of the last pair
+                       taken; if the cumulative mass before or at the cutoff is
+                       within 1e-4 gamma of gamma, the pairs at K* and K*+1 too
+Floating-point outputs: attention max-abs <= 2e-2 and mean-abs <= 2e-3 (bf16 against
+the float64 oracle); C_struct abs 1e-5; p_v, p_s rtol 1e-4 with atol 1e-7.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from oracle import crisp_oracle as O
+
+BAND = 1e-4
+ATTN_MAX_ABS = 2e-2
+ATTN_MEAN_ABS = 2e-3
+CS_ABS = 1e-5
+P_RTOL, P_ATOL = 1e-4, 1e-7
+
+
+def csr_to_sets(row_ptr: np.ndarray, col_idx: np.ndarray, h: int, nb: int):
+    rp = row_ptr[h]
+    return [col_idx[h, rp[qb]:rp[qb + 1]].tolist() for qb in range(nb)]
+
+
+def check_structure(sets, nb, where=""):
+    assert len(sets) == nb, where
+    for qb, s in enumerate(sets):
+        assert s == sorted(set(s)), f"{where} row {qb} not sorted/unique: {s[:20]}"
+        assert s and s[0] == 0 and s[-1] == qb, f"{where} row {qb} misses forced blocks: {s[:10]}..{s[-3:]}"
+
+
+def vs_direction_exempt(p: np.ndarray, alpha: float, k_min: int):
+    """Returns (degenerate, exempt block set) for one VS direction, from oracle values."""
+    nb = len(p)
+    r64 = max(1.0 - p[0] - p[nb - 1], 0.0)
+    if r64 < 2.0 ** -20:
+        return True, set(range(nb))
+    _, _, thr = O.vs_floor(p, alpha)
+    thr = float(thr)
+    ex = {J for J in range(nb) if abs(p[J] - thr) <= BAND * thr}
+    c = int(np.count_nonzero(np.asarray(p, np.float32) > np.float32(thr)))
+    if c < k_min:
+        t = float(np.sort(p)[::-1][min(k_min, nb) - 1])
+        ex |= {J for J in range(nb) if abs(p[J] - t) <= BAND * t}
+    return False, ex
+
+
+def compare_vs(gpu_mask: np.ndarray, ores: O.HeadResult, alpha: float, k_min: int, where=""):
+    """gpu_mask: uint8 [2, N_b] (S_v, S_s membership)."""
+    nb = gpu_mask.shape[1]
+    for dir_, (p, S) in enumerate(((ores.p_v, ores.S_v), (ores.p_s, ores.S_s))):
+        gsel = set(np.nonzero(gpu_mask[dir_])[0].tolist())
+        if nb <= 2:
+            assert not gsel, where
+            continue
+        degenerate, ex = vs_direction_exempt(p, alpha, k_min)
+        if degenerate:
+            continue
+        diff = gsel ^ set(S)
+        bad = diff - ex
+        assert not bad, f"{where} dir {'vs'[dir_]}: blocks {sorted(bad)[:20]} differ (gpu {sorted(gsel)[:30]}, oracle {S[:30]})"
+        assert len(gsel) >= min(k_min, nb), f"{where} dir {'vs'[dir_]}: only {len(gsel)} blocks"
+
+
+def compare_pe(gpu_sets, ores: O.HeadResult, gamma: float, where=""):
+    """Row-by-row comparison of a PE head's block sets with the oracle's, E4 exemptions applied."""
+    At = ores.A_tilde
+    nb = At.shape[0]
+    info = ores.pe_info
+    vals = At.astype(np.float32)
+    tstar = np.float32(info["t_star"])
+    g = float(np.float32(gamma))
+    exempt_val = lambda v: abs(float(v) - float(tstar)) <= BAND * float(tstar)
+    near_cut = abs(info["csum_before"] - g) <= BAND * g or abs(info["csum_at"] - g) <= BAND * g
+    extra = set()
+    if near_cut:
+        qb, kb = np.tril_indices(nb)
+        flat = qb.astype(np.int64) * nb + kb
+        order = np.lexsort((flat, -vals[qb, kb].astype(np.float64)))
+        K = info["kstar"]
+        for pos in (K - 1, K):
+            if 0 <= pos < len(order):
+                extra.add((int(qb[order[pos]]), int(kb[order[pos]])))
+    n_bad = 0
+    first = None
+    for qb_ in range(nb):
+        a, b = set(gpu_sets[qb_]), set(ores.sets[qb_])
+        for kb_ in a ^ b:
+            if exempt_val(vals[qb_, kb_]) or (qb_, kb_) in extra:
+                continue
+            n_bad += 1
+            if first is None:
+                first = (qb_, kb_, float(vals[qb_, kb_]), kb_ in a)
+    assert n_bad == 0, f"{where}: {n_bad} PE pairs differ outside the E4 band, first {first}, t*={float(tstar)}"
+
+
+def compare_attention(o_gpu: np.ndarray, o_ref: np.ndarray, rows=None, where=""):
+    if rows is not None:
+        o_gpu, o_ref = o_gpu[rows], o_ref[rows]
+    err = np.abs(o_gpu.astype(np.float64) - o_ref)
+    mx, mean = float(err.max()) if err.size else 0.0, float(err.mean()) if err.size else 0.0
+    assert mx <= ATTN_MAX_ABS and mean <= ATTN_MEAN_ABS, f"{where}: attention max-abs {mx:.3e} mean-abs {mean:.3e}"
+    return mx, mean
+
+
+def compare_scores(cs_gpu, pv_gpu, ps_gpu, ores: O.HeadResult, where=""):
+    assert abs(float(cs_gpu) - ores.c_struct) <= CS_ABS, f"{where}: C_struct {float(cs_gpu)} vs {ores.c_struct}"
+    for name, g, o in (("p_v", pv_gpu, ores.p_v), ("p_s", ps_gpu, ores.p_s)):
+        err = np.abs(np.asarray(g, np.float64) - o)
+        tol = P_ATOL + P_RTOL * np.abs(o)
+        bad = np.nonzero(err > tol)[0]
+        assert not len(bad), f"{where}: {name} blocks {bad[:10].tolist()} off: gpu {np.asarray(g)[bad[:5]]} oracle {o[bad[:5]]}"
+
+
+def qb_rows(qbs, block, n):
+    rows = []
+    for qb in qbs:
+        rows.extend(range(qb * block, min((qb + 1) * block, n)))
+    return np.asarray(rows, dtype=np.int64)

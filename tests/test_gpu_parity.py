@@ -1,0 +1,282 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Every case prints its name before touching the GPU so that a failing run names
+its case.  Inputs come from the seeded generators in workloads/ (generated on
+the GPU, copied to the host for the oracle) or from small hand-built tensors.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import crisp_oracle as O
+from tests import parity as PR
+from tests.helpers import to_f64
+from workloads import CONFIGS, custom_config, make_layer, stress_config
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _crisp():
+    from paper_2609_01925_amd import crisp
+    return crisp
+
+
+def _say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+def _rand(h, n, d=128, seed=0, scale=1.0):
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    return (torch.randn(h, n, d, generator=g) * scale).to(torch.bfloat16)
+
+
+def _oracle_params(p, block):
+    return O.Params(alpha=p.alpha, tau_proxy=p.tau_proxy, gamma=p.gamma, w_sink=p.w_sink, w_local=p.w_local,
+                    k_min_blocks=p.k_min_blocks, softmax_scale=p.softmax_scale)
+
+
+# ------------------------------------------------------------------ attention kernel
+
+@pytest.mark.parametrize("n,block,hq,hkv", [(4096, 128, 2, 1), (1000, 128, 4, 2), (200, 64, 2, 2), (64, 128, 1, 1),
+                                            (1, 128, 1, 1), (4160, 64, 8, 8), (2048, 128, 16, 4)])
+def test_dense_attention_matches_oracle(n, block, hq, hkv):
+    C = _crisp()
+    _say(f"dense n={n} B={block} hq={hq} hkv={hkv}")
+    q, k, v = _rand(hq, n, seed=1), _rand(hkv, n, seed=2), _rand(hkv, n, seed=3)
+    o = C.crisp_dense_attn(q.to(DEV), k.to(DEV), v.to(DEV), block)
+    torch.cuda.synchronize()
+    og = to_f64(o)
+    Q, K, V = to_f64(q), to_f64(k), to_f64(v)
+    G = hq // hkv
+    nb = O.n_blocks(n, block)
+    for h in range(hq):
+        ref = O.sparse_attention(Q[h], K[h // G], V[h // G], O.dense_causal_sets(nb), block, 1 / math.sqrt(128))
+        PR.compare_attention(og[h], ref, where=f"dense h{h}")
+
+
+def _random_lists(hq, nb, seed, density=0.3, junk=False):
+    rng = np.random.default_rng(seed)
+    cap = nb * (nb + 1) // 2
+    rp = np.zeros((hq, nb + 1), np.int32)
+    ci = np.zeros((hq, cap + (8 if junk else 0)), np.int32)
+    sets = []
+    for h in range(hq):
+        hs, off = [], 0
+        for qb in range(nb):
+            s = {0, qb} | {int(x) for x in np.nonzero(rng.random(qb + 1) < density)[0]}
+            s = sorted(s)
+            hs.append(s)
+            row = list(s)
+            if junk and qb % 3 == 1:
+                row = row + [qb + 1, -5, nb + 7]  # invalid entries the kernel must ignore
+            ci[h, off:off + len(row)] = row
+            rp[h, qb] = off
+            off += len(row)
+        rp[h, nb] = off
+        sets.append(hs)
+    return rp, ci, sets
+
+
+@pytest.mark.parametrize("n,block,junk", [(2048, 128, False), (1100, 64, False), (1500, 128, True)])
+def test_sparse_attention_on_given_lists(n, block, junk):
+    C = _crisp()
+    _say(f"sparse lists n={n} B={block} junk={junk}")
+    hq, hkv = 4, 2
+    nb = O.n_blocks(n, block)
+    q, k, v = _rand(hq, n, seed=4), _rand(hkv, n, seed=5), _rand(hkv, n, seed=6)
+    rp, ci, sets = _random_lists(hq, nb, seed=7, junk=junk)
+    o = C.crisp_sparse_attn(q.to(DEV), k.to(DEV), v.to(DEV), torch.from_numpy(rp).to(DEV),
+                            torch.from_numpy(ci).to(DEV), block)
+    torch.cuda.synchronize()
+    og = to_f64(o)
+    Q, K, V = to_f64(q), to_f64(k), to_f64(v)
+    for h in range(hq):
+        ref = O.sparse_attention(Q[h], K[h // 2], V[h // 2], sets[h], block, 1 / math.sqrt(128))
+        PR.compare_attention(og[h], ref, where=f"sparse h{h}")
+
+
+def test_full_lists_equal_dense_bitwise():
+    C = _crisp()
+    _say("full lists == dense, bitwise")
+    n, block, hq, hkv = 3000, 128, 4, 1
+    nb = O.n_blocks(n, block)
+    q, k, v = (_rand(hq, n, seed=8).to(DEV), _rand(hkv, n, seed=9).to(DEV), _rand(hkv, n, seed=10).to(DEV))
+    sets = O.dense_causal_sets(nb)
+    rp = np.zeros((hq, nb + 1), np.int32)
+    ci = np.zeros((hq, nb * (nb + 1) // 2), np.int32)
+    for h in range(hq):
+        off = 0
+        for qb in range(nb):
+            ci[h, off:off + qb + 1] = sets[qb]
+            rp[h, qb] = off
+            off += qb + 1
+        rp[h, nb] = off
+    o_s = C.crisp_sparse_attn(q, k, v, torch.from_numpy(rp).to(DEV), torch.from_numpy(ci).to(DEV), block)
+    o_d = C.crisp_dense_attn(q, k, v, block)
+    torch.cuda.synchronize()
+    assert torch.equal(o_s, o_d)
+
+
+def test_attention_custom_scale_and_empty_rows():
+    C = _crisp()
+    _say("custom scale, empty rows")
+    n, block = 512, 128
+    nb = O.n_blocks(n, block)
+    q, k, v = _rand(1, n, seed=11), _rand(1, n, seed=12), _rand(1, n, seed=13)
+    rp = np.array([[0, 1, 1, 3, 3]], np.int32)        # row 1 and row 3 have no entries
+    ci = np.zeros((1, nb * (nb + 1) // 2), np.int32)
+    ci[0, :3] = [0, 0, 2]
+    o = C.crisp_sparse_attn(q.to(DEV), k.to(DEV), v.to(DEV), torch.from_numpy(rp).to(DEV),
+                            torch.from_numpy(ci).to(DEV), block, softmax_scale=0.05)
+    torch.cuda.synchronize()
+    og = to_f64(o)[0]
+    assert not og[128:256].any() and not og[384:].any()
+    ref = O.sparse_attention(to_f64(q)[0], to_f64(k)[0], to_f64(v)[0], [[0], [], [0, 2], []], block, 0.05,
+                             qbs=[0, 2])
+    PR.compare_attention(og, ref, rows=PR.qb_rows([0, 2], block, n), where="scale 0.05")
+
+
+# ------------------------------------------------------------------ estimate / route / select
+
+def _run_stages(C, q, k, v, params, block):
+    cs, pv, ps = C.crisp_estimate(q, k, params, block)
+    route, rp, ci, dm = C.crisp_route_select(q, k, cs, pv, ps, params, block)
+    torch.cuda.synchronize()
+    return (cs.cpu().numpy(), pv.cpu().numpy(), ps.cpu().numpy(), route.cpu().numpy(), rp.cpu().numpy(),
+            ci.cpu().numpy(), dm.cpu().numpy())
+
+
+def _check_layer(C, cfg, params, heads=None, qbs_per_head=None, attn=True, where=""):
+    """Runs estimate + route/select (+ prefill) for the layer on the GPU and checks the given heads."""
+    block = cfg.block
+    q, k, v, specs = make_layer(cfg, device=DEV)
+    cs, pv, ps, route, rp, ci, dm = _run_stages(C, q, k, v, params, block)
+    nb = O.n_blocks(cfg.seq_len, block)
+    op = _oracle_params(params, block)
+    k_min = op.k_min(block)
+    heads = list(range(cfg.n_q_heads)) if heads is None else heads
+    o = C.crisp_prefill_attn(q, k, v, params, block) if attn else None
+    torch.cuda.synchronize()
+    Q = to_f64(q[heads]) if heads else None
+    G = cfg.group
+    groups = sorted(set(h // G for h in heads))
+    Kg = {g: to_f64(k[g]) for g in groups}
+    Vg = {g: to_f64(v[g]) for g in groups}
+    og = {h: to_f64(o[h]) for h in heads} if attn else {}
+    for i, h in enumerate(heads):
+        w = f"{where} h{h} ({specs[h].kind})"
+        res = O.crisp_head(Q[i], Kg[h // G], None, block, op, attend=False)
+        PR.compare_scores(cs[h], pv[h], ps[h], res, where=w)
+        assert route[h] == res.route, f"{w}: route gpu {route[h]} oracle {res.route} (C_struct {res.c_struct:.5f})"
+        gsets = PR.csr_to_sets(rp, ci, h, nb)
+        PR.check_structure(gsets, nb, where=w)
+        if res.route == O.ROUTE_VS:
+            PR.compare_vs(dm[h], res, op.alpha, k_min, where=w)
+            S_v = np.nonzero(dm[h, 0])[0].tolist()
+            S_s = np.nonzero(dm[h, 1])[0].tolist()
+            assert gsets == O.vs_block_sets(S_v, S_s, nb), f"{w}: CSR differs from the expansion of its own masks"
+        else:
+            assert not dm[h].any()
+            PR.compare_pe(gsets, res, op.gamma, where=w)
+        if attn:
+            qbs = list(range(nb)) if qbs_per_head is None else qbs_per_head(h, nb)
+            ref = O.sparse_attention(Q[i], Kg[h // G], Vg[h // G], gsets, block, op.scale(128), qbs=qbs)
+            PR.compare_attention(og[h], ref, rows=PR.qb_rows(qbs, block, cfg.seq_len), where=w + " attn(gpu lists)")
+            if gsets == res.sets:
+                pass  # identical sets: the comparison above is also the end-to-end one
+    return route
+
+
+def test_config0_full_path():
+    C = _crisp()
+    _say("config 0 (4k tiny) full path")
+    params = C.make_params(alpha=CONFIGS[0].alpha)
+    route = _check_layer(C, CONFIGS[0], params, where="c0")
+    assert route.tolist() == [0, 1]
+
+
+@pytest.mark.parametrize("n,block,hq,hkv", [(1000, 128, 2, 1), (777, 64, 4, 2), (130, 64, 2, 1), (100, 128, 2, 2),
+                                            (4096, 64, 4, 1)])
+def test_ragged_and_small_layers(n, block, hq, hkv):
+    C = _crisp()
+    _say(f"ragged layer n={n} B={block} hq={hq} hkv={hkv}")
+    cfg = custom_config(n, hq, hkv, block=block, config_id=100 + n % 97)
+    _check_layer(C, cfg, C.make_params(), where=f"n{n}")
+
+
+@pytest.mark.parametrize("tau", [0.0, 1.5])
+def test_forced_routes_and_params(tau):
+    C = _crisp()
+    _say(f"forced route tau={tau}")
+    cfg = custom_config(3000, 4, 2, block=128, config_id=131)
+    params = C.make_params(tau_proxy=tau, alpha=1.25, gamma=0.9, w_sink=64, w_local=200, k_min_blocks=3)
+    route = _check_layer(C, cfg, params, where=f"tau{tau}")
+    assert (route == (0 if tau == 0.0 else 1)).all()
+
+
+def test_config1_sampled():
+    C = _crisp()
+    _say("config 1 (32k Llama shape), 8 heads, sampled query blocks")
+    cfg = CONFIGS[1]
+    heads = [0, 1, 3, 8, 11, 17, 21, 31]
+    qsel = lambda h, nb: sorted({0, 1, nb // 3, nb // 2, nb - 2, nb - 1})
+    _check_layer(C, cfg, C.make_params(), heads=heads, qbs_per_head=qsel, where="c1")
+
+
+@pytest.mark.parametrize("alpha,block", [(0.5, 64), (1.0, 128), (2.0, 128), (1.0, 64)])
+def test_stress_config4(alpha, block):
+    C = _crisp()
+    _say(f"config 4 stress alpha={alpha} B={block}")
+    cfg = stress_config(alpha, block)
+    qsel = lambda h, nb: sorted({0, nb // 2, nb - 1})
+    _check_layer(C, cfg, C.make_params(alpha=alpha), heads=[0, 1, 2, 5, 13], qbs_per_head=qsel, where=cfg.name)
+
+
+def test_prefill_lists_match_stagewise():
+    """crisp_prefill_attn with caller lists reproduces the stage-by-stage calls exactly."""
+    C = _crisp()
+    _say("prefill lists == stages")
+    cfg = custom_config(5000, 4, 1, block=128, config_id=140)
+    q, k, v, _ = make_layer(cfg, device=DEV)
+    params = C.make_params()
+    cs, pv, ps, route, rp, ci, _ = _run_stages(C, q, k, v, params, 128)
+    o1, r2, rp2, ci2 = C.crisp_prefill_attn(q, k, v, params, 128, return_lists=True)
+    o2 = C.crisp_sparse_attn(q, k, v, torch.from_numpy(rp).to(DEV), torch.from_numpy(ci).to(DEV), 128)
+    o3 = C.crisp_prefill_attn(q, k, v, params, 128)
+    torch.cuda.synchronize()
+    assert np.array_equal(r2.cpu().numpy(), route) and np.array_equal(rp2.cpu().numpy(), rp)
+    nb = O.n_blocks(cfg.seq_len, 128)
+    for h in range(4):
+        assert PR.csr_to_sets(rp2.cpu().numpy(), ci2.cpu().numpy(), h, nb) == PR.csr_to_sets(rp, ci, h, nb)
+    assert torch.equal(o1, o2) and torch.equal(o1, o3)
+
+
+def test_run_to_run_determinism():
+    C = _crisp()
+    _say("determinism")
+    cfg = custom_config(6000, 8, 2, block=128, config_id=141)
+    q, k, v, _ = make_layer(cfg, device=DEV)
+    params = C.make_params()
+    a = _run_stages(C, q, k, v, params, 128)
+    b = _run_stages(C, q, k, v, params, 128)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_empty_layer_is_noop():
+    C = _crisp()
+    _say("empty layer")
+    q = torch.zeros(0, 16, 128, dtype=torch.bfloat16, device=DEV)
+    k = torch.zeros(1, 16, 128, dtype=torch.bfloat16, device=DEV)
+    o = C.crisp_dense_attn(q, k, k, 128)
+    assert o.shape == q.shape
+    q = torch.zeros(2, 0, 128, dtype=torch.bfloat16, device=DEV)
+    k = torch.zeros(1, 0, 128, dtype=torch.bfloat16, device=DEV)
+    C.crisp_prefill_attn(q, k, k, C.make_params(), 128)
+    torch.cuda.synchronize()
