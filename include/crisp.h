@@ -139,15 +139,22 @@ crisp_status crisp_route_select(const crisp_shape* shape, const crisp_params* pa
                                 int64_t col_cap_per_head, uint8_t* dir_mask_or_null,
                                 void* workspace, size_t workspace_bytes, crisp_stream stream);
 
+/* Host only.  Bytes of the optional crisp_sparse_attn workspace (256-byte aligned). */
+crisp_status crisp_sparse_workspace_size(const crisp_shape* shape, size_t* bytes);
+
 /* Stage 4 (Eq. 1): o[h][i] = sum_{j in J(i)} softmax_j(scale * q_i . k_j) v_j with
  * J(i) = {j <= i : j / B in row (i / B) of head h's list}.  Accepts caller-built
- * lists; entries outside [0, N_b) are ignored and row_ptr values are clamped to
+ * lists; entries outside [0, qb] are ignored and row_ptr values are clamped to
  * [0, col_cap_per_head], so a malformed list cannot cause an out-of-bounds access.
- * A row with no visible key gets o = 0.  softmax_scale 0 means 1/sqrt(d). */
+ * A row with no visible key gets o = 0.  softmax_scale 0 means 1/sqrt(d).
+ * workspace_or_null (crisp_sparse_workspace_size bytes) holds a longest-first
+ * work list that balances rows of very different lengths over the GPU; with
+ * NULL the rows are processed in a fixed order (same results, less balance). */
 crisp_status crisp_sparse_attn(const crisp_shape* shape, float softmax_scale,
                                const crisp_bf16* q, const crisp_bf16* k, const crisp_bf16* v,
                                const int32_t* row_ptr, const int32_t* col_idx,
-                               int64_t col_cap_per_head, crisp_bf16* o, crisp_stream stream);
+                               int64_t col_cap_per_head, crisp_bf16* o,
+                               void* workspace_or_null, size_t workspace_bytes, crisp_stream stream);
 
 /* Alg. 1: all stages on `stream`: estimate, route and select, sparse attention.
  * route_or_null, row_ptr_or_null and col_idx_or_null, if all three are given,

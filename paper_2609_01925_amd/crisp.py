@@ -51,7 +51,8 @@ def _load():
         "crisp_prefill_workspace_size": (ctypes.c_int, [sh, ctypes.POINTER(SZ)]),
         "crisp_estimate": (ctypes.c_int, [sh, pa, P, P, P, P, P, P, SZ, P]),
         "crisp_route_select": (ctypes.c_int, [sh, pa, P, P, P, P, P, P, P, P, I64, P, P, SZ, P]),
-        "crisp_sparse_attn": (ctypes.c_int, [sh, F, P, P, P, P, P, I64, P, P]),
+        "crisp_sparse_workspace_size": (ctypes.c_int, [sh, ctypes.POINTER(SZ)]),
+        "crisp_sparse_attn": (ctypes.c_int, [sh, F, P, P, P, P, P, I64, P, P, SZ, P]),
         "crisp_prefill_attn": (ctypes.c_int, [sh, pa, P, P, P, P, P, P, P, P, SZ, P]),
         "crisp_dense_attn": (ctypes.c_int, [sh, F, P, P, P, P, P]),
         "crisp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -66,7 +67,7 @@ def _load():
 
 lib = _load()
 EXPORTED = ("crisp_params_default", "crisp_col_capacity", "crisp_workspace_size", "crisp_prefill_workspace_size",
-            "crisp_estimate", "crisp_route_select", "crisp_sparse_attn", "crisp_prefill_attn", "crisp_dense_attn",
+            "crisp_sparse_workspace_size", "crisp_estimate", "crisp_route_select", "crisp_sparse_attn", "crisp_prefill_attn", "crisp_dense_attn",
             "crisp_status_string", "crisp_last_error")
 
 
@@ -108,6 +109,12 @@ def crisp_workspace_size(shape: CrispShape) -> int:
 def crisp_prefill_workspace_size(shape: CrispShape) -> int:
     b = ctypes.c_size_t()
     _check(lib.crisp_prefill_workspace_size(ctypes.byref(shape), ctypes.byref(b)), "crisp_prefill_workspace_size")
+    return int(b.value)
+
+
+def crisp_sparse_workspace_size(shape: CrispShape) -> int:
+    b = ctypes.c_size_t()
+    _check(lib.crisp_sparse_workspace_size(ctypes.byref(shape), ctypes.byref(b)), "crisp_sparse_workspace_size")
     return int(b.value)
 
 
@@ -169,13 +176,20 @@ def crisp_route_select(q: torch.Tensor, k: torch.Tensor, c_struct: torch.Tensor,
 
 def crisp_sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, row_ptr: torch.Tensor,
                       col_idx: torch.Tensor, block: int = 128, softmax_scale: float = 0.0,
-                      out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Stage 4 over caller-given CSR lists -> o bf16 [H_q, n, d]."""
+                      out: Optional[torch.Tensor] = None, balance: bool = True,
+                      ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Stage 4 over caller-given CSR lists -> o bf16 [H_q, n, d].  balance=False passes no
+    workspace (fixed row order)."""
     _inputs(q, k, v)
     sh = shape_of(q, k, block)
     o = torch.empty_like(q) if out is None else out
+    if balance and ws is None:
+        ws = torch.empty(max(crisp_sparse_workspace_size(sh), 256), dtype=torch.uint8, device=q.device)
+    if not balance:
+        ws = None
     _check(lib.crisp_sparse_attn(ctypes.byref(sh), softmax_scale, _ptr(q), _ptr(k), _ptr(v), _ptr(row_ptr),
-                                 _ptr(col_idx), col_idx.shape[1], _ptr(o), _stream(q.device)), "crisp_sparse_attn")
+                                 _ptr(col_idx), col_idx.shape[1], _ptr(o), _ptr(ws), 0 if ws is None else ws.numel(),
+                                 _stream(q.device)), "crisp_sparse_attn")
     return o
 
 

@@ -110,6 +110,7 @@ WsLayout ws_layout(const Dims& d) {
   L.rhist = take(hq * 2048 * sizeof(unsigned long long));
   L.rstate = take(hq * 32);
   L.rowinfo = take(hq * nb * 4 * sizeof(int32_t));
+  L.sched = take(attn_schedule_bytes(d));
   L.total = off;
   return L;
 }
@@ -236,10 +237,18 @@ crisp_status crisp_route_select(const crisp_shape* shape, const crisp_params* pa
                     "crisp_route_select launch");
 }
 
+crisp_status crisp_sparse_workspace_size(const crisp_shape* shape, size_t* bytes) {
+  Dims d;
+  CHECK(check_shape(shape, &d));
+  if (!bytes) return fail(CRISP_EINVAL, "bytes is null");
+  *bytes = align256(attn_schedule_bytes(d));
+  return CRISP_OK;
+}
+
 crisp_status crisp_sparse_attn(const crisp_shape* shape, float softmax_scale, const crisp_bf16* q,
                                const crisp_bf16* k, const crisp_bf16* v, const int32_t* row_ptr,
                                const int32_t* col_idx, int64_t col_cap_per_head, crisp_bf16* o,
-                               crisp_stream stream) {
+                               void* workspace_or_null, size_t workspace_bytes, crisp_stream stream) {
   Dims d;
   CHECK(check_shape(shape, &d));
   if (!(softmax_scale >= 0.f) || !isfinite(softmax_scale))
@@ -252,8 +261,13 @@ crisp_status crisp_sparse_attn(const crisp_shape* shape, float softmax_scale, co
   CHECK(check_ptr(row_ptr, 4, "row_ptr"));
   CHECK(check_ptr(col_idx, 4, "col_idx"));
   if (col_cap_per_head < 0) return fail(CRISP_EINVAL, "col_cap_per_head must be >= 0");
+  if (workspace_or_null) {
+    CHECK(check_ptr(workspace_or_null, 256, "workspace"));
+    if (workspace_bytes < attn_schedule_bytes(d))
+      return fail(CRISP_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, attn_schedule_bytes(d));
+  }
   return hip_status(launch_attn(d, scale_of(softmax_scale), q, k, v, row_ptr, col_idx, col_cap_per_head, false, o,
-                                (hipStream_t)stream),
+                                workspace_or_null, (hipStream_t)stream),
                     "crisp_sparse_attn launch");
 }
 
@@ -268,7 +282,7 @@ crisp_status crisp_dense_attn(const crisp_shape* shape, float softmax_scale, con
   CHECK(check_ptr(k, 16, "k"));
   CHECK(check_ptr(v, 16, "v"));
   CHECK(check_ptr(o, 16, "o"));
-  return hip_status(launch_attn(d, scale_of(softmax_scale), q, k, v, nullptr, nullptr, 0, true, o,
+  return hip_status(launch_attn(d, scale_of(softmax_scale), q, k, v, nullptr, nullptr, 0, true, o, nullptr,
                                 (hipStream_t)stream),
                     "crisp_dense_attn launch");
 }
@@ -311,7 +325,8 @@ crisp_status crisp_prefill_attn(const crisp_shape* shape, const crisp_params* pa
   CHECK(hip_status(launch_select(d, scale, params->alpha, params->tau_proxy, params->gamma, kmin_of(params, d.B), q,
                                  k, cs, pv, ps, route, rp, ci, d.cap, nullptr, ws, st),
                    "crisp_prefill_attn select launch"));
-  return hip_status(launch_attn(d, scale, q, k, v, rp, ci, d.cap, false, o, st), "crisp_prefill_attn attention launch");
+  return hip_status(launch_attn(d, scale, q, k, v, rp, ci, d.cap, false, o, ws + L.sched, st),
+                    "crisp_prefill_attn attention launch");
 }
 
 const char* crisp_status_string(crisp_status s) {

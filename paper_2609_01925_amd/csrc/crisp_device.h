@@ -20,6 +20,7 @@ namespace crisp {
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(4 * sizeof(short)))) short i16x4;
@@ -45,6 +46,31 @@ __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
 // Value held by lane l ^ 32.
 __device__ __forceinline__ float swap_halves(float x) { return __shfl_xor(x, 32); }
+
+// v_permlane32_swap exchanges the upper half-wave of one operand with the lower
+// half-wave of the other; with both operands = x every lane receives the pair
+// {x[l], x[l ^ 32]} (in some order), so a commutative combine of the pair gives
+// the same value in both lanes of a query.
+__device__ __forceinline__ float half_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float half_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Round-to-nearest-even pair conversion (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ bf16x2 pack_bf16(float a, float b) {
+  bf16x2 r = {(__bf16)a, (__bf16)b};
+  return r;
+}
+
+// acc + p[0] + p[1] with the bf16 values (v_dot2c_f32_bf16 against ones).
+__device__ __forceinline__ float dot2_bf16_sum(bf16x2 p, float acc) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(p, ones, acc, false);
+}
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 

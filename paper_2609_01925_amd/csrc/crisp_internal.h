@@ -24,13 +24,17 @@ EstSplit est_split(const Dims& d);
 
 // Workspace layout (byte offsets; every region 256-byte aligned).
 struct WsLayout {
-  size_t rowstat, rowfinal, parts, masks, qbar, kbar, atil, rhist, rstate, rowinfo, total;
+  size_t rowstat, rowfinal, parts, masks, qbar, kbar, atil, rhist, rstate, rowinfo, sched, total;
 };
 WsLayout ws_layout(const Dims& d);
 
+// Bytes of the longest-first work list used by the persistent sparse kernel.
+size_t attn_schedule_bytes(const Dims& d);
+
+// sched == nullptr: static grid (dense, or sparse without a work list).
 hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                        const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, bool dense,
-                       uint16_t* o, hipStream_t stream);
+                       uint16_t* o, void* sched, hipStream_t stream);
 
 hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, const uint16_t* q,
                            const uint16_t* k, float* c_struct, float* p_v, float* p_s, char* ws,

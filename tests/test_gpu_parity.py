@@ -93,7 +93,10 @@ def test_sparse_attention_on_given_lists(n, block, junk):
     rp, ci, sets = _random_lists(hq, nb, seed=7, junk=junk)
     o = C.crisp_sparse_attn(q.to(DEV), k.to(DEV), v.to(DEV), torch.from_numpy(rp).to(DEV),
                             torch.from_numpy(ci).to(DEV), block)
+    o_fixed = C.crisp_sparse_attn(q.to(DEV), k.to(DEV), v.to(DEV), torch.from_numpy(rp).to(DEV),
+                                  torch.from_numpy(ci).to(DEV), block, balance=False)
     torch.cuda.synchronize()
+    assert torch.equal(o, o_fixed)   # the work order never changes a result
     og = to_f64(o)
     Q, K, V = to_f64(q), to_f64(k), to_f64(v)
     for h in range(hq):
