@@ -38,10 +38,10 @@ class CrispError(RuntimeError):
         self.status = status
 
 
-def _load():
-    if not os.path.exists(_LIB_PATH):
-        raise ImportError(f"libcrisp.so not built at {_LIB_PATH}; run `python -m paper_2609_01925_amd.build`")
-    lib = ctypes.CDLL(_LIB_PATH)
+def _load(path: str = _LIB_PATH):
+    if not os.path.exists(path):
+        raise ImportError(f"libcrisp.so not built at {path}; run `python -m paper_2609_01925_amd.build`")
+    lib = ctypes.CDLL(path)
     P, F, I32, I64, SZ = ctypes.c_void_p, ctypes.c_float, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     sh, pa = ctypes.POINTER(CrispShape), ctypes.POINTER(CrispParams)
     sig = {

@@ -2,9 +2,8 @@
 // selected key blocks) and the dense causal baseline, for gfx950.
 //
 // A workgroup computes one (query head, query block) unit at a time: BQ = B
-// query rows, BQ / 32 waves, each wave owning 32 query rows.  Key blocks are
-// streamed in tiles of 64 keys through double-buffered, swizzled LDS.  Per tile
-// and wave:
+// query rows, BQ / 32 waves, each wave owning 32 query rows.  Keys are
+// streamed in tiles of 64.  Per tile and wave:
 //   S^T (64 keys x 32 queries) = K_tile Q^T      16 x v_mfma_f32_32x32x16_bf16
 //   online softmax in fp32 (exp2, log2(e) folded into the scale)
 //   O^T (128 d x 32 queries) += V^T P^T          16 x v_mfma_f32_32x32x16_bf16
@@ -13,8 +12,15 @@
 // layout of S^T is reused directly as the B operand of the PV product; V^T
 // operands come from LDS through ds_read_b64_tr_b16, which transposes 4 keys x
 // 16 dims per 16-lane group, so V needs no transposed copy.
-// The score MFMAs of tile j+1 are issued before the softmax of tile j, so
-// matrix cores and vector ALU can overlap within a wave.
+//
+// K and V tiles move from global memory straight into LDS with LDS-DMA loads
+// (buffer_load ... lds), two 2-deep rings (K, V) of 16 KB stages: 64 KB per
+// workgroup, so two workgroups share a CU and every SIMD interleaves two waves,
+// which hides the latency of one wave's LDS reads and MFMA chains behind the
+// other's work.  At the top of iteration j the DMAs for K(j+2) and V(j+1) go into
+// the stages freed by iteration j-1, so each has a full iteration to land.
+// Within a wave the order is softmax(j), scores(j+1), PV(j): the matrix cores of a
+// SIMD are kept busy by the other resident wave while this one does softmax.
 // The running max is only raised when a row's max grows by more than 2^8
 // (log2 units): until then P may exceed 1 by at most 2^8, which fp32 and bf16
 // hold exactly as well, and the O accumulators are left untouched.
@@ -29,9 +35,10 @@ namespace crisp {
 
 namespace {
 
-constexpr int BK = 64;                  // keys per tile
-constexpr int kTileBytes = BK * 256;    // one K or V tile: 64 rows x 128 bf16
-constexpr float kLazyRescale = 8.0f;    // log2 growth of a row max tolerated before rescaling
+constexpr int BK = 64;                       // keys per tile
+constexpr int kTileBytes = BK * 256;         // one K or V tile: 64 rows x 128 bf16
+constexpr int kRingBytes = 2 * kTileBytes;   // one ring (K or V): 2 stages
+constexpr float kLazyRescale = 8.0f;         // log2 growth of a row max tolerated before rescaling
 constexpr int kCostBuckets = 8192;
 
 struct AttnArgs {
@@ -81,47 +88,13 @@ __device__ __forceinline__ bool map_unit(const AttnArgs& a, int bid, int& h, int
   return true;
 }
 
-template <int NT>
-struct TileRegs {
-  static constexpr int N = (BK * 16) / NT;  // 16-byte chunks per thread per tile
-  u32x4 k[N];
-  u32x4 v[N];
-};
-
-template <int NT>
-__device__ __forceinline__ void load_tile(TileRegs<NT>& t, const uint16_t* Kg, const uint16_t* Vg, int key0, int n,
-                                          int tid) {
-  const int c = tid & 15;
-#pragma unroll
-  for (int i = 0; i < TileRegs<NT>::N; ++i) {
-    const int r = (tid >> 4) + (NT / 16) * i;
-    const int key = key0 + r;
-    if (key < n) {
-      t.k[i] = *reinterpret_cast<const u32x4*>(Kg + (size_t)key * kHeadDim + 8 * c);
-      t.v[i] = *reinterpret_cast<const u32x4*>(Vg + (size_t)key * kHeadDim + 8 * c);
-    } else {
-      t.k[i] = u32x4{0, 0, 0, 0};
-      t.v[i] = u32x4{0, 0, 0, 0};
-    }
-  }
-}
-
-template <int NT>
-__device__ __forceinline__ void store_tile(const TileRegs<NT>& t, char* kbuf, char* vbuf, int tid) {
-  const int c = tid & 15;
-#pragma unroll
-  for (int i = 0; i < TileRegs<NT>::N; ++i) {
-    const int r = (tid >> 4) + (NT / 16) * i;
-    const int off = lds_off(r, 8 * c);
-    *reinterpret_cast<u32x4*>(kbuf + off) = t.k[i];
-    *reinterpret_cast<u32x4*>(vbuf + off) = t.v[i];
-  }
-}
+#if defined(__HIP_DEVICE_COMPILE__)
 
 // Per-lane LDS byte offsets of the MFMA operand reads, fixed for the whole kernel.
-// K (A operand of S^T): row l % 32 (+32 per key sub-block, an immediate), chunk
-// 2 kk + l / 32.  V^T (A operand of O^T, transposing reads): two reads per MFMA,
-// rows r0 and r0 + 8 (+16 ss + 32 mb, immediates), dims 32 db + 16 (grp & 1) + 4 (jj & 3).
+// K (A operand of S^T): row l % 32 (+32 rows for the second key sub-block, an
+// immediate), chunk 2 kk + l / 32.  V^T (A operand of O^T, transposing reads):
+// two reads per MFMA, rows r0 and r0 + 8 (+16 ss + 32 mb rows, immediates),
+// dims 32 db + 16 (grp & 1) + 4 (jj & 3).
 struct Offsets {
   int k[8];
   int v[4][2];
@@ -139,6 +112,72 @@ __device__ __forceinline__ void make_offsets(Offsets& off, int l) {
     off.v[db][1] = lds_off(row + 8, col);
   }
 }
+
+// Tile fetch: a 64-key x 128-dim tile goes straight from global memory into an
+// LDS stage (buffer_load ... lds, 16 bytes per lane, lane t writing LDS base +
+// 16 t).  Instruction (i, w') fills rows 16 i + 4 w' .. +3; lane t supplies row
+// 16 i + 4 w' + t / 16, physical chunk t % 16, so it loads logical chunk
+// (t % 16) ^ swz(row) -- the swizzle only depends on row % 16, so the per-lane
+// source offset is the same for every i (i moves the scalar offset).  Keys at or
+// past n lie outside the buffer range and read as 0.
+template <int NW>
+struct Fetch {
+  static constexpr int kPerWave = 4 / NW;  // w' values per wave
+  int voff[kPerWave];
+};
+
+template <int NW>
+__device__ __forceinline__ void make_fetch(Fetch<NW>& f, int w, int t) {
+#pragma unroll
+  for (int x = 0; x < Fetch<NW>::kPerWave; ++x) {
+    const int wp = w + NW * x;
+    const int row = 4 * wp + (t >> 4);
+    f.voff[x] = row * 256 + (((t & 15) ^ swz(row)) << 4);
+  }
+}
+
+typedef __attribute__((__vector_size__(4 * sizeof(int)))) int i32x4;
+
+// Buffer descriptor (V#) over one KV head's [n, 128] bf16 tensor; num_records
+// bounds the byte range, so reads at or past key n return 0.
+__device__ __forceinline__ i32x4 tensor_rsrc(const uint16_t* base, int n) {
+  const unsigned long long p = (unsigned long long)base;
+  return i32x4{(int)(unsigned)p, (int)(unsigned)(p >> 32), n * 256, 0x00020000};
+}
+
+// One LDS-DMA load: 16 bytes per lane from rsrc + voff + soff into lds_base + 16 * lane.
+// Issued as inline assembly so that the compiler's wait-count pass does not treat
+// every later LDS read as dependent on it; the kernel waits explicitly (wait_dma)
+// and publishes the tile with a workgroup barrier before any wave reads it.
+__device__ __forceinline__ void dma16(i32x4 rsrc, int voff, int soff, const char* lds_base) {
+  const int m0 = __builtin_amdgcn_readfirstlane((int)(size_t)lds_base);
+  const int so = __builtin_amdgcn_readfirstlane(soff);
+#ifdef CRISP_EXP_BUILTIN_DMA
+  const unsigned long long base = ((unsigned long long)(unsigned)rsrc[1] << 32) | (unsigned)rsrc[0];
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(__builtin_amdgcn_make_buffer_rsrc((void*)base, 0, rsrc[2], rsrc[3]),
+      (__attribute__((address_space(3))) void*)lds_base, 16, voff, so, 0, 0);
+#else
+  // The scalar offset comes from v_readfirstlane (a VALU write to an SGPR), which a
+  // VMEM instruction may only read after 5 wait states, and M0 is written just
+  // before; the compiler cannot see these reads inside the assembly, so the wait
+  // states are part of it.
+  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rsrc), "s"(so), "{m0}"(m0));
+#endif
+}
+
+// One tensor's tile into one LDS stage.
+template <int NW>
+__device__ __forceinline__ void fetch_tile(const Fetch<NW>& f, i32x4 rsrc, char* stage, int key0, int w) {
+#pragma unroll
+  for (int x = 0; x < Fetch<NW>::kPerWave; ++x) {
+    const int wp = w + NW * x;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) dma16(rsrc, f.voff[x], (key0 + 16 * i) * 256, stage + (16 * i + 4 * wp) * 256);
+  }
+}
+
+// Waits until every LDS-DMA load of this wave has landed (s_waitcnt vmcnt(0)).
+__device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
 
 // S^T for one tile: s[mb] covers keys 32 * mb + (C-layout rows), queries = lane column.
 // Rows 32..63 have the same swizzle as rows 0..31, so sub-block 1 is +32 rows.
@@ -166,28 +205,46 @@ __device__ __forceinline__ void mask_tile(f32x16 (&s)[2], int key0, int qabs, bo
     }
 }
 
+// P = exp2(s * c - m c) as bf16 MFMA operands, row sums accumulated in l.
+__device__ __forceinline__ void softmax_p(const f32x16& s, float c, float mc, bf16x8 (&pb)[2], float& l) {
+#pragma unroll
+  for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+    for (int e = 0; e < 8; e += 2) {
+      const float p0 = fast_exp2(__builtin_fmaf(s[8 * hh + e], c, -mc));
+      const float p1 = fast_exp2(__builtin_fmaf(s[8 * hh + e + 1], c, -mc));
+      const bf16x2 pr = pack_bf16(p0, p1);
+      pb[hh][e] = pr[0];
+      pb[hh][e + 1] = pr[1];
+      l = dot2_bf16_sum(pr, l);
+    }
+}
+
+// O^T += V^T P^T for one 32-key sub-block of the tile.
+__device__ __forceinline__ void pv_sub(const char* vbuf, const Offsets& off, const bf16x8 (&pb)[2], f32x16 (&o)[4]) {
+#pragma unroll
+  for (int ss = 0; ss < 2; ++ss) {
+    const char* vb = vbuf + 16 * ss * 256;
+#pragma unroll
+    for (int db = 0; db < 4; ++db) {
+      const bf16x8 av = cat(lds_read_tr(vb, off.v[db][0]), lds_read_tr(vb, off.v[db][1]));
+      o[db] = mfma32(av, pb[ss], o[db]);
+    }
+  }
+}
+
 // One (head, query block) unit.
 template <int BQ, bool DENSE>
-__device__ __forceinline__ void attn_unit(const AttnArgs& a, int h, int qb, char* smem, const Offsets& off, int tid) {
-  constexpr int NT = BQ * 2;
+__device__ __forceinline__ void attn_unit(const AttnArgs& a, int h, int qb, char* smem, const Offsets& off,
+                                          const Fetch<BQ / 32>& fe, int tid) {
+  constexpr int NW = BQ / 32;
   constexpr int TPB = BQ / BK;  // tiles per key block
   const int l = tid & 63, w = tid >> 6;
   const int g = h / a.G;
   const int q0 = qb * BQ;
   const int qabs = q0 + 32 * w + (l & 31);
-  const uint16_t* Kg = a.k + (size_t)g * a.n * kHeadDim;
-  const uint16_t* Vg = a.v + (size_t)g * a.n * kHeadDim;
-
-  bf16x8 qf[8];
-  {
-    const uint16_t* qrow = a.q + ((size_t)h * a.n + (qabs < a.n ? qabs : 0)) * kHeadDim;
-#pragma unroll
-    for (int kk = 0; kk < 8; ++kk) {
-      u32x4 raw = *reinterpret_cast<const u32x4*>(qrow + 16 * kk + 8 * (l >> 5));
-      if (qabs >= a.n) raw = u32x4{0, 0, 0, 0};
-      qf[kk] = __builtin_bit_cast(bf16x8, raw);
-    }
-  }
+  const i32x4 rk = tensor_rsrc(a.k + (size_t)g * a.n * kHeadDim, a.n);
+  const i32x4 rv = tensor_rsrc(a.v + (size_t)g * a.n * kHeadDim, a.n);
 
   int beg = 0, cnt;
   const int32_t* cols = nullptr;
@@ -205,6 +262,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int h, int qb, char
   }
   const int T = cnt * TPB;
 
+  // tile j -> first key, validity (entry in [0, qb]) and whether it needs the mask
   auto tile_key0 = [&](int j, bool& valid, bool& needs_mask) -> int {
     int kb = DENSE ? j / TPB : cols[beg + j / TPB];
     valid = kb >= 0 && kb <= qb;
@@ -212,6 +270,25 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int h, int qb, char
     needs_mask = !valid || kb == qb;
     return kb * BQ + (j % TPB) * BK;
   };
+  auto key0_of = [&](int j) {
+    bool vv, mm;
+    return tile_key0(j, vv, mm);
+  };
+  char* kring = smem;
+  char* vring = smem + kRingBytes;
+  auto kst = [&](int j) { return kring + (j & 1) * kTileBytes; };
+  auto vst = [&](int j) { return vring + (j & 1) * kTileBytes; };
+
+  bf16x8 qf[8];
+  {
+    const uint16_t* qrow = a.q + ((size_t)h * a.n + (qabs < a.n ? qabs : 0)) * kHeadDim;
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) {
+      u32x4 raw = *reinterpret_cast<const u32x4*>(qrow + 16 * kk + 8 * (l >> 5));
+      if (qabs >= a.n) raw = u32x4{0, 0, 0, 0};
+      qf[kk] = __builtin_bit_cast(bf16x8, raw);
+    }
+  }
 
   f32x16 o[4];
 #pragma unroll
@@ -219,43 +296,31 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int h, int qb, char
   float m_run = -__builtin_inff(), l_run = 0.f;
 
   if (T > 0) {
-    TileRegs<NT> regs;
-    bool v0, m0;
-    const int k0 = tile_key0(0, v0, m0);
-    load_tile<NT>(regs, Kg, Vg, k0, a.n, tid);
-    store_tile<NT>(regs, smem, smem + kTileBytes, tid);
-    bool vn = false, mn = false;
-    int kn = 0;
-    if (T > 1) {
-      kn = tile_key0(1, vn, mn);
-      load_tile<NT>(regs, Kg, Vg, kn, a.n, tid);
-    }
+    // prologue: K(0), V(0), K(1)
+    fetch_tile<NW>(fe, rk, kst(0), key0_of(0), w);
+    fetch_tile<NW>(fe, rv, vst(0), key0_of(0), w);
+    if (T > 1) fetch_tile<NW>(fe, rk, kst(1), key0_of(1), w);
+    wait_dma();
     __syncthreads();
     f32x16 s[2];
-    qk_tile(smem, qf, off, s);
-    if (m0) mask_tile(s, k0, qabs, v0, l);
+    qk_tile(kst(0), qf, off, s);
 
     for (int j = 0; j < T; ++j) {
-      const int cur = j & 1, nxt = cur ^ 1;
-      char* kcur = smem + cur * 2 * kTileBytes;
-      char* knxt = smem + nxt * 2 * kTileBytes;
-      __syncthreads();  // every wave is done with tile j - 1 (held in buffer nxt)
       const bool has_next = j + 1 < T;
-      const bool vnext = vn, mnext = mn;
-      const int knext = kn;
-      if (has_next) store_tile<NT>(regs, knxt, knxt + kTileBytes, tid);
+      // K(j+1) and V(j), issued one iteration ago (or in the prologue), have landed
+      // for every wave, and every wave is done with the stages of K(j) (scored in
+      // the previous iteration or the prologue) and V(j-1), which are refilled next.
+      wait_dma();
       __syncthreads();
-      if (j + 2 < T) {
-        kn = tile_key0(j + 2, vn, mn);
-        load_tile<NT>(regs, Kg, Vg, kn, a.n, tid);
-      }
-      f32x16 sn[2];
-      if (has_next) {
-        qk_tile(knxt, qf, off, sn);
-        if (mnext) mask_tile(sn, knext, qabs, vnext, l);
+      if (j + 2 < T) fetch_tile<NW>(fe, rk, kst(j + 2), key0_of(j + 2), w);
+      if (has_next) fetch_tile<NW>(fe, rv, vst(j + 1), key0_of(j + 1), w);
+      {
+        bool vj, mj;
+        const int kj = tile_key0(j, vj, mj);
+        if (mj) mask_tile(s, kj, qabs, vj, l);
       }
 
-      // online softmax of tile j (row max raised lazily)
+      // row max of tile j; the running max is raised only when it grows by > 2^8
       float mx = -__builtin_inff();
 #pragma unroll
       for (int i = 0; i < 16; i += 2)
@@ -273,40 +338,13 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int h, int qb, char
         m_run = m_new;
       }
       const float mc = m_run == -__builtin_inff() ? 0.f : m_run * a.c;
-      bf16x8 pb[2][2];
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          float p[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) p[e] = fast_exp2(__builtin_fmaf(s[mb][8 * hh + e], a.c, -mc));
-#pragma unroll
-          for (int e = 0; e < 8; e += 2) {
-            const bf16x2 pr = pack_bf16(p[e], p[e + 1]);
-            pb[mb][hh][e] = pr[0];
-            pb[mb][hh][e + 1] = pr[1];
-            l_run = dot2_bf16_sum(pr, l_run);
-          }
-        }
 
-      // O^T += V^T P^T
-      const char* vcur = kcur + kTileBytes;
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int ss = 0; ss < 2; ++ss) {
-          const char* vb = vcur + (32 * mb + 16 * ss) * 256;
-#pragma unroll
-          for (int db = 0; db < 4; ++db) {
-            const bf16x8 av = cat(lds_read_tr(vb, off.v[db][0]), lds_read_tr(vb, off.v[db][1]));
-            o[db] = mfma32(av, pb[mb][ss], o[db]);
-          }
-        }
-      if (has_next) {
-        s[0] = sn[0];
-        s[1] = sn[1];
-      }
+      bf16x8 pb0[2], pb1[2];
+      softmax_p(s[0], a.c, mc, pb0, l_run);
+      softmax_p(s[1], a.c, mc, pb1, l_run);
+      if (has_next) qk_tile(kst(j + 1), qf, off, s);  // S(j) is consumed: reuse its registers
+      pv_sub(vst(j), off, pb0, o);
+      pv_sub(vst(j) + 32 * 256, off, pb1, o);
     }
   }
 
@@ -328,29 +366,42 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int h, int qb, char
   }
 }
 
+#endif  // __HIP_DEVICE_COMPILE__
+
+#ifdef CRISP_EXP_ONE_WAVE
+#define CRISP_WAVES_PER_EU 1
+#else
+#define CRISP_WAVES_PER_EU 2
+#endif
 template <int BQ, bool DENSE>
-__global__ __launch_bounds__(BQ * 2) void attn_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * 2 * kTileBytes];
+__global__ __launch_bounds__(BQ * 2, CRISP_WAVES_PER_EU) void attn_kernel(AttnArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  // The rings are the kernel's only LDS object, so they start at LDS address 0
+  // (LDS-DMA destinations are then 1 KB aligned); the work-queue slot sits after them.
+  __shared__ __attribute__((aligned(1024))) char smem[2 * kRingBytes + 16];
   const int tid = threadIdx.x;
   Offsets off;
   make_offsets(off, tid & 63);
+  Fetch<BQ / 32> fe;
+  make_fetch<BQ / 32>(fe, tid >> 6, tid & 63);
   if (DENSE || a.order == nullptr) {
     int h, qb;
     if (!map_unit(a, blockIdx.x, h, qb)) return;
-    attn_unit<BQ, DENSE>(a, h, qb, smem, off, tid);
+    attn_unit<BQ, DENSE>(a, h, qb, smem, off, fe, tid);
     return;
   }
-  __shared__ int s_unit;
+  int* s_unit = reinterpret_cast<int*>(smem + 2 * kRingBytes);
   const int total = a.hq * a.nb;
   for (;;) {
-    __syncthreads();  // the previous unit is done with LDS and s_unit
-    if (tid == 0) s_unit = atomicAdd(a.counter, 1);
+    __syncthreads();  // the previous unit is done with LDS and the unit slot
+    if (tid == 0) *s_unit = atomicAdd(a.counter, 1);
     __syncthreads();
-    const int u = s_unit;
+    const int u = *s_unit;
     if (u >= total) break;
     const int unit = a.order[u];
-    attn_unit<BQ, DENSE>(a, unit / a.nb, unit % a.nb, smem, off, tid);
+    attn_unit<BQ, DENSE>(a, unit / a.nb, unit % a.nb, smem, off, fe, tid);
   }
+#endif  // __HIP_DEVICE_COMPILE__
 }
 
 // Longest-first work list for the persistent sparse kernel: a counting sort of
