@@ -37,6 +37,12 @@ def parse():
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--steps-512k", type=int, default=2)
     ap.add_argument("--config", type=int, default=2, help="headline config id (2 = 128k Llama GQA layer)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain 1 GiB device copy, the reference for rocprofv3 byte counters")
+    ap.add_argument("--summarize", metavar="ROCPROF_DIR",
+                    help="summarize rocprofv3 output under ROCPROF_DIR into profiles/ and exit (no GPU)")
+    ap.add_argument("--label", default="attn_128k", help="file stem for --summarize")
+    ap.add_argument("--command", default="", help="the profiling command, recorded by --summarize")
     return ap.parse_args()
 
 
@@ -198,21 +204,103 @@ def cpu_baseline(cfg, res, budget_s=25.0):
     }
 
 
-def attn_traffic(kernel_src_hash, workload):
-    """HBM traffic per launch from the committed rocprofv3 counter summary, if it was taken
-    on the current attention kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "sparse_attn_pmc.json")
+def attn_traffic(kernel_src_hash, label="sparse_attn_128k_pmc"):
+    """HBM bytes (fetch + write) per launch of the sparse attention kernel from the committed
+    rocprofv3 counter summary, if it was taken on the current attention kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", label + ".md")
     if not os.path.exists(path):
         return None
-    with open(path) as f:
-        rec = json.load(f)
-    if rec.get("attn_src_sha") != kernel_src_hash or rec.get("workload") != workload:
+    text = open(path).read()
+    if f"attn.hip sha256[:16]: {kernel_src_hash}" not in text:
         return None
-    return rec.get("hbm_bytes_per_launch")
+    for line in text.splitlines():
+        if "PMC_RECORD " in line:
+            rec = json.loads(line.split("PMC_RECORD ", 1)[1].rstrip("`"))
+            f_, w_ = rec.get("sparse_attn_FETCH_SIZE_bytes"), rec.get("sparse_attn_WRITE_SIZE_bytes")
+            if f_ is not None and w_ is not None:
+                return f_ + w_
+    return None
+
+
+COPY_BYTES = 1 << 30
+
+
+def copy_calibration():
+    """A plain device-to-device copy of COPY_BYTES: its FETCH_SIZE / WRITE_SIZE give the
+    scale from counter units to bytes."""
+    import torch
+    x = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    torch.mul(x, 2.0, out=y)   # one elementwise kernel: reads and writes COPY_BYTES
+    torch.cuda.synchronize()
+    del x, y
+
+
+def summarize(args):
+    """Turns rocprofv3 csv output (kernel trace stats or counter collection) into a short
+    markdown summary under profiles/."""
+    import csv
+    import glob
+    import statistics
+    root = args.summarize
+    out = []
+    out.append(f"# {args.label}\n")
+    out.append(f"Command: `{args.command}`\n")
+    out.append(f"attn.hip sha256[:16]: {src_hash(os.path.join(ROOT, 'paper_2609_01925_amd', 'csrc', 'attn.hip'))}\n")
+    stats = sorted(glob.glob(os.path.join(root, "**", "*kernel_stats.csv"), recursive=True))
+    if stats:
+        out.append("\n## Kernel time (rocprofv3 --kernel-trace --stats)\n")
+        out.append("| kernel | calls | avg us | min us | max us | total ms |\n|---|---|---|---|---|---|\n")
+        for r in csv.DictReader(open(stats[0])):
+            name = r["Name"]
+            if "crisp" not in name:
+                continue
+            short = name.replace("crisp::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
+            out.append(f"| {short} | {r['Calls']} | {float(r['AverageNs'])/1e3:.1f} | {float(r['MinNs'])/1e3:.1f} | "
+                       f"{float(r['MaxNs'])/1e3:.1f} | {float(r['TotalDurationNs'])/1e6:.2f} |\n")
+    pmc = sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True))
+    if pmc:
+        per = {}
+        for path in pmc:
+            for r in csv.DictReader(open(path)):
+                name = r["Kernel_Name"]
+                key = ("sparse_attn" if "attn_kernel<128, false>" in name else
+                       "dense_attn" if "attn_kernel<128, true>" in name else
+                       "copy" if "MulFunctor" in name and int(r["Grid_Size"]) >= (COPY_BYTES // 64) else None)
+                if key is None:
+                    continue
+                per.setdefault((key, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
+        out.append("\n## Counters per dispatch (rocprofv3 --pmc), median over dispatches\n")
+        out.append("| kernel | counter | value (KiB) | dispatches |\n|---|---|---|---|\n")
+        med = {}
+        for (k, c), vals in sorted(per.items()):
+            med[(k, c)] = statistics.median(vals)
+            out.append(f"| {k} | {c} | {med[(k, c)]:.1f} | {len(vals)} |\n")
+        rec = {}
+        for c, known in (("FETCH_SIZE", COPY_BYTES), ("WRITE_SIZE", COPY_BYTES)):
+            if ("copy", c) in med and med[("copy", c)] > 0:
+                scale = known / med[("copy", c)]
+                rec[c + "_bytes_per_unit"] = scale
+                for k in ("sparse_attn", "dense_attn"):
+                    if (k, c) in med:
+                        rec[f"{k}_{c}_bytes"] = med[(k, c)] * scale
+        if rec:
+            out.append("\nScale: a plain copy of %d bytes reads/writes that many bytes; counter units -> bytes:\n" % COPY_BYTES)
+            out.append("\n```\n" + json.dumps(rec, indent=1) + "\n```\n")
+            out.append("\nMachine-readable: `PMC_RECORD " + json.dumps(rec) + "`\n")
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    dst = os.path.join(ROOT, "profiles", args.label + ".md")
+    with open(dst, "w") as f:
+        f.write("".join(out))
+    print(dst)
 
 
 def main():
     args = parse()
+    if args.summarize:
+        summarize(args)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
                           "n_gpus_requested": args.gpus}))
@@ -222,12 +310,15 @@ def main():
 
     assert torch.cuda.is_available(), "no GPU visible"
     cfg = CONFIGS[args.config]
+    if args.copy_calibration:
+        copy_calibration()
     res = layer_measure(cfg, args.steps, args.warmup, "headline")
     attn_src = src_hash(os.path.join(ROOT, "paper_2609_01925_amd", "csrc", "attn.hip"))
     achieved = res["_attn_flop"] / (res["_attn_launch_ms"] * 1e-3) / 1e12
     roofline = {
         "bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-        "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": attn_traffic(attn_src, cfg.name),
+        "frac": achieved / MFMA_BF16_PEAK_TFLOPS,
+        "traffic": attn_traffic(attn_src) if cfg.config_id == 2 else None,
         "kernel": "attn_kernel<128,false> (crisp_sparse_attn)",
         "flop_per_launch": res["_attn_flop"], "launch_ms": res["_attn_launch_ms"],
     }

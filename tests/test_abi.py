@@ -1,0 +1,131 @@
+"""C ABI checks that need no GPU: the library loads, exports every function that
+include/crisp.h declares, and rejects bad arguments on the host before launching
+anything (every call below fails validation or is an empty layer, so no kernel
+is ever enqueued)."""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2609_01925_amd import crisp as C
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "crisp.h")
+
+P_ALIGNED = ctypes.c_void_p(0x100000)      # never dereferenced: validation fails first
+P_MISALIGNED = ctypes.c_void_p(0x100002)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(crisp_[a-z_]+)\s*\(", text)))
+
+
+def test_header_functions_are_exported():
+    names = declared_functions()
+    assert len(names) >= 12
+    out = subprocess.run(["nm", "-D", "--defined-only", C._LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(line.split()[-1] for line in out.splitlines() if line.strip())
+    missing = [n for n in names if n not in exported]
+    assert not missing, f"declared but not exported: {missing}"
+    for n in names:
+        assert hasattr(C.lib, n)
+    assert set(C.EXPORTED) == set(names)
+
+
+def test_params_default_matches_paper():
+    p = C.crisp_params_default()
+    assert (p.alpha, p.w_sink, p.w_local, p.k_min_blocks, p.softmax_scale) == (1.0, 128, 128, 0, 0.0)
+    assert abs(p.tau_proxy - 0.2) < 1e-7 and abs(p.gamma - 0.95) < 1e-7
+
+
+def test_capacity_and_workspace_sizes():
+    sh = C.CrispShape(32, 8, 131072, 128, 128)
+    assert C.crisp_col_capacity(sh) == 1024 * 1025 // 2
+    ragged = C.CrispShape(2, 1, 1000, 128, 128)
+    assert C.crisp_col_capacity(ragged) == 8 * 9 // 2
+    ws = C.crisp_workspace_size(sh)
+    assert ws > 0 and C.crisp_prefill_workspace_size(sh) > ws and C.crisp_sparse_workspace_size(sh) > 0
+    assert C.crisp_col_capacity(C.CrispShape(3, 2, 100, 128, 128)) == -1
+    for bad, code in ((C.CrispShape(3, 2, 100, 128, 128), C.CRISP_EINVAL),
+                      (C.CrispShape(2, 0, 100, 128, 128), C.CRISP_EINVAL),
+                      (C.CrispShape(2, 1, -5, 128, 128), C.CRISP_EINVAL),
+                      (C.CrispShape(2, 1, 100, 64, 128), C.CRISP_EUNSUPPORTED),
+                      (C.CrispShape(2, 1, 100, 128, 96), C.CRISP_EUNSUPPORTED),
+                      (C.CrispShape(2, 1, (1 << 21) + 1, 128, 128), C.CRISP_EUNSUPPORTED)):
+        b = ctypes.c_size_t()
+        assert C.lib.crisp_workspace_size(ctypes.byref(bad), ctypes.byref(b)) == code
+        assert C.lib.crisp_last_error().decode()
+    assert C.lib.crisp_workspace_size(ctypes.byref(sh), None) == C.CRISP_EINVAL
+
+
+def _estimate(sh, p, q=P_ALIGNED, k=P_ALIGNED, ws=P_ALIGNED, ws_bytes=1 << 40):
+    return C.lib.crisp_estimate(ctypes.byref(sh), ctypes.byref(p), q, k, P_ALIGNED, P_ALIGNED, P_ALIGNED, ws,
+                                ws_bytes, None)
+
+
+@pytest.mark.parametrize("field,value", [("alpha", -0.1), ("alpha", math.nan), ("gamma", 0.0), ("gamma", 1.01),
+                                         ("w_sink", -1), ("w_local", -3), ("k_min_blocks", -2),
+                                         ("softmax_scale", -1.0), ("tau_proxy", math.inf)])
+def test_bad_params_rejected(field, value):
+    sh = C.CrispShape(2, 1, 4096, 128, 128)
+    p = C.crisp_params_default()
+    setattr(p, field, value)
+    assert _estimate(sh, p) == C.CRISP_EINVAL
+    assert C.lib.crisp_prefill_attn(ctypes.byref(sh), ctypes.byref(p), P_ALIGNED, P_ALIGNED, P_ALIGNED, P_ALIGNED,
+                                    None, None, None, P_ALIGNED, 1 << 40, None) == C.CRISP_EINVAL
+
+
+def test_null_misaligned_and_small_buffers_rejected():
+    sh = C.CrispShape(2, 1, 4096, 128, 128)
+    p = C.crisp_params_default()
+    assert _estimate(sh, p, q=None) == C.CRISP_EINVAL and "q is null" in C.lib.crisp_last_error().decode()
+    assert _estimate(sh, p, k=P_MISALIGNED) == C.CRISP_EINVAL and "aligned" in C.lib.crisp_last_error().decode()
+    assert _estimate(sh, p, ws=ctypes.c_void_p(0x100010)) == C.CRISP_EINVAL
+    assert _estimate(sh, p, ws_bytes=16) == C.CRISP_EINVAL and "too small" in C.lib.crisp_last_error().decode()
+    cap = C.crisp_col_capacity(sh)
+    st = C.lib.crisp_route_select(ctypes.byref(sh), ctypes.byref(p), P_ALIGNED, P_ALIGNED, P_ALIGNED, P_ALIGNED,
+                                  P_ALIGNED, P_ALIGNED, P_ALIGNED, P_ALIGNED, cap - 1, None, P_ALIGNED, 1 << 40, None)
+    assert st == C.CRISP_EINVAL and "col_cap" in C.lib.crisp_last_error().decode()
+    st = C.lib.crisp_sparse_attn(ctypes.byref(sh), 0.0, P_ALIGNED, P_ALIGNED, P_ALIGNED, None, P_ALIGNED, cap,
+                                 P_ALIGNED, None, 0, None)
+    assert st == C.CRISP_EINVAL
+    st = C.lib.crisp_sparse_attn(ctypes.byref(sh), 0.0, P_ALIGNED, P_ALIGNED, P_ALIGNED, P_ALIGNED, P_ALIGNED, cap,
+                                 P_ALIGNED, P_ALIGNED, 8, None)
+    assert st == C.CRISP_EINVAL and "workspace too small" in C.lib.crisp_last_error().decode()
+    st = C.lib.crisp_dense_attn(ctypes.byref(sh), -1.0, P_ALIGNED, P_ALIGNED, P_ALIGNED, P_ALIGNED, None)
+    assert st == C.CRISP_EINVAL
+    st = C.lib.crisp_dense_attn(ctypes.byref(sh), 0.0, P_ALIGNED, P_ALIGNED, P_ALIGNED, P_MISALIGNED, None)
+    assert st == C.CRISP_EINVAL
+
+
+def test_prefill_lists_all_or_none():
+    sh = C.CrispShape(2, 1, 4096, 128, 128)
+    p = C.crisp_params_default()
+    st = C.lib.crisp_prefill_attn(ctypes.byref(sh), ctypes.byref(p), P_ALIGNED, P_ALIGNED, P_ALIGNED, P_ALIGNED,
+                                  P_ALIGNED, None, P_ALIGNED, P_ALIGNED, 1 << 40, None)
+    assert st == C.CRISP_EINVAL and "all given or all null" in C.lib.crisp_last_error().decode()
+    need = C.crisp_prefill_workspace_size(sh)
+    st = C.lib.crisp_prefill_attn(ctypes.byref(sh), ctypes.byref(p), P_ALIGNED, P_ALIGNED, P_ALIGNED, P_ALIGNED,
+                                  None, None, None, P_ALIGNED, need - 256, None)
+    assert st == C.CRISP_EINVAL
+
+
+def test_empty_layers_are_ok_without_buffers():
+    p = C.crisp_params_default()
+    for sh in (C.CrispShape(0, 1, 4096, 128, 128), C.CrispShape(4, 2, 0, 128, 64)):
+        assert C.lib.crisp_estimate(ctypes.byref(sh), ctypes.byref(p), None, None, None, None, None, None, 0,
+                                    None) == C.CRISP_OK
+        assert C.lib.crisp_prefill_attn(ctypes.byref(sh), ctypes.byref(p), None, None, None, None, None, None, None,
+                                        None, 0, None) == C.CRISP_OK
+        assert C.lib.crisp_dense_attn(ctypes.byref(sh), 0.0, None, None, None, None, None) == C.CRISP_OK
+
+
+def test_status_strings():
+    for code, name in ((0, "CRISP_OK"), (1, "CRISP_EINVAL"), (2, "CRISP_EUNSUPPORTED"), (3, "CRISP_EHIP")):
+        assert C.lib.crisp_status_string(code).decode() == name
+    assert C.lib.crisp_status_string(99).decode() == "CRISP_UNKNOWN"
