@@ -25,9 +25,10 @@
 // (log2 units): until then P may exceed 1 by at most 2^8, which fp32 and bf16
 // hold exactly as well, and the O accumulators are left untouched.
 //
-// Sparse lists are processed by a persistent grid that pulls units from a
-// longest-first work list (built by attn_schedule from the list lengths), so
-// long PE rows start first and short VS rows fill the tail.
+// Sparse lists are processed by a persistent grid that pulls units from per-XCD
+// longest-first work lists (built by attn_schedule from the list lengths), so
+// long PE rows start first, short VS rows fill the tail, and the K/V tiles of a
+// KV group stay in one XCD's L2.
 #include "crisp_device.h"
 #include "crisp_internal.h"
 
@@ -390,47 +391,82 @@ __global__ __launch_bounds__(BQ * 2, CRISP_WAVES_PER_EU) void attn_kernel(AttnAr
     attn_unit<BQ, DENSE>(a, h, qb, smem, off, fe, tid);
     return;
   }
+  // Pop from this XCD's queue (workgroup i runs on XCD i % 8); when it is empty,
+  // take work from the other queues in turn.  Every queue ends, so every
+  // workgroup exits once all units are taken.
   int* s_unit = reinterpret_cast<int*>(smem + 2 * kRingBytes);
-  const int total = a.hq * a.nb;
+  const int x0 = blockIdx.x % kNumXcd;
+  const int* start = a.counter + 8;
   for (;;) {
     __syncthreads();  // the previous unit is done with LDS and the unit slot
-    if (tid == 0) *s_unit = atomicAdd(a.counter, 1);
+    if (tid == 0) {
+      int unit = -1;
+      for (int t = 0; t < kNumXcd && unit < 0; ++t) {
+        const int x = (x0 + t) % kNumXcd;
+        const int len = start[x + 1] - start[x];
+        if (len <= 0) continue;
+        const int pos = atomicAdd(a.counter + x, 1);
+        if (pos < len) unit = a.order[start[x] + pos];
+      }
+      *s_unit = unit;
+    }
     __syncthreads();
-    const int u = *s_unit;
-    if (u >= total) break;
-    const int unit = a.order[u];
+    const int unit = *s_unit;
+    if (unit < 0) break;
     attn_unit<BQ, DENSE>(a, unit / a.nb, unit % a.nb, smem, off, fe, tid);
   }
 #endif  // __HIP_DEVICE_COMPILE__
 }
 
-// Longest-first work list for the persistent sparse kernel: a counting sort of
-// the units (h, qb) by list length, descending.  One workgroup; also resets the
-// work counter.  Order within one length is arbitrary (it only affects which
-// workgroup runs a unit, never a result).
+// Work lists for the persistent sparse kernel: one queue per XCD.  Unit (h, qb)
+// goes to the queue of the XCD its KV group is bound to (group g -> XCD g when
+// there are >= 8 KV groups; with fewer groups each group spans 8 / H_kv XCDs,
+// split by query-block parity), so that XCD's L2 serves the group's K/V tiles to
+// all of the group's heads.  Within a queue units are ordered longest first (a
+// counting sort of list lengths: exact up to 768 blocks, then in steps of 16).
+// One workgroup builds all queues and resets their counters; the order within
+// one length is arbitrary (it only decides which workgroup runs a unit, never a
+// result).  Layout of the schedule area: int counters[8], int start[9], then the
+// units at int offset 64.
+constexpr int kQueueBuckets = kCostBuckets / kNumXcd;  // 1024 cost buckets per XCD queue
+
+__device__ __forceinline__ int unit_xcd(const AttnArgs& a, int h, int qb) {
+  const int g = h / a.G;
+  if (a.hkv >= kNumXcd) return g % kNumXcd;
+  const int r = kNumXcd / a.hkv;  // XCDs per group
+  return (g * r + qb % r) % kNumXcd;
+}
+
+__device__ __forceinline__ int cost_bucket(int64_t c) {
+  c = c < 0 ? 0 : c;
+  const int64_t b = c < 768 ? c : 768 + ((c - 768) >> 4);
+  return (int)(b < kQueueBuckets - 1 ? b : kQueueBuckets - 1);
+}
+
 __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
   __shared__ int hist[kCostBuckets];
+  __shared__ int part[1024];
   const int tid = threadIdx.x;
   const int total = a.hq * a.nb;
   for (int i = tid; i < kCostBuckets; i += 1024) hist[i] = 0;
   __syncthreads();
-  auto cost = [&](int u) {
+  // key: queue-major, longest first inside a queue
+  auto key = [&](int u) {
     const int h = u / a.nb, qb = u % a.nb;
     const int32_t* rp = a.row_ptr + (size_t)h * (a.nb + 1);
-    int64_t c = (int64_t)rp[qb + 1] - (int64_t)rp[qb];
-    c = c < 0 ? 0 : (c >= kCostBuckets ? kCostBuckets - 1 : c);
-    return (int)c;
+    const int c = cost_bucket((int64_t)rp[qb + 1] - (int64_t)rp[qb]);
+    return unit_xcd(a, h, qb) * kQueueBuckets + (kQueueBuckets - 1 - c);
   };
-  for (int u = tid; u < total; u += 1024) atomicAdd(&hist[kCostBuckets - 1 - cost(u)], 1);
+  for (int u = tid; u < total; u += 1024) atomicAdd(&hist[key(u)], 1);
   __syncthreads();
-  // exclusive scan over buckets (descending cost), 8 buckets per thread
-  __shared__ int part[1024];
-  int loc[kCostBuckets / 1024];
+  // exclusive scan over the keys, 8 per thread
+  constexpr int per = kCostBuckets / 1024;
+  int loc[per];
   int s = 0;
 #pragma unroll
-  for (int i = 0; i < kCostBuckets / 1024; ++i) {
+  for (int i = 0; i < per; ++i) {
     loc[i] = s;
-    s += hist[tid * (kCostBuckets / 1024) + i];
+    s += hist[tid * per + i];
   }
   part[tid] = s;
   __syncthreads();
@@ -442,13 +478,19 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
   }
   const int base = part[tid] - s;
 #pragma unroll
-  for (int i = 0; i < kCostBuckets / 1024; ++i) hist[tid * (kCostBuckets / 1024) + i] = base + loc[i];
+  for (int i = 0; i < per; ++i) hist[tid * per + i] = base + loc[i];
+  __syncthreads();
+  // queue x starts at the first key of x: thread x * (kQueueBuckets / per) holds it
+  if (tid < kNumXcd) {
+    a.counter[tid] = 0;
+    a.counter[8 + tid] = hist[tid * kQueueBuckets];
+  }
+  if (tid == 0) a.counter[8 + kNumXcd] = total;
   __syncthreads();
   for (int u = tid; u < total; u += 1024) {
-    const int pos = atomicAdd(&hist[kCostBuckets - 1 - cost(u)], 1);
+    const int pos = atomicAdd(&hist[key(u)], 1);
     const_cast<int32_t*>(a.order)[pos] = u;
   }
-  if (tid == 0) *a.counter = 0;
 }
 
 template <int BQ, bool DENSE>
