@@ -25,6 +25,10 @@ ARCH = "gfx950"
 # otherwise form them from ordinary float code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall", "-Wno-unused-function"]
+# Per-source device flags.  The attention kernel keeps its MFMA results (scores,
+# read by the softmax every tile, and the output accumulators) in VGPRs; left to
+# itself the compiler places them in AGPRs and copies every score out again.
+EXTRA = {"attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def hipcc() -> str:
@@ -55,7 +59,8 @@ def build(verbose: bool = False) -> str:
     jobs = []
     for f in hip:
         obj = os.path.join(BUILD, f[:-4] + ".o")
-        jobs.append([cc, f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS, "-c", os.path.join(CSRC, f), "-o", obj])
+        jobs.append([cc, f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS, *EXTRA.get(f, []), "-c",
+                     os.path.join(CSRC, f), "-o", obj])
     for f in cpp:
         obj = os.path.join(BUILD, f[:-4] + ".o")
         jobs.append([cc, f"--offload-arch={ARCH}", *COMMON, "-c", os.path.join(CSRC, f), "-o", obj])

@@ -7,28 +7,30 @@
 //   S^T (64 keys x 32 queries) = K_tile Q^T      16 x v_mfma_f32_32x32x16_bf16
 //   online softmax in fp32 (exp2, log2(e) folded into the scale)
 //   O^T (128 d x 32 queries) += V^T P^T          16 x v_mfma_f32_32x32x16_bf16
-// The score tile is transposed so that a lane owns one query: row maxima and
-// sums are lane-local plus one v_permlane32_swap with lane l ^ 32.  The C
+// The score tile is transposed so that a lane owns one query: row sums and
+// maxima are lane-local plus one v_permlane32_swap with lane l ^ 32.  The C
 // layout of S^T is reused directly as the B operand of the PV product; V^T
 // operands come from LDS through ds_read_b64_tr_b16, which transposes 4 keys x
 // 16 dims per 16-lane group, so V needs no transposed copy.
 //
 // K and V tiles move from global memory straight into LDS with LDS-DMA loads
 // (buffer_load ... lds), two 2-deep rings (K, V) of 16 KB stages: 64 KB per
-// workgroup, so two workgroups share a CU and every SIMD interleaves two waves,
-// which hides the latency of one wave's LDS reads and MFMA chains behind the
-// other's work.  At the top of iteration j the DMAs for K(j+2) and V(j+1) go into
-// the stages freed by iteration j-1, so each has a full iteration to land.
-// Within a wave the order is softmax(j), scores(j+1), PV(j): the matrix cores of a
-// SIMD are kept busy by the other resident wave while this one does softmax.
-// The running max is only raised when a row's max grows by more than 2^8
-// (log2 units): until then P may exceed 1 by at most 2^8, which fp32 and bf16
-// hold exactly as well, and the O accumulators are left untouched.
+// workgroup, so two workgroups share a CU and every SIMD interleaves two waves.
+// Step j of a unit overlaps three things: tile j's probabilities are formed
+// (against the running max) beside the PV product of tile j-1, then the scores
+// of tile j+1 are computed beside the row sums.  Each ring stage is refilled
+// one step before it is read, and the loop is expanded two steps at a time so
+// that every stage address is a compile-time immediate.  The running max is
+// only raised when some lane's tile sum of P exceeds 2^8 (then every P of that
+// lane does too at most): until then P may exceed 1 by at most 2^8, which fp32
+// and bf16 hold exactly as well, and the O accumulators are left untouched.
 //
 // Sparse lists are processed by a persistent grid that pulls units from per-XCD
 // longest-first work lists (built by attn_schedule from the list lengths), so
 // long PE rows start first, short VS rows fill the tail, and the K/V tiles of a
 // KV group stay in one XCD's L2.
+#include <type_traits>
+
 #include "crisp_device.h"
 #include "crisp_internal.h"
 
@@ -39,7 +41,7 @@ namespace {
 constexpr int BK = 64;                       // keys per tile
 constexpr int kTileBytes = BK * 256;         // one K or V tile: 64 rows x 128 bf16
 constexpr int kRingBytes = 2 * kTileBytes;   // one ring (K or V): 2 stages
-constexpr float kLazyRescale = 8.0f;         // log2 growth of a row max tolerated before rescaling
+constexpr float kSumLimit = 256.0f;          // a lane's tile sum of P above this forces a rescale
 constexpr int kCostBuckets = 8192;
 
 struct AttnArgs {
@@ -88,6 +90,19 @@ __device__ __forceinline__ bool map_unit(const AttnArgs& a, int bid, int& h, int
   h = g * a.G + (u % a.G);
   return true;
 }
+
+// Workgroup geometry for query blocks of BQ rows: QH halves of 32 queries per
+// wave, BQ / (32 QH) waves.  One half per wave (two waves per SIMD, at most 256
+// registers each) is what runs: two halves would halve the LDS operand reads per
+// MFMA, but need one wave per SIMD, which then has no other wave to hide its
+// latencies behind and runs slower.
+template <int BQ>
+struct Geo {
+  static constexpr int kQH = 1;
+  static constexpr int kWaves = BQ / (32 * kQH);
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int kWavesPerEU = kQH == 2 ? 1 : 2;
+};
 
 #if defined(__HIP_DEVICE_COMPILE__)
 
@@ -146,29 +161,24 @@ __device__ __forceinline__ i32x4 tensor_rsrc(const uint16_t* base, int n) {
   return i32x4{(int)(unsigned)p, (int)(unsigned)(p >> 32), n * 256, 0x00020000};
 }
 
-// One LDS-DMA load: 16 bytes per lane from rsrc + voff + soff into lds_base + 16 * lane.
-// Issued as inline assembly so that the compiler's wait-count pass does not treat
-// every later LDS read as dependent on it; the kernel waits explicitly (wait_dma)
-// and publishes the tile with a workgroup barrier before any wave reads it.
-__device__ __forceinline__ void dma16(i32x4 rsrc, int voff, int soff, const char* lds_base) {
-  const int m0 = __builtin_amdgcn_readfirstlane((int)(size_t)lds_base);
+// One LDS-DMA load: 16 bytes per lane from rsrc + voff + soff into LDS address
+// lds_addr + 16 * lane.  Issued as inline assembly so that the compiler's
+// wait-count pass does not treat every later LDS read as dependent on it; the
+// kernel waits explicitly (wait_dma) and publishes the tile with a workgroup
+// barrier before any wave reads it.
+__device__ __forceinline__ void dma16(i32x4 rsrc, int voff, int soff, int lds_addr) {
+  const int m0 = __builtin_amdgcn_readfirstlane(lds_addr);
   const int so = __builtin_amdgcn_readfirstlane(soff);
-#ifdef CRISP_EXP_BUILTIN_DMA
-  const unsigned long long base = ((unsigned long long)(unsigned)rsrc[1] << 32) | (unsigned)rsrc[0];
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(__builtin_amdgcn_make_buffer_rsrc((void*)base, 0, rsrc[2], rsrc[3]),
-      (__attribute__((address_space(3))) void*)lds_base, 16, voff, so, 0, 0);
-#else
-  // The scalar offset comes from v_readfirstlane (a VALU write to an SGPR), which a
-  // VMEM instruction may only read after 5 wait states, and M0 is written just
-  // before; the compiler cannot see these reads inside the assembly, so the wait
-  // states are part of it.
+  // The scalar offset may come from v_readfirstlane (a VALU write to an SGPR),
+  // which a VMEM instruction may only read after 5 wait states, and M0 is written
+  // just before; the compiler cannot see these reads inside the assembly, so the
+  // wait states are part of it.
   asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rsrc), "s"(so), "{m0}"(m0));
-#endif
 }
 
-// One tensor's tile into one LDS stage.
+// One tensor's tile into the LDS stage at address stage.
 template <int NW>
-__device__ __forceinline__ void fetch_tile(const Fetch<NW>& f, i32x4 rsrc, char* stage, int key0, int w) {
+__device__ __forceinline__ void fetch_tile(const Fetch<NW>& f, i32x4 rsrc, int stage, int key0, int w) {
 #pragma unroll
   for (int x = 0; x < Fetch<NW>::kPerWave; ++x) {
     const int wp = w + NW * x;
@@ -177,20 +187,30 @@ __device__ __forceinline__ void fetch_tile(const Fetch<NW>& f, i32x4 rsrc, char*
   }
 }
 
+// LDS reads at integer LDS addresses (no generic-pointer conversion).
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+__device__ __forceinline__ bf16x8 lds_ld16(int addr) { return *(const lds_bf16x8*)(uint32_t)addr; }
+__device__ __forceinline__ bf16x4 lds_ld_tr(int addr) {
+  return __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(uint32_t)addr));
+}
+
 // Waits until every LDS-DMA load of this wave has landed (s_waitcnt vmcnt(0)).
 __device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
 
-// S^T for one tile: s[mb] covers keys 32 * mb + (C-layout rows), queries = lane column.
-// Rows 32..63 have the same swizzle as rows 0..31, so sub-block 1 is +32 rows.
-__device__ __forceinline__ void qk_tile(const char* kbuf, const bf16x8 (&qf)[8], const Offsets& off, f32x16 (&s)[2]) {
-  s[0] = zero16();
-  s[1] = zero16();
+// S^T for one tile: s[h][mb] holds keys 32 mb + (C-layout row) against the 32
+// queries of half h (lane column).  qk_sub computes sub-block MB for every half;
+// rows 32..63 have the same swizzle as rows 0..31, so sub-block 1 is +32 rows,
+// and each K operand read serves every half.
+template <int QH, int MB>
+__device__ __forceinline__ void qk_sub(int kbuf, const bf16x8 (&qf)[QH][8], const Offsets& off, f32x16 (&s)[QH][2]) {
+#pragma unroll
+  for (int h = 0; h < QH; ++h) s[h][MB] = zero16();
 #pragma unroll
   for (int kk = 0; kk < 8; ++kk) {
-    const bf16x8 a0 = lds_read16(kbuf, off.k[kk]);
-    const bf16x8 a1 = lds_read16(kbuf + 32 * 256, off.k[kk]);
-    s[0] = mfma32(a0, qf[kk], s[0]);
-    s[1] = mfma32(a1, qf[kk], s[1]);
+    const bf16x8 ak = lds_ld16(kbuf + 32 * 256 * MB + off.k[kk]);
+#pragma unroll
+    for (int h = 0; h < QH; ++h) s[h][MB] = mfma32(ak, qf[h][kk], s[h][MB]);
   }
 }
 
@@ -206,44 +226,75 @@ __device__ __forceinline__ void mask_tile(f32x16 (&s)[2], int key0, int qabs, bo
     }
 }
 
-// P = exp2(s * c - m c) as bf16 MFMA operands, row sums accumulated in l.
-__device__ __forceinline__ void softmax_p(const f32x16& s, float c, float mc, bf16x8 (&pb)[2], float& l) {
+// Maximum of the lane's 16 scores of one sub-block.
+__device__ __forceinline__ float max16(const f32x16& s) {
+  float m = vmax(s[0], s[1]);
+#pragma unroll
+  for (int i = 2; i < 16; i += 2) m = vmax(vmax(m, s[i]), s[i + 1]);
+  return m;
+}
+
+// P = exp2(s c - mc) for one sub-block as bf16 B operands of the PV product:
+// pb[hh] covers the keys of registers 8 hh .. 8 hh + 7.
+__device__ __forceinline__ void exp_sub(const f32x16& s, float c, float mc, bf16x8 (&pb)[2]) {
 #pragma unroll
   for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
     for (int e = 0; e < 8; e += 2) {
-      const float p0 = fast_exp2(__builtin_fmaf(s[8 * hh + e], c, -mc));
-      const float p1 = fast_exp2(__builtin_fmaf(s[8 * hh + e + 1], c, -mc));
-      const bf16x2 pr = pack_bf16(p0, p1);
+      const bf16x2 pr = pack_bf16(fast_exp2(__builtin_fmaf(s[8 * hh + e], c, -mc)),
+                                  fast_exp2(__builtin_fmaf(s[8 * hh + e + 1], c, -mc)));
       pb[hh][e] = pr[0];
       pb[hh][e + 1] = pr[1];
-      l = dot2_bf16_sum(pr, l);
     }
 }
 
-// O^T += V^T P^T for one 32-key sub-block of the tile.
-__device__ __forceinline__ void pv_sub(const char* vbuf, const Offsets& off, const bf16x8 (&pb)[2], f32x16 (&o)[4]) {
+// l + the lane's sum of the tile's (bf16) probabilities.
+__device__ __forceinline__ float sum_tile(const bf16x8 (&pb)[2][2], float l) {
 #pragma unroll
-  for (int ss = 0; ss < 2; ++ss) {
-    const char* vb = vbuf + 16 * ss * 256;
+  for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-    for (int db = 0; db < 4; ++db) {
-      const bf16x8 av = cat(lds_read_tr(vb, off.v[db][0]), lds_read_tr(vb, off.v[db][1]));
-      o[db] = mfma32(av, pb[ss], o[db]);
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int e = 0; e < 8; e += 2) {
+        bf16x2 pr;
+        pr[0] = pb[mb][hh][e];
+        pr[1] = pb[mb][hh][e + 1];
+        l = dot2_bf16_sum(pr, l);
+      }
+  return l;
+}
+
+// O^T[h] (128 d x 32 queries) += V^T P^T[h] for one tile; each V^T operand (two
+// transposing reads) serves every half.
+template <int QH>
+__device__ __forceinline__ void pv_tile(int vbuf, const Offsets& off, const bf16x8 (&pb)[QH][2][2], f32x16 (&o)[QH][4]) {
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int ss = 0; ss < 2; ++ss) {
+      const int vb = vbuf + (32 * mb + 16 * ss) * 256;
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        const bf16x8 av = cat(lds_ld_tr(vb + off.v[db][0]), lds_ld_tr(vb + off.v[db][1]));
+#pragma unroll
+        for (int h = 0; h < QH; ++h) o[h][db] = mfma32(av, pb[h][mb][ss], o[h][db]);
+      }
     }
-  }
 }
 
 // One (head, query block) unit.
 template <int BQ, bool DENSE>
-__device__ __forceinline__ void attn_unit(const AttnArgs& a, int h, int qb, char* smem, const Offsets& off,
-                                          const Fetch<BQ / 32>& fe, int tid) {
-  constexpr int NW = BQ / 32;
+__device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, int lds0, const Offsets& off,
+                                          const Fetch<Geo<BQ>::kWaves>& fe, int tid) {
+  constexpr int QH = Geo<BQ>::kQH;
+  constexpr int NW = Geo<BQ>::kWaves;
   constexpr int TPB = BQ / BK;  // tiles per key block
   const int l = tid & 63, w = tid >> 6;
-  const int g = h / a.G;
+  const int g = head / a.G;
   const int q0 = qb * BQ;
-  const int qabs = q0 + 32 * w + (l & 31);
+  int qabs[QH];
+#pragma unroll
+  for (int h = 0; h < QH; ++h) qabs[h] = q0 + 32 * (QH * w + h) + (l & 31);
   const i32x4 rk = tensor_rsrc(a.k + (size_t)g * a.n * kHeadDim, a.n);
   const i32x4 rv = tensor_rsrc(a.v + (size_t)g * a.n * kHeadDim, a.n);
 
@@ -252,14 +303,14 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int h, int qb, char
   if (DENSE) {
     cnt = qb + 1;
   } else {
-    const int32_t* rp = a.row_ptr + (size_t)h * (a.nb + 1);
+    const int32_t* rp = a.row_ptr + (size_t)head * (a.nb + 1);
     const int64_t cap = a.col_cap;
     int64_t b0 = rp[qb], e0 = rp[qb + 1];
     b0 = b0 < 0 ? 0 : (b0 > cap ? cap : b0);
     e0 = e0 < b0 ? b0 : (e0 > cap ? cap : e0);
     beg = (int)b0;
     cnt = (int)(e0 - b0);
-    cols = a.col_idx + (size_t)h * cap;
+    cols = a.col_idx + (size_t)head * cap;
   }
   const int T = cnt * TPB;
 
@@ -275,120 +326,172 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int h, int qb, char
     bool vv, mm;
     return tile_key0(j, vv, mm);
   };
-  char* kring = smem;
-  char* vring = smem + kRingBytes;
-  auto kst = [&](int j) { return kring + (j & 1) * kTileBytes; };
-  auto vst = [&](int j) { return vring + (j & 1) * kTileBytes; };
+  // ring stages by parity: K at lds0 + {0, 16 KB}, V at lds0 + 32 KB + {0, 16 KB}
+  auto kst = [&](int parity) { return lds0 + parity * kTileBytes; };
+  auto vst = [&](int parity) { return lds0 + kRingBytes + parity * kTileBytes; };
 
-  bf16x8 qf[8];
-  {
-    const uint16_t* qrow = a.q + ((size_t)h * a.n + (qabs < a.n ? qabs : 0)) * kHeadDim;
+  bf16x8 qf[QH][8];
+#pragma unroll
+  for (int h = 0; h < QH; ++h) {
+    const uint16_t* qrow = a.q + ((size_t)head * a.n + (qabs[h] < a.n ? qabs[h] : 0)) * kHeadDim;
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) {
       u32x4 raw = *reinterpret_cast<const u32x4*>(qrow + 16 * kk + 8 * (l >> 5));
-      if (qabs >= a.n) raw = u32x4{0, 0, 0, 0};
-      qf[kk] = __builtin_bit_cast(bf16x8, raw);
+      if (qabs[h] >= a.n) raw = u32x4{0, 0, 0, 0};
+      qf[h][kk] = __builtin_bit_cast(bf16x8, raw);
     }
   }
 
-  f32x16 o[4];
+  f32x16 o[QH][4];
+  float m_run[QH], l_run[QH];
 #pragma unroll
-  for (int db = 0; db < 4; ++db) o[db] = zero16();
-  float m_run = -__builtin_inff(), l_run = 0.f;
+  for (int h = 0; h < QH; ++h) {
+#pragma unroll
+    for (int db = 0; db < 4; ++db) o[h][db] = zero16();
+    m_run[h] = -__builtin_inff();
+    l_run[h] = 0.f;
+  }
 
+  f32x16 s[QH][2];
   if (T > 0) {
-    // prologue: K(0), V(0), K(1)
-    fetch_tile<NW>(fe, rk, kst(0), key0_of(0), w);
-    fetch_tile<NW>(fe, rv, vst(0), key0_of(0), w);
-    if (T > 1) fetch_tile<NW>(fe, rk, kst(1), key0_of(1), w);
-    wait_dma();
-    __syncthreads();
-    f32x16 s[2];
-    qk_tile(kst(0), qf, off, s);
-
-    for (int j = 0; j < T; ++j) {
-      const bool has_next = j + 1 < T;
-      // K(j+1) and V(j), issued one iteration ago (or in the prologue), have landed
-      // for every wave, and every wave is done with the stages of K(j) (scored in
-      // the previous iteration or the prologue) and V(j-1), which are refilled next.
+    // Step j (parity P): tile j's scores S(j) are in registers and P(j-1) is
+    // formed.  At the top, K(j+1) and V(j-1), issued in step j-1 (or the
+    // prologue), have landed for every wave, and every wave is done with the
+    // stages of K(j) (scored in step j-1) and V(j-2), which are refilled with
+    // K(j+2) and V(j).  Tile j's probabilities are formed against the running max
+    // beside the PV product of tile j-1.  They stand while each lane's sum of them
+    // stays at most 2^8 (so does every one of them); otherwise the (rare) branch
+    // raises the running max to the tile's row max, rescales O and l, and forms
+    // them again.  Last, the scores of tile j+1 replace S(j).
+    auto step = [&](int j, auto par, auto first, const bf16x8 (&pp)[QH][2][2], bf16x8 (&pn)[QH][2][2]) {
+      constexpr int P = decltype(par)::value;
       wait_dma();
       __syncthreads();
-      if (j + 2 < T) fetch_tile<NW>(fe, rk, kst(j + 2), key0_of(j + 2), w);
-      if (has_next) fetch_tile<NW>(fe, rv, vst(j + 1), key0_of(j + 1), w);
+      if (j + 2 < T) fetch_tile<NW>(fe, rk, kst(P), key0_of(j + 2), w);
+      fetch_tile<NW>(fe, rv, vst(P), key0_of(j), w);
       {
         bool vj, mj;
         const int kj = tile_key0(j, vj, mj);
-        if (mj) mask_tile(s, kj, qabs, vj, l);
-      }
-
-      // row max of tile j; the running max is raised only when it grows by > 2^8
-      float mx = -__builtin_inff();
+        if (mj) {
 #pragma unroll
-      for (int i = 0; i < 16; i += 2)
-        mx = fmaxf(fmaxf(mx, fmaxf(s[0][i], s[0][i + 1])), fmaxf(s[1][i], s[1][i + 1]));
-      mx = half_max(mx);
-      const bool grow = mx * a.c > m_run * a.c + kLazyRescale || m_run == -__builtin_inff();
+          for (int h = 0; h < QH; ++h) mask_tile(s[h], kj, qabs[h], vj, l);
+        }
+      }
+      float ts[QH];
+      bool grow = false;
+#pragma unroll
+      for (int h = 0; h < QH; ++h) {
+        const float mc = m_run[h] == -__builtin_inff() ? 0.f : m_run[h] * a.c;
+        exp_sub(s[h][0], a.c, mc, pn[h][0]);
+        exp_sub(s[h][1], a.c, mc, pn[h][1]);
+        ts[h] = sum_tile(pn[h], 0.f);
+        grow = grow || !(ts[h] <= kSumLimit) || m_run[h] == -__builtin_inff();
+      }
+      if (!decltype(first)::value) pv_tile<QH>(vst(1 - P), off, pp, o);
+      // Keeps the probabilities formed here, beside the PV product, rather than
+      // letting the compiler sink them into the no-rescale path.
+#pragma unroll
+      for (int h = 0; h < QH; ++h)
+        asm volatile("" ::"v"(pn[h][0][0]), "v"(pn[h][0][1]), "v"(pn[h][1][0]), "v"(pn[h][1][1]), "v"(ts[h]));
       if (__ballot(grow)) {
-        const float m_new = grow ? fmaxf(m_run, mx) : m_run;
-        const float alpha = m_run == -__builtin_inff() ? 0.f : fast_exp2((m_run - m_new) * a.c);
-        l_run *= alpha;
 #pragma unroll
-        for (int db = 0; db < 4; ++db)
+        for (int h = 0; h < QH; ++h) {
+          const float mx = half_max(vmax(max16(s[h][0]), max16(s[h][1])));
+          const float m_new = vmax(m_run[h], mx);
+          const float alpha = m_run[h] == -__builtin_inff() ? 0.f : fast_exp2((m_run[h] - m_new) * a.c);
+          l_run[h] *= alpha;
 #pragma unroll
-          for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
-        m_run = m_new;
+          for (int db = 0; db < 4; ++db)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) o[h][db][i] *= alpha;
+          m_run[h] = m_new;
+          const float mcn = m_new == -__builtin_inff() ? 0.f : m_new * a.c;
+          exp_sub(s[h][0], a.c, mcn, pn[h][0]);
+          exp_sub(s[h][1], a.c, mcn, pn[h][1]);
+          ts[h] = sum_tile(pn[h], 0.f);
+        }
       }
-      const float mc = m_run == -__builtin_inff() ? 0.f : m_run * a.c;
+#pragma unroll
+      for (int h = 0; h < QH; ++h) l_run[h] += ts[h];
+      // After the last tile the stage of K(j+1) holds stale data that no DMA
+      // targets; those scores are never used.  The scheduler interleaves the
+      // K operand reads with the MFMAs in its LDS/MFMA pipelining mode.
+      __builtin_amdgcn_iglp_opt(0);
+      qk_sub<QH, 0>(kst(1 - P), qf, off, s);
+      qk_sub<QH, 1>(kst(1 - P), qf, off, s);
+    };
+    using Even = std::integral_constant<int, 0>;
+    using Odd = std::integral_constant<int, 1>;
 
-      bf16x8 pb0[2], pb1[2];
-      softmax_p(s[0], a.c, mc, pb0, l_run);
-      softmax_p(s[1], a.c, mc, pb1, l_run);
-      if (has_next) qk_tile(kst(j + 1), qf, off, s);  // S(j) is consumed: reuse its registers
-      pv_sub(vst(j), off, pb0, o);
-      pv_sub(vst(j) + 32 * 256, off, pb1, o);
+    // prologue: K(0), K(1), then the scores of tile 0
+    fetch_tile<NW>(fe, rk, kst(0), key0_of(0), w);
+    if (T > 1) fetch_tile<NW>(fe, rk, kst(1), key0_of(1), w);
+    wait_dma();
+    __syncthreads();
+    qk_sub<QH, 0>(kst(0), qf, off, s);
+    qk_sub<QH, 1>(kst(0), qf, off, s);
+    // two P buffers with fixed registers: steps alternate between them, and the
+    // parity of every step is known where it is expanded
+    bf16x8 pa[QH][2][2], pz[QH][2][2];
+    step(0, Even{}, std::true_type{}, pz, pa);
+    int j = 1;
+    for (; j + 1 < T; j += 2) {
+      step(j, Odd{}, std::false_type{}, pa, pz);
+      step(j + 1, Even{}, std::false_type{}, pz, pa);
+    }
+    // PV of the last tile: its V stage was filled in the last step
+    if (j < T) {
+      step(j, Odd{}, std::false_type{}, pa, pz);
+      wait_dma();
+      __syncthreads();
+      pv_tile<QH>(vst(1), off, pz, o);
+    } else {
+      wait_dma();
+      __syncthreads();
+      pv_tile<QH>(vst(0), off, pa, o);
     }
   }
 
-  const float l_tot = half_sum(l_run);
-  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-  if (qabs < a.n) {
-    uint16_t* orow = a.o + ((size_t)h * a.n + qabs) * kHeadDim;
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
+  for (int h = 0; h < QH; ++h) {
+    const float l_tot = half_sum(l_run[h]);
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    if (qabs[h] < a.n) {
+      uint16_t* orow = a.o + ((size_t)head * a.n + qabs[h]) * kHeadDim;
 #pragma unroll
-      for (int i4 = 0; i4 < 4; ++i4) {
-        const int d = 32 * db + 8 * i4 + 4 * (l >> 5);
-        const bf16x2 lo = pack_bf16(o[db][4 * i4 + 0] * inv, o[db][4 * i4 + 1] * inv);
-        const bf16x2 hi = pack_bf16(o[db][4 * i4 + 2] * inv, o[db][4 * i4 + 3] * inv);
-        bf16x4 r;
-        r[0] = lo[0]; r[1] = lo[1]; r[2] = hi[0]; r[3] = hi[1];
-        *reinterpret_cast<bf16x4*>(orow + d) = r;
-      }
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          const int d = 32 * db + 8 * i4 + 4 * (l >> 5);
+          const bf16x2 lo = pack_bf16(o[h][db][4 * i4 + 0] * inv, o[h][db][4 * i4 + 1] * inv);
+          const bf16x2 hi = pack_bf16(o[h][db][4 * i4 + 2] * inv, o[h][db][4 * i4 + 3] * inv);
+          bf16x4 r;
+          r[0] = lo[0]; r[1] = lo[1]; r[2] = hi[0]; r[3] = hi[1];
+          *reinterpret_cast<bf16x4*>(orow + d) = r;
+        }
+    }
   }
 }
 
 #endif  // __HIP_DEVICE_COMPILE__
 
-#ifdef CRISP_EXP_ONE_WAVE
-#define CRISP_WAVES_PER_EU 1
-#else
-#define CRISP_WAVES_PER_EU 2
-#endif
 template <int BQ, bool DENSE>
-__global__ __launch_bounds__(BQ * 2, CRISP_WAVES_PER_EU) void attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_kernel(AttnArgs a) {
 #if defined(__HIP_DEVICE_COMPILE__)
   // The rings are the kernel's only LDS object, so they start at LDS address 0
   // (LDS-DMA destinations are then 1 KB aligned); the work-queue slot sits after them.
   __shared__ __attribute__((aligned(1024))) char smem[2 * kRingBytes + 16];
+  const int lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);  // LDS address of the rings
+  constexpr int NW = Geo<BQ>::kWaves;
   const int tid = threadIdx.x;
   Offsets off;
   make_offsets(off, tid & 63);
-  Fetch<BQ / 32> fe;
-  make_fetch<BQ / 32>(fe, tid >> 6, tid & 63);
+  Fetch<NW> fe;
+  make_fetch<NW>(fe, tid >> 6, tid & 63);
   if (DENSE || a.order == nullptr) {
     int h, qb;
     if (!map_unit(a, blockIdx.x, h, qb)) return;
-    attn_unit<BQ, DENSE>(a, h, qb, smem, off, fe, tid);
+    attn_unit<BQ, DENSE>(a, h, qb, lds0, off, fe, tid);
     return;
   }
   // Pop from this XCD's queue (workgroup i runs on XCD i % 8); when it is empty,
@@ -413,7 +516,7 @@ __global__ __launch_bounds__(BQ * 2, CRISP_WAVES_PER_EU) void attn_kernel(AttnAr
     __syncthreads();
     const int unit = *s_unit;
     if (unit < 0) break;
-    attn_unit<BQ, DENSE>(a, unit / a.nb, unit % a.nb, smem, off, fe, tid);
+    attn_unit<BQ, DENSE>(a, unit / a.nb, unit % a.nb, lds0, off, fe, tid);
   }
 #endif  // __HIP_DEVICE_COMPILE__
 }
@@ -495,7 +598,7 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
 
 template <int BQ, bool DENSE>
 hipError_t launch_t(const AttnArgs& a, int grid, hipStream_t stream) {
-  hipLaunchKernelGGL((attn_kernel<BQ, DENSE>), dim3(grid), dim3(BQ * 2), 0, stream, a);
+  hipLaunchKernelGGL((attn_kernel<BQ, DENSE>), dim3(grid), dim3(Geo<BQ>::kThreads), 0, stream, a);
   return hipGetLastError();
 }
 
@@ -508,7 +611,7 @@ int persistent_grid() {
   if (cached[dev] > 0) return cached[dev];
   int cus = 0, per = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_kernel<BQ, false>, BQ * 2, 0) != hipSuccess || per <= 0)
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_kernel<BQ, false>, Geo<BQ>::kThreads, 0) != hipSuccess || per <= 0)
     per = 1;
   cached[dev] = cus * per;
   return cached[dev];
