@@ -314,9 +314,29 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
   }
   const int T = cnt * TPB;
 
+  // Sparse lists: the unit's column indices are held 64 to a VGPR (one per lane;
+  // chunk c of the list in colv0 or colv1 by its parity), the chunk of the current tile and the
+  // next one, so a lookup is a v_readlane and never waits on memory.  A chunk is
+  // fetched at the end of a step, a whole chunk ahead of its first use, and lands
+  // under the wait at the top of the next step.  Lanes past the list end load its
+  // last entry; they are never looked up.
+  int colv0 = 0, colv1 = 0;
+  int chunk0 = 0;  // chunk of the current tile
+  auto load_chunk = [&](int c) -> int {
+    const int i = 64 * c + l;
+    return cols[beg + (i < cnt ? i : cnt - 1)];
+  };
+  auto col_of = [&](int bi) -> int {
+    return __builtin_amdgcn_readlane((bi >> 6) & 1 ? colv1 : colv0, bi & 63);
+  };
+  if (!DENSE && cnt > 0) {
+    colv0 = load_chunk(0);
+    colv1 = load_chunk(1);
+  }
+
   // tile j -> first key, validity (entry in [0, qb]) and whether it needs the mask
   auto tile_key0 = [&](int j, bool& valid, bool& needs_mask) -> int {
-    int kb = DENSE ? j / TPB : cols[beg + j / TPB];
+    int kb = DENSE ? j / TPB : col_of(j / TPB);
     valid = kb >= 0 && kb <= qb;
     if (!valid) kb = 0;
     needs_mask = !valid || kb == qb;
@@ -367,6 +387,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
       constexpr int P = decltype(par)::value;
       wait_dma();
       __syncthreads();
+
       if (j + 2 < T) fetch_tile<NW>(fe, rk, kst(P), key0_of(j + 2), w);
       fetch_tile<NW>(fe, rv, vst(P), key0_of(j), w);
       {
@@ -419,6 +440,13 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
       __builtin_amdgcn_iglp_opt(0);
       qk_sub<QH, 0>(kst(1 - P), qf, off, s);
       qk_sub<QH, 1>(kst(1 - P), qf, off, s);
+      if (!DENSE && (((j + 1) / TPB) >> 6) != chunk0) {  // tile j+1 starts the next chunk
+        ++chunk0;
+        if ((chunk0 + 1) & 1)
+          colv1 = load_chunk(chunk0 + 1);
+        else
+          colv0 = load_chunk(chunk0 + 1);
+      }
     };
     using Even = std::integral_constant<int, 0>;
     using Odd = std::integral_constant<int, 1>;
