@@ -39,6 +39,11 @@ class Params:
     w_local: int = 128
     k_min_blocks: int = 0          # 0 -> ceil(1024 / B) blocks
     softmax_scale: float = 0.0     # 0 -> 1 / sqrt(d)
+    # FlexPrefill comparator (App. A): route by the JSD pattern search instead of
+    # C_struct, and/or select VS blocks by gamma coverage instead of the noise floor.
+    route_mode: str = "cstruct"    # "cstruct" (Alg. 2) or "jsd" (App. A, pattern search)
+    vs_mode: str = "floor"         # "floor" (Alg. 3) or "gamma" (App. A, VS index selection)
+    tau_jsd: float = 0.1           # JSD threshold; the paper gives none (reading R26)
 
     def scale(self, d: int) -> float:
         return self.softmax_scale if self.softmax_scale > 0 else 1.0 / math.sqrt(d)
@@ -275,6 +280,73 @@ def dense_causal_sets(nb: int) -> List[List[int]]:
 
 
 # ----------------------------------------------------------------------------
+# FlexPrefill comparator (App. A): JSD pattern search and gamma-coverage VS selection
+# ----------------------------------------------------------------------------
+
+def js_distance(p: np.ndarray, q: np.ndarray) -> float:
+    """D_JS = sqrt(KL(p || m) / 2 + KL(q || m) / 2) with m = (p + q) / 2 (App. A,
+    pattern search).  Natural logarithms; terms with a zero numerator are 0.
+    Reading: the square root is taken, as the listing writes it (a distance)."""
+    p = np.asarray(p, dtype=np.float64)
+    q = np.asarray(q, dtype=np.float64)
+    m = 0.5 * (p + q)
+
+    def kl(a, b):
+        nz = a > 0
+        return float(np.sum(a[nz] * np.log(a[nz] / b[nz])))
+
+    return math.sqrt(max(0.5 * kl(p, m) + 0.5 * kl(q, m), 0.0))
+
+
+def pooled_estimate(q: np.ndarray, k: np.ndarray, block: int, scale: float) -> np.ndarray:
+    """a_bar = Softmax(pool(Q_hat) pool(K)^T s) over the N_b key blocks (App. A, pattern
+    search): Q_hat is the last b = min(B, n) queries pooled to one row (mean), K is
+    pooled per block (mean; a partial last block over its own rows).  Every key
+    block lies at or before Q_hat's block, so no mask applies."""
+    n = q.shape[0]
+    b = min(block, n)
+    qp = q[n - b:].mean(axis=0)
+    z = (pool_blocks(k, block) @ qp) * scale
+    e = np.exp(z - z.max())
+    return e / e.sum()
+
+
+def jsd_score(q: np.ndarray, k: np.ndarray, p_v: np.ndarray, block: int, scale: float) -> float:
+    """The pattern-search score of App. A: D_JS(a_hat, a_bar), where a_hat is the
+    per-query mean of the proxy attention sum-pooled over key blocks -- exactly the
+    vertical block score p_v of Alg. 3 (each proxy row sums to 1, divided by b) --
+    and a_bar the pooled estimate."""
+    return js_distance(p_v, pooled_estimate(q, k, block, scale))
+
+
+def route_jsd(score: float, tau: float) -> int:
+    """VS iff D_JS >= tau (App. A), compared in float32."""
+    return ROUTE_VS if np.float32(score) >= np.float32(tau) else ROUTE_PE
+
+
+def vs_select_gamma(p: np.ndarray, gamma: float, k_min: int) -> List[int]:
+    """FlexPrefill's VS index selection for one direction (App. A): sort the block
+    scores descending and keep the shortest prefix whose cumulative mass reaches
+    gamma; k = min(max(that length, k_min), N_b).
+
+    Readings: the scores are the block scores p_d of Alg. 3 (they already sum to
+    1, the listing's normalisation); order (p desc, block index asc) on the
+    float32 values; float64 cumulative sum against float32(gamma); all blocks if
+    it never reaches gamma; k_min as in Alg. 3; N_b <= 2 selects nothing extra.
+    Returns the selected block indices, ascending."""
+    nb = len(p)
+    if nb <= 2:
+        return []
+    p32 = np.asarray(p, dtype=np.float32)
+    order = sorted(range(nb), key=lambda J: (-float(p32[J]), J))
+    csum = np.cumsum(p32[order].astype(np.float64))
+    hit = np.nonzero(csum >= np.float64(np.float32(gamma)))[0]
+    c = int(hit[0]) + 1 if len(hit) else nb
+    kd = min(max(c, k_min), nb)
+    return sorted(order[:kd])
+
+
+# ----------------------------------------------------------------------------
 # Whole path, per head and per layer (Alg. 1)
 # ----------------------------------------------------------------------------
 
@@ -291,6 +363,7 @@ class HeadResult:
     A_tilde: Optional[np.ndarray] = None
     sets: List[List[int]] = field(default_factory=list)
     out: Optional[np.ndarray] = None
+    jsd: Optional[float] = None
 
 
 def crisp_head(q: np.ndarray, k: np.ndarray, v: Optional[np.ndarray], block: int, params: Params,
@@ -302,11 +375,20 @@ def crisp_head(q: np.ndarray, k: np.ndarray, v: Optional[np.ndarray], block: int
     ahat = proxy_attention(q, k, block, s)
     cs = c_struct(ahat, n, params.w_sink, params.w_local)
     _, _, p_v, p_s = vs_scores(ahat, n, block)
-    res = HeadResult(route=route(cs, params.tau_proxy), c_struct=cs, p_v=p_v, p_s=p_s)
+    if params.route_mode == "jsd":
+        res = HeadResult(route=ROUTE_PE, c_struct=cs, p_v=p_v, p_s=p_s)
+        res.jsd = jsd_score(q, k, p_v, block, s)
+        res.route = route_jsd(res.jsd, params.tau_jsd)
+    else:
+        res = HeadResult(route=route(cs, params.tau_proxy), c_struct=cs, p_v=p_v, p_s=p_s)
     if res.route == ROUTE_VS:
         km = params.k_min(block)
-        res.S_v = vs_select(p_v, params.alpha, km)
-        res.S_s = vs_select(p_s, params.alpha, km)
+        if params.vs_mode == "gamma":
+            res.S_v = vs_select_gamma(p_v, params.gamma, km)
+            res.S_s = vs_select_gamma(p_s, params.gamma, km)
+        else:
+            res.S_v = vs_select(p_v, params.alpha, km)
+            res.S_s = vs_select(p_s, params.alpha, km)
         res.sets = vs_block_sets(res.S_v, res.S_s, nb)
     else:
         At = pe_scores(q, k, block, s)

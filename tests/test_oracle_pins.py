@@ -15,6 +15,9 @@ Stage -> pins:
   PE scores and cutoff (Alg. 4)   P4 closed-form A_tilde and K*, brute-force cutoff, P7 gamma monotone
   block sets                      P9 structure, slash geometry walk
   sparse attention (Eq. 1)        P1 all blocks == dense SDPA, P2 explicit-mask softmax
+  JSD pattern search (App. A)     P10 closed forms and scipy for D_JS, closed-form pooled estimate
+                                  (flat and sink heads), routes by visible-key counting
+  gamma VS selection (App. A)     P10 explicit cases, brute-force minimal subsets, mass-cliff count
 """
 import math
 
@@ -451,3 +454,127 @@ def test_p9_mass_accounting_brute_force():
         outside = sum(row[J * block: min((J + 1) * block, i + 1)].sum()
                       for J in range(i // block + 1) if J not in r.sets[i // block])
         assert abs(inside + outside - 1) < 1e-12
+
+
+# ---------------------------------------------------------------- P10 (FlexPrefill comparator, App. A)
+
+def test_p10_js_distance_closed_forms_and_library():
+    """D_JS: 0 on equal inputs, sqrt(ln 2) on disjoint supports, a closed form for a
+    one-hot against uniform, symmetric, bounded, and equal to scipy's independent
+    jensenshannon (natural logarithm)."""
+    from scipy.spatial.distance import jensenshannon
+    p = np.array([0.2, 0.3, 0.5])
+    assert O.js_distance(p, p) == 0.0
+    assert abs(O.js_distance([1.0, 0.0], [0.0, 1.0]) - math.sqrt(math.log(2))) < 1e-15
+    assert abs(O.js_distance([1.0, 0.0], [0.5, 0.5]) - math.sqrt(0.75 * math.log(4 / 3))) < 1e-15
+    rng = np.random.default_rng(30)
+    for _ in range(50):
+        m = int(rng.integers(1, 40))
+        a = rng.dirichlet(np.full(m, rng.uniform(0.05, 3)))
+        b = rng.dirichlet(np.full(m, rng.uniform(0.05, 3)))
+        if rng.random() < 0.3:
+            a[rng.integers(0, m)] = 0.0
+            a /= a.sum()
+        d = O.js_distance(a, b)
+        assert abs(d - O.js_distance(b, a)) < 1e-15
+        assert 0.0 <= d <= math.sqrt(math.log(2)) + 1e-15
+        assert abs(d - jensenshannon(a, b)) < 1e-12
+
+
+def test_p10_pooled_estimate_flat_and_sink_closed_forms():
+    """Q = 0: the pooled estimate is uniform over the N_b key blocks whatever K is.  A sink
+    head (query carries only the sink tag): pool(K) block 0 = (8 * 4 / 128) e_0, so
+    the pooled logit of block 0 is beta / 32 and every other block's is 0."""
+    n, block = 4096, 128
+    nb = n // block
+    k = bf16_round(np.random.default_rng(31).standard_normal((n, 128)))
+    ab = O.pooled_estimate(np.zeros((n, 128)), k, block, S128)
+    assert np.allclose(ab, 1.0 / nb, rtol=0, atol=1e-16)
+    beta = 40.0
+    q, ks, _ = sink_head(n, beta=beta)
+    ab = O.pooled_estimate(q, ks, block, S128)
+    logit0 = q[0, 0] * (8.0 * 4 / 128) * S128          # q carries bf16(beta sqrt(d) / 8) on dim 0
+    assert abs(logit0 - beta / 32) < 0.01
+    z = math.exp(logit0) + (nb - 1)
+    assert abs(ab[0] - math.exp(logit0) / z) < 1e-14
+    assert np.allclose(ab[1:], 1.0 / z, rtol=1e-14, atol=0)
+
+
+def test_p10_jsd_routes_flat_pe_and_sink_vs():
+    """The flat head's per-block proxy mass follows from counting visible keys; its
+    distance to the uniform pooled estimate is small (routes PE at tau 0.1), while a
+    sink head puts all proxy mass in block 0 (routes VS)."""
+    n, block = 4096, 128
+    nb, b = n // block, block
+    p_flat = np.zeros(nb)
+    for r in range(b):
+        i = n - b + r                      # proxy row r sees keys 0..i
+        for J in range(nb):
+            p_flat[J] += max(0, min((J + 1) * block, i + 1) - J * block) / (i + 1)
+    p_flat /= b
+    k = bf16_round(np.random.default_rng(32).standard_normal((n, 128)))
+    q0 = np.zeros((n, 128))
+    A = O.proxy_attention(q0, k, block, S128)
+    _, _, p_v, _ = O.vs_scores(A, n, block)
+    assert np.allclose(p_v, p_flat, rtol=0, atol=1e-14)
+    d_flat = O.jsd_score(q0, k, p_v, block, S128)
+    assert abs(d_flat - O.js_distance(p_flat, np.full(nb, 1.0 / nb))) < 1e-12
+    assert d_flat < 0.05 and O.route_jsd(d_flat, 0.1) == O.ROUTE_PE
+    q, ks, v = sink_head(n, beta=40.0)
+    res = O.crisp_head(q, ks, v, block, O.Params(route_mode="jsd"), attend=False)
+    assert res.p_v[0] > 1 - 1e-9 and res.jsd > 0.5 and res.route == O.ROUTE_VS
+    assert abs(res.jsd - O.js_distance(res.p_v, O.pooled_estimate(q, ks, block, S128))) < 1e-15
+
+
+def test_p10_gamma_selection_cases():
+    p = np.array([0.5, 0.1, 0.3, 0.1], dtype=np.float32)
+    assert O.vs_select_gamma(p, 0.8, 1) == [0, 2]
+    assert O.vs_select_gamma(p, 0.85, 1) == [0, 1, 2]           # tie at 0.1: lower block first
+    assert O.vs_select_gamma(p, 0.5, 3) == [0, 1, 2]            # k_min raises the budget
+    assert O.vs_select_gamma(p, 1.0, 1) == [0, 1, 2, 3]
+    short = np.array([0.4, 0.3, 0.2, 0.0], dtype=np.float32)    # sums to 0.9 < gamma
+    assert O.vs_select_gamma(short, 0.95, 1) == [0, 1, 2, 3]
+    assert O.vs_select_gamma(np.array([0.6, 0.4]), 0.5, 1) == []  # N_b <= 2: forced blocks cover all
+
+
+def test_p10_gamma_selection_brute_force():
+    """|S| is the smallest number of blocks whose mass can reach gamma (exhaustive search
+    over subsets), and S is a prefix of the (value desc, block asc) order."""
+    import itertools
+    rng = np.random.default_rng(33)
+    for _ in range(60):
+        nb = int(rng.integers(3, 10))
+        p = rng.dirichlet(np.full(nb, rng.uniform(0.2, 2))).astype(np.float32)
+        if rng.random() < 0.3:
+            p[rng.integers(0, nb)] = p[rng.integers(0, nb)]       # plant a tie
+        gamma = float(np.float32(rng.uniform(0.2, 0.99)))
+        vals = p.astype(np.float64)
+        best = nb
+        for size in range(1, nb + 1):
+            if any(sum(vals[list(c)]) >= gamma for c in itertools.combinations(range(nb), size)):
+                best = size
+                break
+        S = O.vs_select_gamma(p, gamma, 1)
+        assert len(S) == max(best, 1)
+        rest = [J for J in range(nb) if J not in S]
+        for J in S:
+            for K in rest:
+                assert p[J] > p[K] or (p[J] == p[K] and J < K)
+
+
+def test_p10_gamma_pulls_in_the_noise_floor_does_not():
+    """App. C's mass cliff in one direction: 3 signal blocks holding 0.8 of the mass and
+    0.2 spread evenly over the other blocks.  gamma = 0.95 has to add
+    ceil(0.15 / noise share) noise blocks; the sink-aware floor keeps the signal."""
+    nb = 100
+    signal = {0: 0.5, 40: 0.2, 70: 0.1}
+    p = np.full(nb, 0.2 / (nb - 3))
+    for J, m in signal.items():
+        p[J] = m
+    p = p.astype(np.float32)
+    noise = float(np.float32(0.2 / (nb - 3)))
+    S = O.vs_select_gamma(p, 0.95, 1)
+    csum_signal = float(sum(np.float64(p[J]) for J in signal))
+    need = math.ceil((float(np.float32(0.95)) - csum_signal) / noise - 1e-9)
+    assert len(S) == 3 + need and set(signal) <= set(S)
+    assert O.vs_select(p, 1.0, 1) == sorted(signal)
