@@ -63,6 +63,16 @@ typedef enum {
 
 enum { CRISP_ROUTE_VS = 0, CRISP_ROUTE_PE = 1 };
 
+/* crisp_params.route_mode: what decides a head's route.
+ *   CRISP_ROUTE_BY_CSTRUCT  C_struct >= tau_proxy (Alg. 2, the paper's method)
+ *   CRISP_ROUTE_BY_JSD      D_JS >= tau_jsd (App. A, FlexPrefill's pattern search)
+ * crisp_params.vs_mode: how a VS head selects blocks per direction.
+ *   CRISP_VS_FLOOR          sink-aware noise floor (Alg. 3, Sec. 4.3)
+ *   CRISP_VS_GAMMA          shortest prefix of the blocks by decreasing score whose
+ *                           mass reaches gamma (App. A, FlexPrefill's VS selection) */
+enum { CRISP_ROUTE_BY_CSTRUCT = 0, CRISP_ROUTE_BY_JSD = 1 };
+enum { CRISP_VS_FLOOR = 0, CRISP_VS_GAMMA = 1 };
+
 /* Layer shape.  H_q % H_kv == 0, H_kv >= 1, n >= 0, head_dim == 128,
  * block in {64, 128}.  n == 0 or H_q == 0 is a valid empty layer: calls return
  * CRISP_OK and launch nothing. */
@@ -81,7 +91,11 @@ typedef struct {
  *   gamma          PE cumulative-mass target, 0 < gamma <= 1
  *   w_sink/w_local anchor windows in tokens: keys [0, w_sink) and [n - w_local, n); >= 0
  *   k_min_blocks   minimum blocks per VS direction; 0 means ceil(1024 / block)
- *   softmax_scale  logit scale; 0 means 1 / sqrt(head_dim)                     */
+ *   softmax_scale  logit scale; 0 means 1 / sqrt(head_dim)
+ * The FlexPrefill comparator of App. A on the same kernels (defaults: the paper's method):
+ *   route_mode     CRISP_ROUTE_BY_CSTRUCT (default) or CRISP_ROUTE_BY_JSD
+ *   vs_mode        CRISP_VS_FLOOR (default) or CRISP_VS_GAMMA (uses gamma)
+ *   tau_jsd        D_JS route threshold, finite; default 0.1 (the paper gives none) */
 typedef struct {
   float alpha;
   float tau_proxy;
@@ -90,6 +104,9 @@ typedef struct {
   int32_t w_local;
   int32_t k_min_blocks;
   float softmax_scale;
+  int32_t route_mode;
+  int32_t vs_mode;
+  float tau_jsd;
 } crisp_params;
 
 /* Fills *p with the paper's defaults listed above. */
@@ -118,8 +135,25 @@ crisp_status crisp_estimate(const crisp_shape* shape, const crisp_params* params
                             float* c_struct, float* p_v, float* p_s,
                             void* workspace, size_t workspace_bytes, crisp_stream stream);
 
+/* FlexPrefill's pattern search (App. A), the comparator's route score.  For each
+ * query head h: a_bar = Softmax(scale * pool(Q_hat) . pool(K)^T) over the N_b key
+ * blocks (Q_hat = the last b queries pooled to one row, K mean-pooled per block,
+ * a partial last block over its own rows) and
+ *   jsd[h] = sqrt(KL(p_v[h] || m) / 2 + KL(a_bar || m) / 2),  m = (p_v[h] + a_bar) / 2,
+ * natural logarithms, p_v[h] being crisp_estimate's vertical block mass (App. A's
+ * per-query mean, sum-pooled over blocks).  Output: jsd float[H_q].  Leaves the
+ * pooled K in the workspace. */
+crisp_status crisp_jsd(const crisp_shape* shape, const crisp_params* params,
+                       const crisp_bf16* q, const crisp_bf16* k, const float* p_v, float* jsd,
+                       void* workspace, size_t workspace_bytes, crisp_stream stream);
+
 /* Stage 3 (Alg. 2 route; Alg. 3 with the noise floor of Sec. 4.3; Alg. 4).
- * route[h] = VS iff c_struct[h] >= tau_proxy (float32 compare), else PE.
+ * c_struct is the route score: C_struct from crisp_estimate, or, with route_mode
+ * CRISP_ROUTE_BY_JSD, D_JS from crisp_jsd.  route[h] = VS iff score >= tau_proxy
+ * (tau_jsd for D_JS), float32 compare, else PE.  With vs_mode CRISP_VS_GAMMA a VS
+ * direction takes the shortest prefix of its blocks ordered by decreasing p_d (ties:
+ * lower block first) whose mass reaches gamma, then k = min(max(that, k_min), N_b)
+ * as below (all blocks if the mass never reaches gamma).
  * VS head, per direction d in {v, s}: r = max((1 - p_d[0]) - p_d[N_b-1], 0),
  *   mu = r / (N_b - 2), c = #{J : p_d[J] > alpha * mu}, k = min(max(c, k_min), N_b),
  *   S_d = the k largest p_d (ties: lower block index first); nothing when N_b <= 2.
@@ -156,7 +190,8 @@ crisp_status crisp_sparse_attn(const crisp_shape* shape, float softmax_scale,
                                int64_t col_cap_per_head, crisp_bf16* o,
                                void* workspace_or_null, size_t workspace_bytes, crisp_stream stream);
 
-/* Alg. 1: all stages on `stream`: estimate, route and select, sparse attention.
+/* Alg. 1: all stages on `stream`: estimate, route and select, sparse attention
+ * (with route_mode CRISP_ROUTE_BY_JSD, crisp_jsd's pattern search before the route).
  * route_or_null, row_ptr_or_null and col_idx_or_null, if all three are given,
  * receive the route and block lists (col_idx capacity crisp_col_capacity per
  * head); if they are all null the library keeps them in the workspace (then

@@ -29,7 +29,8 @@ class CrispShape(ctypes.Structure):
 class CrispParams(ctypes.Structure):
     _fields_ = [("alpha", ctypes.c_float), ("tau_proxy", ctypes.c_float), ("gamma", ctypes.c_float),
                 ("w_sink", ctypes.c_int32), ("w_local", ctypes.c_int32), ("k_min_blocks", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float)]
+                ("softmax_scale", ctypes.c_float), ("route_mode", ctypes.c_int32), ("vs_mode", ctypes.c_int32),
+                ("tau_jsd", ctypes.c_float)]
 
 
 class CrispError(RuntimeError):
@@ -50,6 +51,7 @@ def _load(path: str = _LIB_PATH):
         "crisp_workspace_size": (ctypes.c_int, [sh, ctypes.POINTER(SZ)]),
         "crisp_prefill_workspace_size": (ctypes.c_int, [sh, ctypes.POINTER(SZ)]),
         "crisp_estimate": (ctypes.c_int, [sh, pa, P, P, P, P, P, P, SZ, P]),
+        "crisp_jsd": (ctypes.c_int, [sh, pa, P, P, P, P, P, SZ, P]),
         "crisp_route_select": (ctypes.c_int, [sh, pa, P, P, P, P, P, P, P, P, I64, P, P, SZ, P]),
         "crisp_sparse_workspace_size": (ctypes.c_int, [sh, ctypes.POINTER(SZ)]),
         "crisp_sparse_attn": (ctypes.c_int, [sh, F, P, P, P, P, P, I64, P, P, SZ, P]),
@@ -67,8 +69,12 @@ def _load(path: str = _LIB_PATH):
 
 lib = _load()
 EXPORTED = ("crisp_params_default", "crisp_col_capacity", "crisp_workspace_size", "crisp_prefill_workspace_size",
-            "crisp_sparse_workspace_size", "crisp_estimate", "crisp_route_select", "crisp_sparse_attn", "crisp_prefill_attn", "crisp_dense_attn",
-            "crisp_status_string", "crisp_last_error")
+            "crisp_sparse_workspace_size", "crisp_estimate", "crisp_jsd", "crisp_route_select", "crisp_sparse_attn",
+            "crisp_prefill_attn", "crisp_dense_attn", "crisp_status_string", "crisp_last_error")
+
+# route_mode / vs_mode values (include/crisp.h)
+ROUTE_BY_CSTRUCT, ROUTE_BY_JSD = 0, 1
+VS_FLOOR, VS_GAMMA = 0, 1
 
 
 def _check(status: int, what: str):
@@ -78,8 +84,14 @@ def _check(status: int, what: str):
 
 
 def make_params(alpha=1.0, tau_proxy=0.2, gamma=0.95, w_sink=128, w_local=128, k_min_blocks=0,
-                softmax_scale=0.0) -> CrispParams:
-    return CrispParams(alpha, tau_proxy, gamma, w_sink, w_local, k_min_blocks, softmax_scale)
+                softmax_scale=0.0, route_mode=ROUTE_BY_CSTRUCT, vs_mode=VS_FLOOR, tau_jsd=0.1) -> CrispParams:
+    return CrispParams(alpha, tau_proxy, gamma, w_sink, w_local, k_min_blocks, softmax_scale, route_mode, vs_mode,
+                       tau_jsd)
+
+
+def flexprefill_params(gamma=0.95, tau_jsd=0.1, **kw) -> CrispParams:
+    """The FlexPrefill comparator (App. A): JSD routing and gamma-coverage VS selection."""
+    return make_params(gamma=gamma, tau_jsd=tau_jsd, route_mode=ROUTE_BY_JSD, vs_mode=VS_GAMMA, **kw)
 
 
 def crisp_params_default() -> CrispParams:
@@ -153,11 +165,25 @@ def crisp_estimate(q: torch.Tensor, k: torch.Tensor, params: CrispParams, block:
     return cs, pv, ps
 
 
+def crisp_jsd(q: torch.Tensor, k: torch.Tensor, p_v: torch.Tensor, params: CrispParams, block: int = 128,
+              ws: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """FlexPrefill's pattern search (App. A) -> D_JS per query head, float32 [H_q]."""
+    _inputs(q, k)
+    sh = shape_of(q, k, block)
+    dev = q.device
+    jsd = torch.empty(q.shape[0], dtype=torch.float32, device=dev)
+    ws = workspace(sh, dev) if ws is None else ws
+    _check(lib.crisp_jsd(ctypes.byref(sh), ctypes.byref(params), _ptr(q), _ptr(k), _ptr(p_v), _ptr(jsd), _ptr(ws),
+                         ws.numel(), _stream(dev)), "crisp_jsd")
+    return jsd
+
+
 def crisp_route_select(q: torch.Tensor, k: torch.Tensor, c_struct: torch.Tensor, p_v: torch.Tensor,
                        p_s: torch.Tensor, params: CrispParams, block: int = 128, want_mask: bool = True,
                        ws: Optional[torch.Tensor] = None):
     """Stage 3 -> (route int8 [H_q], row_ptr int32 [H_q, N_b+1], col_idx int32 [H_q, cap],
-    dir_mask uint8 [H_q, 2, N_b] or None)."""
+    dir_mask uint8 [H_q, 2, N_b] or None).  c_struct is the route score: C_struct, or D_JS
+    from crisp_jsd when params.route_mode is ROUTE_BY_JSD."""
     _inputs(q, k)
     sh = shape_of(q, k, block)
     nb = n_blocks(q.shape[1], block)

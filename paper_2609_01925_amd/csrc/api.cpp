@@ -61,11 +61,18 @@ crisp_status check_params(const crisp_params* p, const Dims& d) {
   if (p->k_min_blocks < 0) return fail(CRISP_EINVAL, "k_min_blocks must be >= 0");
   if (!(p->softmax_scale >= 0.f) || !isfinite(p->softmax_scale))
     return fail(CRISP_EINVAL, "softmax_scale must be finite and >= 0");
+  if (p->route_mode != CRISP_ROUTE_BY_CSTRUCT && p->route_mode != CRISP_ROUTE_BY_JSD)
+    return fail(CRISP_EINVAL, "route_mode %d unknown", p->route_mode);
+  if (p->vs_mode != CRISP_VS_FLOOR && p->vs_mode != CRISP_VS_GAMMA)
+    return fail(CRISP_EINVAL, "vs_mode %d unknown", p->vs_mode);
+  if (!isfinite(p->tau_jsd)) return fail(CRISP_EINVAL, "tau_jsd must be finite");
   (void)d;
   return CRISP_OK;
 }
 
 float scale_of(float s) { return s > 0.f ? s : 1.0f / sqrtf((float)kHeadDim); }
+
+float route_tau(const crisp_params* p) { return p->route_mode == CRISP_ROUTE_BY_JSD ? p->tau_jsd : p->tau_proxy; }
 
 int kmin_of(const crisp_params* p, int B) { return p->k_min_blocks > 0 ? p->k_min_blocks : (1024 + B - 1) / B; }
 
@@ -163,6 +170,9 @@ void crisp_params_default(crisp_params* p) {
   p->w_local = 128;
   p->k_min_blocks = 0;
   p->softmax_scale = 0.0f;
+  p->route_mode = CRISP_ROUTE_BY_CSTRUCT;
+  p->vs_mode = CRISP_VS_FLOOR;
+  p->tau_jsd = 0.1f;
 }
 
 int64_t crisp_col_capacity(const crisp_shape* shape) {
@@ -207,6 +217,25 @@ crisp_status crisp_estimate(const crisp_shape* shape, const crisp_params* params
                     "crisp_estimate launch");
 }
 
+crisp_status crisp_jsd(const crisp_shape* shape, const crisp_params* params, const crisp_bf16* q,
+                       const crisp_bf16* k, const float* p_v, float* jsd, void* workspace, size_t workspace_bytes,
+                       crisp_stream stream) {
+  Dims d;
+  CHECK(check_shape(shape, &d));
+  CHECK(check_params(params, d));
+  if (empty(d)) return CRISP_OK;
+  CHECK(check_ptr(q, 16, "q"));
+  CHECK(check_ptr(k, 16, "k"));
+  CHECK(check_ptr(p_v, 4, "p_v"));
+  CHECK(check_ptr(jsd, 4, "jsd"));
+  CHECK(check_ptr(workspace, 256, "workspace"));
+  if (workspace_bytes < ws_layout(d).total)
+    return fail(CRISP_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, ws_layout(d).total);
+  return hip_status(launch_jsd(d, scale_of(params->softmax_scale), q, k, p_v, jsd, (char*)workspace,
+                               (hipStream_t)stream),
+                    "crisp_jsd launch");
+}
+
 crisp_status crisp_route_select(const crisp_shape* shape, const crisp_params* params, const crisp_bf16* q,
                                 const crisp_bf16* k, const float* c_struct, const float* p_v, const float* p_s,
                                 int8_t* route, int32_t* row_ptr, int32_t* col_idx, int64_t col_cap_per_head,
@@ -230,10 +259,10 @@ crisp_status crisp_route_select(const crisp_shape* shape, const crisp_params* pa
                 (long long)d.cap);
   if (workspace_bytes < ws_layout(d).total)
     return fail(CRISP_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, ws_layout(d).total);
-  return hip_status(launch_select(d, scale_of(params->softmax_scale), params->alpha, params->tau_proxy,
-                                  params->gamma, kmin_of(params, d.B), q, k, c_struct, p_v, p_s, route, row_ptr,
-                                  col_idx, col_cap_per_head, dir_mask_or_null, (char*)workspace,
-                                  (hipStream_t)stream),
+  return hip_status(launch_select(d, scale_of(params->softmax_scale), params->alpha, route_tau(params),
+                                  params->gamma, kmin_of(params, d.B), params->vs_mode, false, q, k, c_struct, p_v,
+                                  p_s, route, row_ptr, col_idx, col_cap_per_head, dir_mask_or_null,
+                                  (char*)workspace, (hipStream_t)stream),
                     "crisp_route_select launch");
 }
 
@@ -322,8 +351,11 @@ crisp_status crisp_prefill_attn(const crisp_shape* shape, const crisp_params* pa
   hipStream_t st = (hipStream_t)stream;
   CHECK(hip_status(launch_estimate(d, scale, params->w_sink, params->w_local, q, k, cs, pv, ps, ws, st),
                    "crisp_prefill_attn estimate launch"));
-  CHECK(hip_status(launch_select(d, scale, params->alpha, params->tau_proxy, params->gamma, kmin_of(params, d.B), q,
-                                 k, cs, pv, ps, route, rp, ci, d.cap, nullptr, ws, st),
+  const bool by_jsd = params->route_mode == CRISP_ROUTE_BY_JSD;
+  if (by_jsd)  // the route score slot then holds D_JS instead of C_struct
+    CHECK(hip_status(launch_jsd(d, scale, q, k, pv, cs, ws, st), "crisp_prefill_attn pattern search launch"));
+  CHECK(hip_status(launch_select(d, scale, params->alpha, route_tau(params), params->gamma, kmin_of(params, d.B),
+                                 params->vs_mode, by_jsd, q, k, cs, pv, ps, route, rp, ci, d.cap, nullptr, ws, st),
                    "crisp_prefill_attn select launch"));
   return hip_status(launch_attn(d, scale, q, k, v, rp, ci, d.cap, false, o, ws + L.sched, st),
                     "crisp_prefill_attn attention launch");

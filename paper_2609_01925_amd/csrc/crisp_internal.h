@@ -40,9 +40,15 @@ hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, 
                            const uint16_t* k, float* c_struct, float* p_v, float* p_s, char* ws,
                            hipStream_t stream);
 
-hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, float gamma, int k_min,
-                         const uint16_t* q, const uint16_t* k, const float* c_struct, const float* p_v,
-                         const float* p_s, int8_t* route, int32_t* row_ptr, int32_t* col_idx,
+// route_score is C_struct (tau = tau_proxy) or D_JS (tau = tau_jsd); vs_mode 0 is the
+// noise floor, 1 gamma coverage; kbar_all: K_bar of every KV group is already in ws.
+hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, float gamma, int k_min, int vs_mode,
+                         bool kbar_all, const uint16_t* q, const uint16_t* k, const float* route_score,
+                         const float* p_v, const float* p_s, int8_t* route, int32_t* row_ptr, int32_t* col_idx,
                          int64_t col_cap, uint8_t* dir_mask, char* ws, hipStream_t stream);
+
+// D_JS per query head into jsd[hq]; leaves K_bar of every KV group in ws.
+hipError_t launch_jsd(const Dims& d, float scale, const uint16_t* q, const uint16_t* k, const float* p_v,
+                      float* jsd, char* ws, hipStream_t stream);
 
 }  // namespace crisp

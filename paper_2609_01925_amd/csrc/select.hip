@@ -40,7 +40,7 @@ struct RState {
 struct SelArgs {
   const uint16_t* q;
   const uint16_t* k;
-  const float* c_struct;
+  const float* c_struct;  // route score: C_struct, or D_JS in the pattern-search mode
   const float* p_v;
   const float* p_s;
   int8_t* route;
@@ -52,6 +52,8 @@ struct SelArgs {
   float c2;  // softmax scale * log2(e)
   float alpha, tau, gamma;
   int k_min;
+  int vs_mode;   // 0: noise floor (Alg. 3), 1: gamma coverage per direction (App. A)
+  int kbar_all;  // 1: K_bar of every KV group is already in kbar (the JSD pattern search pooled it)
   int64_t cap;  // nb * (nb + 1) / 2
   uint8_t* masks;
   float* qbar;
@@ -139,41 +141,10 @@ __device__ uint32_t kth_largest(const float* p, int nb, int k, uint32_t* hist, i
   return prefix;
 }
 
-// Route (Alg. 2) and VS selection per direction (Alg. 3).  grid (hq, 2), 1024 threads.
-__global__ __launch_bounds__(1024) void sel_route_vs(SelArgs a) {
-  __shared__ uint32_t hist[256];
-  __shared__ int wtot[16];
-  __shared__ int sh[2];
-  const int h = blockIdx.x, dir = blockIdx.y, tid = threadIdx.x;
-  const bool vs = a.c_struct[h] >= a.tau;
-  if (dir == 0 && tid == 0) a.route[h] = vs ? 0 : 1;
-  const int nb = a.nb;
-  const float* p = (dir == 0 ? a.p_v : a.p_s) + (size_t)h * nb;
-  uint8_t* m = a.masks + ((size_t)h * 2 + dir) * nb;
-  uint8_t* dm = a.dir_mask ? a.dir_mask + ((size_t)h * 2 + dir) * nb : nullptr;
-  if (!vs || nb <= 2) {
-    for (int J = tid; J < nb; J += 1024) {
-      m[J] = 0;
-      if (dm) dm[J] = 0;
-    }
-    return;
-  }
-  const float r = fmaxf((1.0f - p[0]) - p[nb - 1], 0.0f);
-  const float mu = r / (float)(nb - 2);
-  const float thr = a.alpha * mu;
-  int c = 0;
-  for (int J = tid; J < nb; J += 1024) c += p[J] > thr;
-  c = block_sum_1024(c, wtot);
-  int kd = c > a.k_min ? c : a.k_min;
-  kd = kd < nb ? kd : nb;
-  if (kd == c) {
-    for (int J = tid; J < nb; J += 1024) {
-      const uint8_t s = p[J] > thr;
-      m[J] = s;
-      if (dm) dm[J] = s;
-    }
-    return;
-  }
+// Marks the kd largest p (ties: lower block first) in m (and dm).  1024 threads.
+__device__ void select_top_k(const float* p, int nb, int kd, uint8_t* m, uint8_t* dm, uint32_t* hist, int* sh,
+                             int* wtot) {
+  const int tid = threadIdx.x;
   const uint32_t t = kth_largest(p, nb, kd, hist, sh);
   int ngt = 0;
   for (int J = tid; J < nb; J += 1024) ngt += fbits(p[J]) > t;
@@ -195,26 +166,135 @@ __global__ __launch_bounds__(1024) void sel_route_vs(SelArgs a) {
   }
 }
 
-// Mean-pool Q of PE heads and K of KV groups with a PE head (Alg. 4).  grid (nb, hq + hkv), 256 threads.
-__global__ __launch_bounds__(256) void sel_pool(SelArgs a) {
-  __shared__ float red[16][128];
-  const int J = blockIdx.x, y = blockIdx.y, tid = threadIdx.x;
-  const uint16_t* src;
-  float* dst;
-  if (y < a.hq) {
-    if (a.route[y] != 1) return;
-    src = a.q + (size_t)y * a.n * kHeadDim;
-    dst = a.qbar + ((size_t)y * a.nb + J) * kHeadDim;
-  } else {
-    const int g = y - a.hq;
-    bool any = false;
-    for (int i = 0; i < a.G; ++i) any |= a.route[g * a.G + i] == 1;
-    if (!any) return;
-    src = a.k + (size_t)g * a.n * kHeadDim;
-    dst = a.kbar + ((size_t)g * a.nb + J) * kHeadDim;
+// Gamma prefix of one direction (App. A, VS index selection): the blocks taken in
+// order of decreasing p (ties: lower block first) until their mass reaches gamma.
+// A mass-weighted radix select over the float bit patterns (11 + 11 + 10 bits),
+// masses in 2^-60 fixed point so the sums are exact and order-independent: t is
+// the value of the last block taken and `ceq` how many blocks equal to t (in
+// block order) complete the mass.  Returns the number of blocks taken, or nb
+// (with *all = 1) when the total mass never reaches gamma.  1024 threads.
+__device__ int gamma_prefix(const float* p, int nb, float gamma, uint32_t* t_out, int* ceq_out, int* all_out,
+                            unsigned long long* hist, unsigned long long* sh64, int* wtot) {
+  const int tid = threadIdx.x;
+  unsigned long long need = (unsigned long long)ceil((double)gamma * kFix);
+  uint32_t prefix = 0, pmask = 0;
+  int all = 0;
+  const int shifts[3] = {21, 10, 0};
+  const int widths[3] = {11, 11, 10};
+#pragma unroll
+  for (int pass = 0; pass < 3; ++pass) {
+    if (all) break;
+    const int shift = shifts[pass], bins = 1 << widths[pass];
+    for (int i = tid; i < bins; i += 1024) hist[i] = 0ull;
+    __syncthreads();
+    for (int J = tid; J < nb; J += 1024) {
+      const uint32_t b = fbits(p[J]);
+      if ((b & pmask) == prefix) atomicAdd(&hist[(b >> shift) & (uint32_t)(bins - 1)], fixed_mass(b));
+    }
+    __syncthreads();
+    if (tid == 0) {
+      unsigned long long cum = 0;
+      int d = bins - 1;
+      for (; d >= 0; --d) {
+        if (cum + hist[d] >= need) break;
+        cum += hist[d];
+      }
+      sh64[0] = d < 0 ? ~0ull : (unsigned long long)d;
+      sh64[1] = d < 0 ? 0ull : need - cum;
+    }
+    __syncthreads();
+    if (sh64[0] == ~0ull) {
+      all = 1;
+    } else {
+      prefix |= (uint32_t)sh64[0] << shift;
+      pmask |= (uint32_t)(bins - 1) << shift;
+      need = sh64[1];
+    }
+    __syncthreads();
   }
-  const int r0 = J * a.B;
-  const int r1 = r0 + a.B < a.n ? r0 + a.B : a.n;
+  *all_out = all;
+  if (all) return nb;
+  const unsigned long long mt = fixed_mass(prefix);
+  // mt > 0: the digit search only stops on a bin holding mass
+  const int ceq = (int)((need + mt - 1) / mt);
+  int gt = 0;
+  for (int J = tid; J < nb; J += 1024) gt += fbits(p[J]) > prefix;
+  gt = block_sum_1024(gt, wtot);
+  *t_out = prefix;
+  *ceq_out = ceq;
+  return gt + ceq;
+}
+
+// Route (Alg. 2, or App. A's pattern search when the score is D_JS) and VS selection
+// per direction (Alg. 3, or App. A's gamma coverage).  grid (hq, 2), 1024 threads.
+__global__ __launch_bounds__(1024) void sel_route_vs(SelArgs a) {
+  __shared__ uint32_t hist[256];
+  __shared__ unsigned long long hist64[2048];
+  __shared__ unsigned long long sh64[2];
+  __shared__ int wtot[16];
+  __shared__ int sh[2];
+  const int h = blockIdx.x, dir = blockIdx.y, tid = threadIdx.x;
+  const bool vs = a.c_struct[h] >= a.tau;
+  if (dir == 0 && tid == 0) a.route[h] = vs ? 0 : 1;
+  const int nb = a.nb;
+  const float* p = (dir == 0 ? a.p_v : a.p_s) + (size_t)h * nb;
+  uint8_t* m = a.masks + ((size_t)h * 2 + dir) * nb;
+  uint8_t* dm = a.dir_mask ? a.dir_mask + ((size_t)h * 2 + dir) * nb : nullptr;
+  if (!vs || nb <= 2) {
+    for (int J = tid; J < nb; J += 1024) {
+      m[J] = 0;
+      if (dm) dm[J] = 0;
+    }
+    return;
+  }
+  if (a.vs_mode == 1) {
+    uint32_t t = 0;
+    int ceq = 0, all = 0;
+    const int c = gamma_prefix(p, nb, a.gamma, &t, &ceq, &all, hist64, sh64, wtot);
+    int kd = c > a.k_min ? c : a.k_min;
+    kd = kd < nb ? kd : nb;
+    if (kd == c) {
+      int running = 0;
+      for (int base = 0; base < nb; base += 1024) {
+        const int J = base + tid;
+        const uint32_t b = J < nb ? fbits(p[J]) : 0u;
+        const int eq = J < nb && b == t;
+        int tot;
+        const int rank = running + block_scan_1024(eq, wtot, &tot);
+        if (J < nb) {
+          const uint8_t s = all || (b > t) || (eq && rank < ceq);
+          m[J] = s;
+          if (dm) dm[J] = s;
+        }
+        running += tot;
+      }
+      return;
+    }
+    select_top_k(p, nb, kd, m, dm, hist, sh, wtot);
+    return;
+  }
+  const float r = fmaxf((1.0f - p[0]) - p[nb - 1], 0.0f);
+  const float mu = r / (float)(nb - 2);
+  const float thr = a.alpha * mu;
+  int c = 0;
+  for (int J = tid; J < nb; J += 1024) c += p[J] > thr;
+  c = block_sum_1024(c, wtot);
+  int kd = c > a.k_min ? c : a.k_min;
+  kd = kd < nb ? kd : nb;
+  if (kd == c) {
+    for (int J = tid; J < nb; J += 1024) {
+      const uint8_t s = p[J] > thr;
+      m[J] = s;
+      if (dm) dm[J] = s;
+    }
+    return;
+  }
+  select_top_k(p, nb, kd, m, dm, hist, sh, wtot);
+}
+
+// Mean of rows [r0, r1) of a [rows][128] bf16 tensor into dst[0..128) (fp32).  256 threads.
+__device__ void pool_rows(const uint16_t* src, int r0, int r1, float* dst, float (*red)[128]) {
+  const int tid = threadIdx.x;
   const int c = tid & 15, rg = tid >> 4;
   float acc[8];
 #pragma unroll
@@ -235,6 +315,103 @@ __global__ __launch_bounds__(256) void sel_pool(SelArgs a) {
     for (int i = 0; i < 16; ++i) s += red[i][tid];
     dst[tid] = s / (float)(r1 - r0);
   }
+}
+
+// Mean-pool Q of PE heads and K of KV groups with a PE head (Alg. 4).  grid (nb, hq + hkv), 256 threads.
+__global__ __launch_bounds__(256) void sel_pool(SelArgs a) {
+  __shared__ float red[16][128];
+  const int J = blockIdx.x, y = blockIdx.y;
+  const uint16_t* src;
+  float* dst;
+  if (y < a.hq) {
+    if (a.route[y] != 1) return;
+    src = a.q + (size_t)y * a.n * kHeadDim;
+    dst = a.qbar + ((size_t)y * a.nb + J) * kHeadDim;
+  } else {
+    if (a.kbar_all) return;
+    const int g = y - a.hq;
+    bool any = false;
+    for (int i = 0; i < a.G; ++i) any |= a.route[g * a.G + i] == 1;
+    if (!any) return;
+    src = a.k + (size_t)g * a.n * kHeadDim;
+    dst = a.kbar + ((size_t)g * a.nb + J) * kHeadDim;
+  }
+  const int r0 = J * a.B;
+  pool_rows(src, r0, r0 + a.B < a.n ? r0 + a.B : a.n, dst, red);
+}
+
+// ---------------------------------------------------------------------------
+// FlexPrefill's pattern search (App. A): D_JS between the proxy's per-block mass
+// p_v (App. A's per-query mean, sum-pooled over key blocks) and the pooled
+// estimate softmax(pool(Q_hat) pool(K)^T * scale) over the N_b key blocks.
+struct JsdArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const float* p_v;
+  float* jsd;
+  float* kbar;  // [hkv][nb][128] fp32
+  float* zbuf;  // [hq][nb] fp32 pooled logits
+  int n, nb, B, b, hq, hkv, G;
+  float scale;
+};
+
+// K_bar of every KV group.  grid (nb, hkv), 256 threads.
+__global__ __launch_bounds__(256) void jsd_pool_k(JsdArgs a) {
+  __shared__ float red[16][128];
+  const int J = blockIdx.x, g = blockIdx.y;
+  const int r0 = J * a.B;
+  pool_rows(a.k + (size_t)g * a.n * kHeadDim, r0, r0 + a.B < a.n ? r0 + a.B : a.n,
+            a.kbar + ((size_t)g * a.nb + J) * kHeadDim, red);
+}
+
+__device__ double block_sum_256d(double x, double* red) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  const int tid = threadIdx.x;
+  if ((tid & 63) == 0) red[tid >> 6] = x;
+  __syncthreads();
+  const double s = (red[0] + red[1]) + (red[2] + red[3]);
+  __syncthreads();
+  return s;
+}
+
+// One query head per workgroup, 256 threads: pooled last query block, logits
+// against K_bar (one wave per key block), softmax and the two KL terms in fp64.
+__global__ __launch_bounds__(256) void jsd_score(JsdArgs a) {
+  __shared__ float red[16][128];
+  __shared__ float qm[128];
+  __shared__ float fred[4];
+  __shared__ double dred[4];
+  const int h = blockIdx.x, g = h / a.G, tid = threadIdx.x, l = tid & 63, w = tid >> 6;
+  pool_rows(a.q + (size_t)h * a.n * kHeadDim, a.n - a.b, a.n, qm, red);
+  __syncthreads();
+  const float* kb = a.kbar + (size_t)g * a.nb * kHeadDim;
+  float* z = a.zbuf + (size_t)h * a.nb;
+  const float q0 = qm[2 * l], q1 = qm[2 * l + 1];
+  float mx = -__builtin_inff();
+  for (int J = w; J < a.nb; J += 4) {
+    const float* kr = kb + (size_t)J * kHeadDim + 2 * l;
+    const float d = wave_sum(q0 * kr[0] + q1 * kr[1]) * a.scale;
+    if (l == 0) z[J] = d;
+    mx = fmaxf(mx, d);
+  }
+  if (l == 0) fred[w] = mx;
+  __syncthreads();  // also publishes the z written by lane 0 of every wave
+  mx = fmaxf(fmaxf(fred[0], fred[1]), fmaxf(fred[2], fred[3]));
+  double s = 0.0;
+  for (int J = tid; J < a.nb; J += 256) s += (double)expf(z[J] - mx);
+  s = block_sum_256d(s, dred);
+  double t = 0.0;
+  const float* pv = a.p_v + (size_t)h * a.nb;
+  for (int J = tid; J < a.nb; J += 256) {
+    const double ab = (double)expf(z[J] - mx) / s;
+    const double ah = (double)pv[J];
+    const double m = 0.5 * (ah + ab);
+    if (ah > 0.0) t += ah * log(ah / m);
+    if (ab > 0.0) t += ab * log(ab / m);
+  }
+  t = block_sum_256d(t, dred);
+  if (tid == 0) a.jsd[h] = (float)sqrt(fmax(0.5 * t, 0.0));
 }
 
 // Pooled logits (log2 domain), 64 x 64 tiles of the block-causal triangle.  grid (ntri, hq), 256 threads.
@@ -564,18 +741,34 @@ __global__ __launch_bounds__(256) void sel_csr_fill(SelArgs a) {
 
 }  // namespace
 
-hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, float gamma, int k_min,
-                         const uint16_t* q, const uint16_t* k, const float* c_struct, const float* p_v,
-                         const float* p_s, int8_t* route, int32_t* row_ptr, int32_t* col_idx,
+hipError_t launch_jsd(const Dims& d, float scale, const uint16_t* q, const uint16_t* k, const float* p_v,
+                      float* jsd, char* ws, hipStream_t stream) {
+  if (d.n == 0 || d.hq == 0) return hipSuccess;
+  const WsLayout L = ws_layout(d);
+  JsdArgs a;
+  a.q = q; a.k = k; a.p_v = p_v; a.jsd = jsd;
+  a.kbar = reinterpret_cast<float*>(ws + L.kbar);
+  a.zbuf = reinterpret_cast<float*>(ws + L.atil);  // free until the PE scores of stage 3
+  a.n = d.n; a.nb = d.nb; a.B = d.B; a.b = d.b; a.hq = d.hq; a.hkv = d.hkv; a.G = d.G;
+  a.scale = scale;
+  hipLaunchKernelGGL(jsd_pool_k, dim3(d.nb, d.hkv), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(jsd_score, dim3(d.hq), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, float gamma, int k_min, int vs_mode,
+                         bool kbar_all, const uint16_t* q, const uint16_t* k, const float* route_score,
+                         const float* p_v, const float* p_s, int8_t* route, int32_t* row_ptr, int32_t* col_idx,
                          int64_t col_cap, uint8_t* dir_mask, char* ws, hipStream_t stream) {
   if (d.n == 0 || d.hq == 0) return hipSuccess;
   const WsLayout L = ws_layout(d);
   SelArgs a;
-  a.q = q; a.k = k; a.c_struct = c_struct; a.p_v = p_v; a.p_s = p_s;
+  a.q = q; a.k = k; a.c_struct = route_score; a.p_v = p_v; a.p_s = p_s;
   a.route = route; a.row_ptr = row_ptr; a.col_idx = col_idx; a.col_cap = col_cap; a.dir_mask = dir_mask;
   a.n = d.n; a.nb = d.nb; a.B = d.B; a.hq = d.hq; a.hkv = d.hkv; a.G = d.G;
   a.c2 = scale * kLog2e;
   a.alpha = alpha; a.tau = tau; a.gamma = gamma; a.k_min = k_min;
+  a.vs_mode = vs_mode; a.kbar_all = kbar_all ? 1 : 0;
   a.cap = d.cap;
   a.masks = reinterpret_cast<uint8_t*>(ws + L.masks);
   a.qbar = reinterpret_cast<float*>(ws + L.qbar);

@@ -12,8 +12,14 @@ flip them:
   E4  PE cutoff band:  pairs with |A~ - t*| <= 1e-4 t*, t* = A~ of the last pair
                        taken; if the cumulative mass before or at the cutoff is
                        within 1e-4 gamma of gamma, the pairs at K* and K*+1 too
+  E5  JSD route band:  |D_JS - tau_jsd| <= JSD_BAND (the oracle's D_JS)
+  E6  VS gamma band:   blocks with |p_d[J] - t| <= 1e-4 t, t = p_d of the last block
+                       taken; if the cumulative mass before or at the cutoff is within
+                       1e-4 gamma of gamma, the blocks at positions k and k+1 too
 Floating-point outputs: attention max-abs <= 2e-2 and mean-abs <= 2e-3 (bf16 against
-the float64 oracle); C_struct abs 1e-5; p_v, p_s rtol 1e-4 with atol 1e-7.
+the float64 oracle); C_struct abs 1e-5; p_v, p_s rtol 1e-4 with atol 1e-7; D_JS abs
+JSD_ABS (the pooled estimate in fp32 from bf16 inputs; a p_v error of 1e-6 relative
+moves D_JS by far less).
 """
 from __future__ import annotations
 
@@ -26,6 +32,8 @@ ATTN_MAX_ABS = 2e-2
 ATTN_MEAN_ABS = 2e-3
 CS_ABS = 1e-5
 P_RTOL, P_ATOL = 1e-4, 1e-7
+JSD_ABS = 1e-4
+JSD_BAND = 1e-3
 
 
 def csr_to_sets(row_ptr: np.ndarray, col_idx: np.ndarray, h: int, nb: int):
@@ -70,6 +78,36 @@ def compare_vs(gpu_mask: np.ndarray, ores: O.HeadResult, alpha: float, k_min: in
         diff = gsel ^ set(S)
         bad = diff - ex
         assert not bad, f"{where} dir {'vs'[dir_]}: blocks {sorted(bad)[:20]} differ (gpu {sorted(gsel)[:30]}, oracle {S[:30]})"
+        assert len(gsel) >= min(k_min, nb), f"{where} dir {'vs'[dir_]}: only {len(gsel)} blocks"
+
+
+def gamma_direction_info(p: np.ndarray, gamma: float, k_min: int):
+    """(order, k, c, t, csum_before, csum_at) of the oracle's gamma selection of one direction."""
+    nb = len(p)
+    p32 = np.asarray(p, dtype=np.float32)
+    order = sorted(range(nb), key=lambda J: (-float(p32[J]), J))
+    csum = np.cumsum(p32[order].astype(np.float64))
+    hit = np.nonzero(csum >= np.float64(np.float32(gamma)))[0]
+    c = int(hit[0]) + 1 if len(hit) else nb
+    kd = min(max(c, k_min), nb)
+    return order, kd, c, float(p32[order[kd - 1]]), float(csum[kd - 2]) if kd >= 2 else 0.0, float(csum[kd - 1])
+
+
+def compare_vs_gamma(gpu_mask: np.ndarray, ores: O.HeadResult, gamma: float, k_min: int, where=""):
+    """gpu_mask: uint8 [2, N_b] of a VS head selected by gamma coverage; E6 exemptions."""
+    nb = gpu_mask.shape[1]
+    g = float(np.float32(gamma))
+    for dir_, (p, S) in enumerate(((ores.p_v, ores.S_v), (ores.p_s, ores.S_s))):
+        gsel = set(np.nonzero(gpu_mask[dir_])[0].tolist())
+        if nb <= 2:
+            assert not gsel, where
+            continue
+        order, kd, c, t, cb, ca = gamma_direction_info(p, gamma, k_min)
+        ex = {J for J in range(nb) if abs(p[J] - t) <= BAND * t}
+        if abs(cb - g) <= BAND * g or abs(ca - g) <= BAND * g:
+            ex |= {order[i] for i in (kd - 1, kd) if 0 <= i < nb}
+        bad = (gsel ^ set(S)) - ex
+        assert not bad, f"{where} dir {'vs'[dir_]}: blocks {sorted(bad)[:20]} differ (gpu {len(gsel)}, oracle {len(S)})"
         assert len(gsel) >= min(k_min, nb), f"{where} dir {'vs'[dir_]}: only {len(gsel)} blocks"
 
 

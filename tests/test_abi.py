@@ -41,6 +41,10 @@ def test_params_default_matches_paper():
     p = C.crisp_params_default()
     assert (p.alpha, p.w_sink, p.w_local, p.k_min_blocks, p.softmax_scale) == (1.0, 128, 128, 0, 0.0)
     assert abs(p.tau_proxy - 0.2) < 1e-7 and abs(p.gamma - 0.95) < 1e-7
+    assert (p.route_mode, p.vs_mode) == (C.ROUTE_BY_CSTRUCT, C.VS_FLOOR) and abs(p.tau_jsd - 0.1) < 1e-7
+    assert ctypes.sizeof(C.CrispParams) == 40
+    f = C.flexprefill_params()
+    assert (f.route_mode, f.vs_mode) == (C.ROUTE_BY_JSD, C.VS_GAMMA)
 
 
 def test_capacity_and_workspace_sizes():
@@ -70,7 +74,8 @@ def _estimate(sh, p, q=P_ALIGNED, k=P_ALIGNED, ws=P_ALIGNED, ws_bytes=1 << 40):
 
 @pytest.mark.parametrize("field,value", [("alpha", -0.1), ("alpha", math.nan), ("gamma", 0.0), ("gamma", 1.01),
                                          ("w_sink", -1), ("w_local", -3), ("k_min_blocks", -2),
-                                         ("softmax_scale", -1.0), ("tau_proxy", math.inf)])
+                                         ("softmax_scale", -1.0), ("tau_proxy", math.inf), ("route_mode", 2),
+                                         ("route_mode", -1), ("vs_mode", 2), ("tau_jsd", math.nan)])
 def test_bad_params_rejected(field, value):
     sh = C.CrispShape(2, 1, 4096, 128, 128)
     p = C.crisp_params_default()
@@ -101,6 +106,19 @@ def test_null_misaligned_and_small_buffers_rejected():
     assert st == C.CRISP_EINVAL
     st = C.lib.crisp_dense_attn(ctypes.byref(sh), 0.0, P_ALIGNED, P_ALIGNED, P_ALIGNED, P_MISALIGNED, None)
     assert st == C.CRISP_EINVAL
+
+
+def test_jsd_entry_validates_before_launch():
+    sh = C.CrispShape(2, 1, 4096, 128, 128)
+    p = C.crisp_params_default()
+    call = lambda q=P_ALIGNED, pv=P_ALIGNED, out=P_ALIGNED, ws=P_ALIGNED, n=1 << 40: C.lib.crisp_jsd(
+        ctypes.byref(sh), ctypes.byref(p), q, P_ALIGNED, pv, out, ws, n, None)
+    assert call(q=None) == C.CRISP_EINVAL and "q is null" in C.lib.crisp_last_error().decode()
+    assert call(pv=ctypes.c_void_p(0x100001)) == C.CRISP_EINVAL
+    assert call(out=None) == C.CRISP_EINVAL and "jsd" in C.lib.crisp_last_error().decode()
+    assert call(n=16) == C.CRISP_EINVAL and "too small" in C.lib.crisp_last_error().decode()
+    empty = C.CrispShape(0, 1, 4096, 128, 128)
+    assert C.lib.crisp_jsd(ctypes.byref(empty), ctypes.byref(p), None, None, None, None, None, 0, None) == C.CRISP_OK
 
 
 def test_prefill_lists_all_or_none():

@@ -38,7 +38,9 @@ def _rand(h, n, d=128, seed=0, scale=1.0):
 
 def _oracle_params(p, block):
     return O.Params(alpha=p.alpha, tau_proxy=p.tau_proxy, gamma=p.gamma, w_sink=p.w_sink, w_local=p.w_local,
-                    k_min_blocks=p.k_min_blocks, softmax_scale=p.softmax_scale)
+                    k_min_blocks=p.k_min_blocks, softmax_scale=p.softmax_scale,
+                    route_mode="jsd" if p.route_mode == 1 else "cstruct",
+                    vs_mode="gamma" if p.vs_mode == 1 else "floor", tau_jsd=p.tau_jsd)
 
 
 # ------------------------------------------------------------------ attention kernel
@@ -147,19 +149,22 @@ def test_attention_custom_scale_and_empty_rows():
 
 # ------------------------------------------------------------------ estimate / route / select
 
-def _run_stages(C, q, k, v, params, block):
+def _run_stages(C, q, k, v, params, block, want_jsd=False):
     cs, pv, ps = C.crisp_estimate(q, k, params, block)
-    route, rp, ci, dm = C.crisp_route_select(q, k, cs, pv, ps, params, block)
+    jsd = C.crisp_jsd(q, k, pv, params, block) if (params.route_mode == 1 or want_jsd) else None
+    score = jsd if params.route_mode == 1 else cs
+    route, rp, ci, dm = C.crisp_route_select(q, k, score, pv, ps, params, block)
     torch.cuda.synchronize()
-    return (cs.cpu().numpy(), pv.cpu().numpy(), ps.cpu().numpy(), route.cpu().numpy(), rp.cpu().numpy(),
-            ci.cpu().numpy(), dm.cpu().numpy())
+    out = (cs.cpu().numpy(), pv.cpu().numpy(), ps.cpu().numpy(), route.cpu().numpy(), rp.cpu().numpy(),
+           ci.cpu().numpy(), dm.cpu().numpy())
+    return out + ((jsd.cpu().numpy(),) if want_jsd else ())
 
 
 def _check_layer(C, cfg, params, heads=None, qbs_per_head=None, attn=True, where=""):
     """Runs estimate + route/select (+ prefill) for the layer on the GPU and checks the given heads."""
     block = cfg.block
     q, k, v, specs = make_layer(cfg, device=DEV)
-    cs, pv, ps, route, rp, ci, dm = _run_stages(C, q, k, v, params, block)
+    cs, pv, ps, route, rp, ci, dm, jsd = _run_stages(C, q, k, v, params, block, want_jsd=True)
     nb = O.n_blocks(cfg.seq_len, block)
     op = _oracle_params(params, block)
     k_min = op.k_min(block)
@@ -176,10 +181,23 @@ def _check_layer(C, cfg, params, heads=None, qbs_per_head=None, attn=True, where
         w = f"{where} h{h} ({specs[h].kind})"
         res = O.crisp_head(Q[i], Kg[h // G], None, block, op, attend=False)
         PR.compare_scores(cs[h], pv[h], ps[h], res, where=w)
-        assert route[h] == res.route, f"{w}: route gpu {route[h]} oracle {res.route} (C_struct {res.c_struct:.5f})"
+        d_or = O.jsd_score(Q[i], Kg[h // G], res.p_v, block, op.scale(128))
+        assert abs(float(jsd[h]) - d_or) <= PR.JSD_ABS, f"{w}: D_JS gpu {float(jsd[h]):.6f} oracle {d_or:.6f}"
+        if op.route_mode == "jsd" and abs(d_or - op.tau_jsd) <= PR.JSD_BAND:
+            continue  # E5: the route itself may flip; the rest follows the GPU's route
+        assert route[h] == res.route, (f"{w}: route gpu {route[h]} oracle {res.route} "
+                                       f"(C_struct {res.c_struct:.5f}, D_JS {d_or:.5f})")
         gsets = PR.csr_to_sets(rp, ci, h, nb)
         PR.check_structure(gsets, nb, where=w)
-        if res.route == O.ROUTE_VS:
+        if res.route == O.ROUTE_VS and op.vs_mode == "gamma":
+            PR.compare_vs_gamma(dm[h], res, op.gamma, k_min, where=w)
+            for dir_, p_gpu in enumerate((pv[h], ps[h])):  # the selection itself, on the GPU's own scores
+                want = O.vs_select_gamma(p_gpu, op.gamma, k_min)
+                assert np.nonzero(dm[h, dir_])[0].tolist() == want, f"{w} dir {dir_}: gamma selection on gpu p"
+            S_v = np.nonzero(dm[h, 0])[0].tolist()
+            S_s = np.nonzero(dm[h, 1])[0].tolist()
+            assert gsets == O.vs_block_sets(S_v, S_s, nb), f"{w}: CSR differs from the expansion of its own masks"
+        elif res.route == O.ROUTE_VS:
             PR.compare_vs(dm[h], res, op.alpha, k_min, where=w)
             S_v = np.nonzero(dm[h, 0])[0].tolist()
             S_s = np.nonzero(dm[h, 1])[0].tolist()
@@ -239,6 +257,65 @@ def test_stress_config4(alpha, block):
     cfg = stress_config(alpha, block)
     qsel = lambda h, nb: sorted({0, nb // 2, nb - 1})
     _check_layer(C, cfg, C.make_params(alpha=alpha), heads=[0, 1, 2, 5, 13], qbs_per_head=qsel, where=cfg.name)
+
+
+# ------------------------------------------------------------------ FlexPrefill comparator (App. A)
+
+def test_flexprefill_config0_full_path():
+    C = _crisp()
+    _say("FlexPrefill mode, config 0 full path")
+    route = _check_layer(C, CONFIGS[0], C.flexprefill_params(), where="fp c0")
+    assert route.tolist() == [0, 1]
+
+
+@pytest.mark.parametrize("n,block,hq,hkv,gamma", [(1000, 128, 2, 1, 0.95), (777, 64, 4, 2, 0.9),
+                                                  (4096, 64, 4, 1, 0.95), (3000, 128, 4, 2, 1.0)])
+def test_flexprefill_ragged_and_gamma(n, block, hq, hkv, gamma):
+    C = _crisp()
+    _say(f"FlexPrefill mode n={n} B={block} hq={hq} hkv={hkv} gamma={gamma}")
+    cfg = custom_config(n, hq, hkv, block=block, config_id=150 + n % 89)
+    _check_layer(C, cfg, C.flexprefill_params(gamma=gamma), where=f"fp n{n}")
+
+
+def test_flexprefill_config1_sampled():
+    C = _crisp()
+    _say("FlexPrefill mode, config 1 (32k), 8 heads, sampled query blocks")
+    heads = [0, 1, 3, 8, 11, 17, 21, 31]
+    qsel = lambda h, nb: sorted({0, 1, nb // 2, nb - 1})
+    _check_layer(C, CONFIGS[1], C.flexprefill_params(), heads=heads, qbs_per_head=qsel, where="fp c1")
+
+
+@pytest.mark.parametrize("route_mode,vs_mode,tau_jsd", [(0, 1, 0.1), (1, 0, 0.1), (1, 1, 0.0), (1, 1, 2.0)])
+def test_comparator_mixes_and_forced_routes(route_mode, vs_mode, tau_jsd):
+    """The two ablation mixes (C_struct + gamma, JSD + sink-aware floor) and forced JSD routes."""
+    C = _crisp()
+    _say(f"comparator mix route_mode={route_mode} vs_mode={vs_mode} tau_jsd={tau_jsd}")
+    cfg = custom_config(6000, 4, 2, block=128, config_id=161)
+    params = C.make_params(route_mode=route_mode, vs_mode=vs_mode, tau_jsd=tau_jsd, k_min_blocks=2)
+    route = _check_layer(C, cfg, params, where=f"mix{route_mode}{vs_mode}")
+    if route_mode == 1 and tau_jsd == 0.0:
+        assert (route == 0).all()
+    if route_mode == 1 and tau_jsd == 2.0:
+        assert (route == 1).all()
+
+
+def test_flexprefill_prefill_matches_stagewise():
+    """crisp_prefill_attn in the comparator mode (pattern search inside, pooled K reused) gives the
+    lists and output of the stage-by-stage calls."""
+    C = _crisp()
+    _say("FlexPrefill prefill lists == stages")
+    cfg = custom_config(5000, 4, 1, block=128, config_id=141)
+    q, k, v, _ = make_layer(cfg, device=DEV)
+    params = C.flexprefill_params()
+    _, _, _, route, rp, ci, _ = _run_stages(C, q, k, v, params, 128)
+    o1, r2, rp2, ci2 = C.crisp_prefill_attn(q, k, v, params, 128, return_lists=True)
+    o2 = C.crisp_sparse_attn(q, k, v, torch.from_numpy(rp).to(DEV), torch.from_numpy(ci).to(DEV), 128)
+    torch.cuda.synchronize()
+    assert np.array_equal(r2.cpu().numpy(), route) and np.array_equal(rp2.cpu().numpy(), rp)
+    nb = O.n_blocks(cfg.seq_len, 128)
+    for h in range(4):
+        assert PR.csr_to_sets(rp2.cpu().numpy(), ci2.cpu().numpy(), h, nb) == PR.csr_to_sets(rp, ci, h, nb)
+    assert torch.equal(o1, o2)
 
 
 def test_prefill_lists_match_stagewise():
