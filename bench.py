@@ -2,7 +2,9 @@
 
 One step = one full CRISP pass over one attention layer (estimate, route and
 select, block-sparse attention) on seeded synthetic bf16 inputs already resident
-in HBM.  The headline workload is the Llama-3-8B GQA layer at 128k tokens
+in HBM.  The FlexPrefill comparator of App. A (JSD pattern search, gamma VS
+selection) and the two ablation mixes run on the same kernels and layers and
+are reported under "comparators".  The headline workload is the Llama-3-8B GQA layer at 128k tokens
 (32 query heads, 8 KV heads, d = 128, B = 128); the 512k Qwen2-7B-like layer is
 reported alongside.  The dense causal baseline is the same attention kernel with
 every causal block listed.
@@ -36,6 +38,8 @@ def parse():
     ap.add_argument("--skip-512k", action="store_true")
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--steps-512k", type=int, default=2)
+    ap.add_argument("--skip-comparators", action="store_true",
+                    help="skip the FlexPrefill comparator and ablation timings (App. A)")
     ap.add_argument("--config", type=int, default=2, help="headline config id (2 = 128k Llama GQA layer)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy, the reference for rocprofv3 byte counters")
@@ -139,6 +143,48 @@ def layer_measure(cfg, steps, warmup, label):
     res["_attn_flop"] = attn_flop
     res["_tensors"] = (q, k, v, specs, route_c, rp.cpu(), ci.cpu(), pairs_per_head)
     return res
+
+
+def comparator_measure(cfg, res, steps, warmup, label, mixes=True):
+    """The FlexPrefill comparator of App. A on the same kernels (JSD pattern search and gamma
+    VS selection), and the two ablation mixes, timed end to end like CRISP on the same layer."""
+    import torch
+    from paper_2609_01925_amd import crisp as C
+
+    q, k, v = res["_tensors"][:3]
+    block = cfg.block
+    route_cs = res["_tensors"][4]
+    nb = C.n_blocks(cfg.seq_len, block)
+    dense_pairs = cfg.n_q_heads * nb * (nb + 1) / 2
+    sh = C.shape_of(q, k, block)
+    ws = C.workspace(sh, q.device, prefill=True)
+    o = torch.empty_like(q)
+    modes = [("flexprefill", C.flexprefill_params(alpha=cfg.alpha))]
+    if mixes:
+        modes += [("cstruct_route_gamma_vs", C.make_params(alpha=cfg.alpha, vs_mode=C.VS_GAMMA)),
+                  ("jsd_route_floor_vs", C.make_params(alpha=cfg.alpha, route_mode=C.ROUTE_BY_JSD))]
+    out = {}
+    for name, params in modes:
+        _, route, rp, _ = C.crisp_prefill_attn(q, k, v, params, block, return_lists=True)
+        torch.cuda.synchronize()
+        pairs = float(rp[:, nb].double().sum())
+        t = time_events(lambda: C.crisp_prefill_attn(q, k, v, params, block, ws=ws, out=o), steps, warmup)
+        rc = route.cpu()
+        n_vs = int((rc == 0).sum())
+        rec = {"ms_per_layer": t["median"], "speedup_vs_dense": res["dense_ms_per_layer"] / t["median"],
+               "crisp_speedup_vs_this": t["median"] / res["ms_per_layer"],
+               "routes": {"vs": n_vs, "pe": cfg.n_q_heads - n_vs}, "executed_pairs": pairs,
+               "density": pairs / dense_pairs,
+               "route_agreement_with_cstruct": float((rc == route_cs).double().mean())}
+        if params.route_mode == C.ROUTE_BY_JSD:
+            cs, pv, ps = C.crisp_estimate(q, k, params, block)
+            wsj = C.workspace(sh, q.device)
+            rec["pattern_search_ms"] = time_events(lambda: C.crisp_jsd(q, k, pv, params, block, ws=wsj),
+                                                   steps, warmup)["median"]
+        out[name] = rec
+        log(f"{label}: {name} {t['median']:.3f} ms/layer, density {rec['density']:.3f}, "
+            f"routes VS {n_vs}, agreement {rec['route_agreement_with_cstruct']:.2f}")
+    return out
 
 
 def cpu_baseline(cfg, res, budget_s=25.0):
@@ -313,6 +359,8 @@ def main():
     if args.copy_calibration:
         copy_calibration()
     res = layer_measure(cfg, args.steps, args.warmup, "headline")
+    if not args.skip_comparators:
+        res["comparators"] = comparator_measure(cfg, res, args.steps, args.warmup, "headline")
     attn_src = src_hash(os.path.join(ROOT, "paper_2609_01925_amd", "csrc", "attn.hip"))
     achieved = res["_attn_flop"] / (res["_attn_launch_ms"] * 1e-3) / 1e12
     roofline = {
@@ -326,6 +374,8 @@ def main():
     if not args.skip_512k and args.config != 3:
         try:
             r3 = layer_measure(CONFIGS[3], args.steps_512k, 1, "512k")
+            if not args.skip_comparators:
+                r3["comparators"] = comparator_measure(CONFIGS[3], r3, args.steps_512k, 1, "512k", mixes=False)
             extra = {k_: v_ for k_, v_ in r3.items() if not k_.startswith("_")}
             del r3
             torch.cuda.empty_cache()
