@@ -44,6 +44,7 @@ class Params:
     route_mode: str = "cstruct"    # "cstruct" (Alg. 2) or "jsd" (App. A, pattern search)
     vs_mode: str = "floor"         # "floor" (Alg. 3) or "gamma" (App. A, VS index selection)
     tau_jsd: float = 0.1           # JSD threshold; the paper gives none (reading R26)
+    floor_mode: str = "mean"       # "mean" (Sec. 4.3) or "median" (App. H variant)
 
     def scale(self, d: int) -> float:
         return self.softmax_scale if self.softmax_scale > 0 else 1.0 / math.sqrt(d)
@@ -132,18 +133,27 @@ def vs_scores(ahat: np.ndarray, n: int, block: int):
     return a_v, a_s, p_v, p_s
 
 
-def vs_floor(p: np.ndarray, alpha: float):
+def vs_floor(p: np.ndarray, alpha: float, floor: str = "mean"):
     """r_d = max(1 - p_d[0] - p_d[N_b-1], 0), mu_d = r_d / (N_b - 2), threshold alpha * mu_d
     (Alg. 3; noise-floor equation, Sec. 4.3).  Evaluated in float32 as
-    ((1 - p[0]) - p[N_b-1]), then / (N_b - 2), then * alpha.  Needs N_b > 2."""
+    ((1 - p[0]) - p[N_b-1]), then / (N_b - 2), then * alpha.  Needs N_b > 2.
+
+    floor="median" is App. H's robust variant: mu_d is the median of the N_b - 2
+    non-anchor block scores p_d[1 .. N_b-2] (reading R29: for an even count the
+    mean of the two middle values, in float32)."""
     nb = len(p)
     p32 = np.asarray(p, dtype=np.float32)
     r = np.maximum((np.float32(1.0) - p32[0]) - p32[nb - 1], np.float32(0.0))
-    mu = r / np.float32(nb - 2)
+    if floor == "median":
+        mid = np.sort(p32[1:nb - 1])
+        m = len(mid)
+        mu = mid[m // 2] if m % 2 else (mid[m // 2 - 1] + mid[m // 2]) * np.float32(0.5)
+    else:
+        mu = r / np.float32(nb - 2)
     return r, mu, np.float32(alpha) * mu
 
 
-def vs_select(p: np.ndarray, alpha: float, k_min: int) -> List[int]:
+def vs_select(p: np.ndarray, alpha: float, k_min: int, floor: str = "mean") -> List[int]:
     """S_d = top-k_d(p_d) with k_d = clip(|{J : p_d[J] > alpha mu_d}|, k_min, N_b) (Alg. 3).
 
     Readings: the floor test is strict (>); k_min is in blocks; top-k orders
@@ -155,7 +165,7 @@ def vs_select(p: np.ndarray, alpha: float, k_min: int) -> List[int]:
     if nb <= 2:
         return []
     p32 = np.asarray(p, dtype=np.float32)
-    _, _, thr = vs_floor(p, alpha)
+    _, _, thr = vs_floor(p, alpha, floor)
     c = int(np.count_nonzero(p32 > thr))
     kd = min(max(c, k_min), nb)
     order = sorted(range(nb), key=lambda J: (-float(p32[J]), J))
@@ -387,8 +397,8 @@ def crisp_head(q: np.ndarray, k: np.ndarray, v: Optional[np.ndarray], block: int
             res.S_v = vs_select_gamma(p_v, params.gamma, km)
             res.S_s = vs_select_gamma(p_s, params.gamma, km)
         else:
-            res.S_v = vs_select(p_v, params.alpha, km)
-            res.S_s = vs_select(p_s, params.alpha, km)
+            res.S_v = vs_select(p_v, params.alpha, km, params.floor_mode)
+            res.S_s = vs_select(p_s, params.alpha, km, params.floor_mode)
         res.sets = vs_block_sets(res.S_v, res.S_s, nb)
     else:
         At = pe_scores(q, k, block, s)

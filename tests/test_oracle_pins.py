@@ -18,6 +18,7 @@ Stage -> pins:
   JSD pattern search (App. A)     P10 closed forms and scipy for D_JS, closed-form pooled estimate
                                   (flat and sink heads), routes by visible-key counting
   gamma VS selection (App. A)     P10 explicit cases, brute-force minimal subsets, mass-cliff count
+  median noise floor (App. H)     P11 odd/even closed forms, clumpy-noise case, brute-force median
 """
 import math
 
@@ -578,3 +579,51 @@ def test_p10_gamma_pulls_in_the_noise_floor_does_not():
     need = math.ceil((float(np.float32(0.95)) - csum_signal) / noise - 1e-9)
     assert len(S) == 3 + need and set(signal) <= set(S)
     assert O.vs_select(p, 1.0, 1) == sorted(signal)
+
+
+# ---------------------------------------------------------------- P11 (median noise floor, App. H)
+
+def test_p11_median_floor_closed_forms():
+    """The median of the N_b - 2 non-anchor scores (odd and even counts), and App. H's
+    clumpy-noise case: one dominant non-anchor block lifts the mean above a genuine
+    weaker block, which the median floor keeps."""
+    p = np.array([0.3, 0.05, 0.2, 0.01, 0.02, 0.03, 0.39], dtype=np.float32)   # middle: 5 values
+    _, mu, thr = O.vs_floor(p, 1.0, "median")
+    assert mu == np.float32(0.03) and thr == np.float32(0.03)
+    q = np.array([0.3, 0.05, 0.2, 0.01, 0.02, 0.42], dtype=np.float32)         # middle: 4 values
+    _, mu, _ = O.vs_floor(q, 2.0, "median")
+    assert mu == (np.float32(0.02) + np.float32(0.05)) * np.float32(0.5)
+    nb = 40
+    clump = np.full(nb, 0.004, dtype=np.float64)
+    clump[0], clump[nb - 1] = 0.2, 0.1
+    clump[10] = 0.45                      # dominant non-anchor block
+    clump[20] = 0.015                     # weaker genuine signal, below the mean of the residual
+    clump[1:nb - 1][clump[1:nb - 1] == 0.004] = (1 - 0.2 - 0.1 - 0.45 - 0.015) / (nb - 4)
+    p32 = clump.astype(np.float32)
+    mean_sel = O.vs_select(p32, 1.0, 1, "mean")
+    med_sel = O.vs_select(p32, 1.0, 1, "median")
+    _, mu_mean, _ = O.vs_floor(p32, 1.0, "mean")
+    _, mu_med, _ = O.vs_floor(p32, 1.0, "median")
+    assert abs(float(mu_mean) - 0.7 / 38) < 1e-7 and mu_med == p32[1]   # the noise level
+    assert mean_sel == [0, 10, nb - 1]
+    assert med_sel == [0, 10, 20, nb - 1]
+
+
+def test_p11_median_floor_brute_force():
+    """Median by brute force (the value with as many scores above as below) on random vectors."""
+    rng = np.random.default_rng(34)
+    for _ in range(40):
+        nb = int(rng.integers(3, 30))
+        p = rng.dirichlet(np.full(nb, rng.uniform(0.2, 3))).astype(np.float32)
+        mid = [float(x) for x in p[1:nb - 1]]
+        m = len(mid)
+        cands = [x for x in mid if sum(y < x for y in mid) <= (m - 1) // 2 and sum(y > x for y in mid) <= m // 2]
+        _, mu, _ = O.vs_floor(p, 1.0, "median")
+        if m % 2:
+            assert float(mu) in cands
+        else:
+            lo = sorted(mid)[m // 2 - 1]
+            hi = sorted(mid)[m // 2]
+            assert float(mu) == float((np.float32(lo) + np.float32(hi)) * np.float32(0.5))
+        S = O.vs_select(p, 1.0, 0, "median")
+        assert S == sorted(J for J in range(nb) if p[J] > mu) or len(S) == 0 and not (p > mu).any()
