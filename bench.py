@@ -39,7 +39,7 @@ def parse():
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--steps-512k", type=int, default=2)
     ap.add_argument("--skip-comparators", action="store_true",
-                    help="skip the FlexPrefill comparator and ablation timings (App. A)")
+                    help="skip the FlexPrefill comparator, ablation and noise-floor variant timings")
     ap.add_argument("--config", type=int, default=2, help="headline config id (2 = 128k Llama GQA layer)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy, the reference for rocprofv3 byte counters")
@@ -184,6 +184,32 @@ def comparator_measure(cfg, res, steps, warmup, label, mixes=True):
         out[name] = rec
         log(f"{label}: {name} {t['median']:.3f} ms/layer, density {rec['density']:.3f}, "
             f"routes VS {n_vs}, agreement {rec['route_agreement_with_cstruct']:.2f}")
+    return out
+
+
+def floor_variants_measure(cfg, res, steps, warmup, label):
+    """The noise-floor variants (App. H and the alpha sweep): the median floor and alpha in
+    {0.75, 1.25, 1.5}, each timed end to end on the same layer with its executed density."""
+    import torch
+    from paper_2609_01925_amd import crisp as C
+
+    q, k, v = res["_tensors"][:3]
+    block = cfg.block
+    nb = C.n_blocks(cfg.seq_len, block)
+    dense_pairs = cfg.n_q_heads * nb * (nb + 1) / 2
+    ws = C.workspace(C.shape_of(q, k, block), q.device, prefill=True)
+    o = torch.empty_like(q)
+    out = {}
+    for name, params in (("median_alpha1.0", C.make_params(floor_mode=C.FLOOR_MEDIAN)),
+                         ("mean_alpha0.75", C.make_params(alpha=0.75)),
+                         ("mean_alpha1.25", C.make_params(alpha=1.25)),
+                         ("mean_alpha1.5", C.make_params(alpha=1.5))):
+        _, _, rp, _ = C.crisp_prefill_attn(q, k, v, params, block, return_lists=True)
+        torch.cuda.synchronize()
+        pairs = float(rp[:, nb].double().sum())
+        t = time_events(lambda: C.crisp_prefill_attn(q, k, v, params, block, ws=ws, out=o), steps, warmup)
+        out[name] = {"ms_per_layer": t["median"], "density": pairs / dense_pairs, "executed_pairs": pairs}
+        log(f"{label}: floor {name} {t['median']:.3f} ms/layer, density {pairs / dense_pairs:.4f}")
     return out
 
 
@@ -361,6 +387,7 @@ def main():
     res = layer_measure(cfg, args.steps, args.warmup, "headline")
     if not args.skip_comparators:
         res["comparators"] = comparator_measure(cfg, res, args.steps, args.warmup, "headline")
+        res["floor_variants"] = floor_variants_measure(cfg, res, args.steps, args.warmup, "headline")
     attn_src = src_hash(os.path.join(ROOT, "paper_2609_01925_amd", "csrc", "attn.hip"))
     achieved = res["_attn_flop"] / (res["_attn_launch_ms"] * 1e-3) / 1e12
     roofline = {

@@ -73,6 +73,12 @@ enum { CRISP_ROUTE_VS = 0, CRISP_ROUTE_PE = 1 };
 enum { CRISP_ROUTE_BY_CSTRUCT = 0, CRISP_ROUTE_BY_JSD = 1 };
 enum { CRISP_VS_FLOOR = 0, CRISP_VS_GAMMA = 1 };
 
+/* crisp_params.floor_mode: the noise level mu of the floor (vs_mode CRISP_VS_FLOOR).
+ *   CRISP_FLOOR_MEAN        r / (N_b - 2), the mean non-anchor mass (Sec. 4.3)
+ *   CRISP_FLOOR_MEDIAN      the median of p_d[1 .. N_b-2] (App. H; for an even count
+ *                           the mean of the two middle values, float32)          */
+enum { CRISP_FLOOR_MEAN = 0, CRISP_FLOOR_MEDIAN = 1 };
+
 /* Layer shape.  H_q % H_kv == 0, H_kv >= 1, n >= 0, head_dim == 128,
  * block in {64, 128}.  n == 0 or H_q == 0 is a valid empty layer: calls return
  * CRISP_OK and launch nothing. */
@@ -95,7 +101,8 @@ typedef struct {
  * The FlexPrefill comparator of App. A on the same kernels (defaults: the paper's method):
  *   route_mode     CRISP_ROUTE_BY_CSTRUCT (default) or CRISP_ROUTE_BY_JSD
  *   vs_mode        CRISP_VS_FLOOR (default) or CRISP_VS_GAMMA (uses gamma)
- *   tau_jsd        D_JS route threshold, finite; default 0.1 (the paper gives none) */
+ *   tau_jsd        D_JS route threshold, finite; default 0.1 (the paper gives none)
+ *   floor_mode     CRISP_FLOOR_MEAN (default) or CRISP_FLOOR_MEDIAN (App. H)        */
 typedef struct {
   float alpha;
   float tau_proxy;
@@ -107,6 +114,7 @@ typedef struct {
   int32_t route_mode;
   int32_t vs_mode;
   float tau_jsd;
+  int32_t floor_mode;
 } crisp_params;
 
 /* Fills *p with the paper's defaults listed above. */

@@ -30,7 +30,7 @@ class CrispParams(ctypes.Structure):
     _fields_ = [("alpha", ctypes.c_float), ("tau_proxy", ctypes.c_float), ("gamma", ctypes.c_float),
                 ("w_sink", ctypes.c_int32), ("w_local", ctypes.c_int32), ("k_min_blocks", ctypes.c_int32),
                 ("softmax_scale", ctypes.c_float), ("route_mode", ctypes.c_int32), ("vs_mode", ctypes.c_int32),
-                ("tau_jsd", ctypes.c_float)]
+                ("tau_jsd", ctypes.c_float), ("floor_mode", ctypes.c_int32)]
 
 
 class CrispError(RuntimeError):
@@ -75,6 +75,7 @@ EXPORTED = ("crisp_params_default", "crisp_col_capacity", "crisp_workspace_size"
 # route_mode / vs_mode values (include/crisp.h)
 ROUTE_BY_CSTRUCT, ROUTE_BY_JSD = 0, 1
 VS_FLOOR, VS_GAMMA = 0, 1
+FLOOR_MEAN, FLOOR_MEDIAN = 0, 1
 
 
 def _check(status: int, what: str):
@@ -84,9 +85,10 @@ def _check(status: int, what: str):
 
 
 def make_params(alpha=1.0, tau_proxy=0.2, gamma=0.95, w_sink=128, w_local=128, k_min_blocks=0,
-                softmax_scale=0.0, route_mode=ROUTE_BY_CSTRUCT, vs_mode=VS_FLOOR, tau_jsd=0.1) -> CrispParams:
+                softmax_scale=0.0, route_mode=ROUTE_BY_CSTRUCT, vs_mode=VS_FLOOR, tau_jsd=0.1,
+                floor_mode=FLOOR_MEAN) -> CrispParams:
     return CrispParams(alpha, tau_proxy, gamma, w_sink, w_local, k_min_blocks, softmax_scale, route_mode, vs_mode,
-                       tau_jsd)
+                       tau_jsd, floor_mode)
 
 
 def flexprefill_params(gamma=0.95, tau_jsd=0.1, **kw) -> CrispParams:

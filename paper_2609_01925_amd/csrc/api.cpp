@@ -66,6 +66,8 @@ crisp_status check_params(const crisp_params* p, const Dims& d) {
   if (p->vs_mode != CRISP_VS_FLOOR && p->vs_mode != CRISP_VS_GAMMA)
     return fail(CRISP_EINVAL, "vs_mode %d unknown", p->vs_mode);
   if (!isfinite(p->tau_jsd)) return fail(CRISP_EINVAL, "tau_jsd must be finite");
+  if (p->floor_mode != CRISP_FLOOR_MEAN && p->floor_mode != CRISP_FLOOR_MEDIAN)
+    return fail(CRISP_EINVAL, "floor_mode %d unknown", p->floor_mode);
   (void)d;
   return CRISP_OK;
 }
@@ -173,6 +175,7 @@ void crisp_params_default(crisp_params* p) {
   p->route_mode = CRISP_ROUTE_BY_CSTRUCT;
   p->vs_mode = CRISP_VS_FLOOR;
   p->tau_jsd = 0.1f;
+  p->floor_mode = CRISP_FLOOR_MEAN;
 }
 
 int64_t crisp_col_capacity(const crisp_shape* shape) {
@@ -260,7 +263,8 @@ crisp_status crisp_route_select(const crisp_shape* shape, const crisp_params* pa
   if (workspace_bytes < ws_layout(d).total)
     return fail(CRISP_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, ws_layout(d).total);
   return hip_status(launch_select(d, scale_of(params->softmax_scale), params->alpha, route_tau(params),
-                                  params->gamma, kmin_of(params, d.B), params->vs_mode, false, q, k, c_struct, p_v,
+                                  params->gamma, kmin_of(params, d.B), params->vs_mode, params->floor_mode, false, q, k,
+                                  c_struct, p_v,
                                   p_s, route, row_ptr, col_idx, col_cap_per_head, dir_mask_or_null,
                                   (char*)workspace, (hipStream_t)stream),
                     "crisp_route_select launch");
@@ -355,7 +359,8 @@ crisp_status crisp_prefill_attn(const crisp_shape* shape, const crisp_params* pa
   if (by_jsd)  // the route score slot then holds D_JS instead of C_struct
     CHECK(hip_status(launch_jsd(d, scale, q, k, pv, cs, ws, st), "crisp_prefill_attn pattern search launch"));
   CHECK(hip_status(launch_select(d, scale, params->alpha, route_tau(params), params->gamma, kmin_of(params, d.B),
-                                 params->vs_mode, by_jsd, q, k, cs, pv, ps, route, rp, ci, d.cap, nullptr, ws, st),
+                                 params->vs_mode, params->floor_mode, by_jsd, q, k, cs, pv, ps, route, rp, ci,
+                                 d.cap, nullptr, ws, st),
                    "crisp_prefill_attn select launch"));
   return hip_status(launch_attn(d, scale, q, k, v, rp, ci, d.cap, false, o, ws + L.sched, st),
                     "crisp_prefill_attn attention launch");

@@ -41,9 +41,10 @@ hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, 
                            hipStream_t stream);
 
 // route_score is C_struct (tau = tau_proxy) or D_JS (tau = tau_jsd); vs_mode 0 is the
-// noise floor, 1 gamma coverage; kbar_all: K_bar of every KV group is already in ws.
+// noise floor (floor_mode 0: mean, 1: median), 1 gamma coverage; kbar_all: K_bar of
+// every KV group is already in ws.
 hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, float gamma, int k_min, int vs_mode,
-                         bool kbar_all, const uint16_t* q, const uint16_t* k, const float* route_score,
+                         int floor_mode, bool kbar_all, const uint16_t* q, const uint16_t* k, const float* route_score,
                          const float* p_v, const float* p_s, int8_t* route, int32_t* row_ptr, int32_t* col_idx,
                          int64_t col_cap, uint8_t* dir_mask, char* ws, hipStream_t stream);
 

@@ -7,6 +7,7 @@
 //
 // VS, per (head, direction), one workgroup:
 //   floor  r = max((1 - p[0]) - p[N_b-1], 0), mu = r / (N_b - 2), thr = alpha * mu
+//          (App. H variant: mu = median of p[1 .. N_b-2], by radix select)
 //   count  c = #{p > thr};  k = min(max(c, k_min), N_b)
 //   if k > c: radix-select the k-th largest value t on the float bit pattern
 //   (p >= 0, so bit order is value order) and keep ties at t in block order.
@@ -53,6 +54,7 @@ struct SelArgs {
   float alpha, tau, gamma;
   int k_min;
   int vs_mode;   // 0: noise floor (Alg. 3), 1: gamma coverage per direction (App. A)
+  int floor_mode;  // 0: mean of the non-anchor mass (Sec. 4.3), 1: their median (App. H)
   int kbar_all;  // 1: K_bar of every KV group is already in kbar (the JSD pattern search pooled it)
   int64_t cap;  // nb * (nb + 1) / 2
   uint8_t* masks;
@@ -273,8 +275,21 @@ __global__ __launch_bounds__(1024) void sel_route_vs(SelArgs a) {
     select_top_k(p, nb, kd, m, dm, hist, sh, wtot);
     return;
   }
-  const float r = fmaxf((1.0f - p[0]) - p[nb - 1], 0.0f);
-  const float mu = r / (float)(nb - 2);
+  float mu;
+  if (a.floor_mode == 1) {
+    // median of p[1 .. nb-2] (for an even count, the mean of the two middle values)
+    const int m = nb - 2;
+    const float hi = __uint_as_float(kth_largest(p + 1, m, m / 2 + (m & 1), hist, sh));
+    if (m & 1) {
+      mu = hi;
+    } else {
+      const float lo = __uint_as_float(kth_largest(p + 1, m, m / 2 + 1, hist, sh));
+      mu = (lo + hi) * 0.5f;
+    }
+  } else {
+    const float r = fmaxf((1.0f - p[0]) - p[nb - 1], 0.0f);
+    mu = r / (float)(nb - 2);
+  }
   const float thr = a.alpha * mu;
   int c = 0;
   for (int J = tid; J < nb; J += 1024) c += p[J] > thr;
@@ -757,7 +772,7 @@ hipError_t launch_jsd(const Dims& d, float scale, const uint16_t* q, const uint1
 }
 
 hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, float gamma, int k_min, int vs_mode,
-                         bool kbar_all, const uint16_t* q, const uint16_t* k, const float* route_score,
+                         int floor_mode, bool kbar_all, const uint16_t* q, const uint16_t* k, const float* route_score,
                          const float* p_v, const float* p_s, int8_t* route, int32_t* row_ptr, int32_t* col_idx,
                          int64_t col_cap, uint8_t* dir_mask, char* ws, hipStream_t stream) {
   if (d.n == 0 || d.hq == 0) return hipSuccess;
@@ -768,7 +783,7 @@ hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, flo
   a.n = d.n; a.nb = d.nb; a.B = d.B; a.hq = d.hq; a.hkv = d.hkv; a.G = d.G;
   a.c2 = scale * kLog2e;
   a.alpha = alpha; a.tau = tau; a.gamma = gamma; a.k_min = k_min;
-  a.vs_mode = vs_mode; a.kbar_all = kbar_all ? 1 : 0;
+  a.vs_mode = vs_mode; a.floor_mode = floor_mode; a.kbar_all = kbar_all ? 1 : 0;
   a.cap = d.cap;
   a.masks = reinterpret_cast<uint8_t*>(ws + L.masks);
   a.qbar = reinterpret_cast<float*>(ws + L.qbar);

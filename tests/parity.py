@@ -48,13 +48,13 @@ def check_structure(sets, nb, where=""):
         assert s and s[0] == 0 and s[-1] == qb, f"{where} row {qb} misses forced blocks: {s[:10]}..{s[-3:]}"
 
 
-def vs_direction_exempt(p: np.ndarray, alpha: float, k_min: int):
+def vs_direction_exempt(p: np.ndarray, alpha: float, k_min: int, floor: str = "mean"):
     """Returns (degenerate, exempt block set) for one VS direction, from oracle values."""
     nb = len(p)
     r64 = max(1.0 - p[0] - p[nb - 1], 0.0)
     if r64 < 2.0 ** -20:
         return True, set(range(nb))
-    _, _, thr = O.vs_floor(p, alpha)
+    _, _, thr = O.vs_floor(p, alpha, floor)
     thr = float(thr)
     ex = {J for J in range(nb) if abs(p[J] - thr) <= BAND * thr}
     c = int(np.count_nonzero(np.asarray(p, np.float32) > np.float32(thr)))
@@ -64,7 +64,7 @@ def vs_direction_exempt(p: np.ndarray, alpha: float, k_min: int):
     return False, ex
 
 
-def compare_vs(gpu_mask: np.ndarray, ores: O.HeadResult, alpha: float, k_min: int, where=""):
+def compare_vs(gpu_mask: np.ndarray, ores: O.HeadResult, alpha: float, k_min: int, where="", floor: str = "mean"):
     """gpu_mask: uint8 [2, N_b] (S_v, S_s membership)."""
     nb = gpu_mask.shape[1]
     for dir_, (p, S) in enumerate(((ores.p_v, ores.S_v), (ores.p_s, ores.S_s))):
@@ -72,7 +72,7 @@ def compare_vs(gpu_mask: np.ndarray, ores: O.HeadResult, alpha: float, k_min: in
         if nb <= 2:
             assert not gsel, where
             continue
-        degenerate, ex = vs_direction_exempt(p, alpha, k_min)
+        degenerate, ex = vs_direction_exempt(p, alpha, k_min, floor)
         if degenerate:
             continue
         diff = gsel ^ set(S)

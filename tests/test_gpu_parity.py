@@ -40,7 +40,8 @@ def _oracle_params(p, block):
     return O.Params(alpha=p.alpha, tau_proxy=p.tau_proxy, gamma=p.gamma, w_sink=p.w_sink, w_local=p.w_local,
                     k_min_blocks=p.k_min_blocks, softmax_scale=p.softmax_scale,
                     route_mode="jsd" if p.route_mode == 1 else "cstruct",
-                    vs_mode="gamma" if p.vs_mode == 1 else "floor", tau_jsd=p.tau_jsd)
+                    vs_mode="gamma" if p.vs_mode == 1 else "floor", tau_jsd=p.tau_jsd,
+                    floor_mode="median" if p.floor_mode == 1 else "mean")
 
 
 # ------------------------------------------------------------------ attention kernel
@@ -198,7 +199,7 @@ def _check_layer(C, cfg, params, heads=None, qbs_per_head=None, attn=True, where
             S_s = np.nonzero(dm[h, 1])[0].tolist()
             assert gsets == O.vs_block_sets(S_v, S_s, nb), f"{w}: CSR differs from the expansion of its own masks"
         elif res.route == O.ROUTE_VS:
-            PR.compare_vs(dm[h], res, op.alpha, k_min, where=w)
+            PR.compare_vs(dm[h], res, op.alpha, k_min, where=w, floor=op.floor_mode)
             S_v = np.nonzero(dm[h, 0])[0].tolist()
             S_s = np.nonzero(dm[h, 1])[0].tolist()
             assert gsets == O.vs_block_sets(S_v, S_s, nb), f"{w}: CSR differs from the expansion of its own masks"
@@ -297,6 +298,24 @@ def test_comparator_mixes_and_forced_routes(route_mode, vs_mode, tau_jsd):
         assert (route == 0).all()
     if route_mode == 1 and tau_jsd == 2.0:
         assert (route == 1).all()
+
+
+@pytest.mark.parametrize("alpha,block,n", [(1.0, 128, 6000), (0.75, 64, 3001), (1.5, 128, 300)])
+def test_median_floor(alpha, block, n):
+    """App. H's median noise floor against the oracle (odd and even non-anchor counts)."""
+    C = _crisp()
+    _say(f"median floor alpha={alpha} B={block} n={n}")
+    cfg = custom_config(n, 4, 2, block=block, config_id=170 + n % 53)
+    _check_layer(C, cfg, C.make_params(alpha=alpha, floor_mode=C.FLOOR_MEDIAN, k_min_blocks=1), where=f"med{n}")
+
+
+def test_median_floor_stress_config4():
+    C = _crisp()
+    _say("median floor on the config 4 stress layer")
+    cfg = stress_config(1.0, 128)
+    qsel = lambda h, nb: sorted({0, nb // 2, nb - 1})
+    _check_layer(C, cfg, C.make_params(floor_mode=C.FLOOR_MEDIAN), heads=[0, 1, 2, 5, 13], qbs_per_head=qsel,
+                 where="med stress")
 
 
 def test_flexprefill_prefill_matches_stagewise():
