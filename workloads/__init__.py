@@ -16,4 +16,6 @@ from .synth import (  # noqa: F401
     custom_config,
     STRESS_ALPHAS,
     STRESS_BLOCKS,
+    PE_SWEEP_LENGTHS,
+    structured_pe_config,
 )

@@ -27,6 +27,13 @@ Key layout per KV group (d = 128):
                  k_{i-o}'s code attends to the diagonal at offset o
   dim  112       sink tag: TAG on keys 0..3, else 0
   dims 113..127  vertical tags: TAG on one planted column each (15 per group)
+Configs with `structured_pe` (the paper-like PE workload) give dims 96..111 to a
+smooth position code instead (the slash code keeps dims 48..95, rows still of
+norm 8): SMOOTH_SCALE * (cos, sin)(2 pi m j / n) for m = 1..8.  Their PE heads
+("structured") carry a few of these frequencies, so every query prefers keys by
+a gently varying log-weight sum_m A_m cos(2 pi m j / n - phi_m) of 1.5-5 nats:
+block masses that decay smoothly with no floor to cut, whose top-50 blocks hold
+a fraction of the mass rather than almost all of it (App. B's diffuse heads).
 """
 from __future__ import annotations
 
@@ -49,6 +56,8 @@ SINK_DIM = 112
 VERT_DIM0 = 113
 LOCAL_WINDOW = 128         # box filter width of the local code
 BG_SIGMA = 0.5             # std of the per-query background direction (concentrated heads)
+SMOOTH_DIMS = (96, 112)    # smooth position code of structured-PE configs (8 frequencies x cos, sin)
+SMOOTH_SCALE = 4.0
 LOCAL_PEAK = 2.5           # local-window logit boost at |i - j| = 0, in nats (not length-scaled:
                            # neighbouring queries share the local code, so its cross-talk on far
                            # keys does not average out over the proxy rows and must stay small)
@@ -72,6 +81,7 @@ class LayerConfig:
     tiny: bool = False             # head 0 concentrated, head 1 diffuse with i.i.d. K
     adversarial: bool = False      # heads 0..2 replaced by the three stress heads
     variant: int = 0
+    structured_pe: bool = False    # PE heads carry a smooth key preference (see module notes)
 
     @property
     def group(self) -> int:
@@ -88,6 +98,7 @@ class HeadSpec:
     slash_offsets: Tuple[int, ...] = ()
     s_slash: Tuple[float, ...] = ()
     s_loc: float = 0.0
+    smooth: Tuple[Tuple[int, float, float], ...] = ()   # structured PE: (cycles m, amplitude A, phase phi)
 
 
 CONFIGS = {
@@ -99,6 +110,16 @@ CONFIGS = {
 
 STRESS_ALPHAS = (0.5, 1.0, 2.0)
 STRESS_BLOCKS = (64, 128)
+
+
+PE_SWEEP_LENGTHS = (8192, 65536, 131072, 262144, 524288)
+
+
+def structured_pe_config(seq_len: int = 131072) -> LayerConfig:
+    """The paper-like PE workload: the Llama-3-8B GQA mix (60% concentrated heads) whose other
+    heads are structured PE heads instead of i.i.d. noise; one config per length of the sweep."""
+    return LayerConfig(f"llama3-8b-pe-{seq_len // 1024}k", 5, seq_len, 32, 8, structured_pe=True,
+                       variant=PE_SWEEP_LENGTHS.index(seq_len) if seq_len in PE_SWEEP_LENGTHS else 99)
 
 
 def stress_config(alpha: float, block: int) -> LayerConfig:
@@ -158,6 +179,15 @@ def head_specs(cfg: LayerConfig) -> List[HeadSpec]:
     diffuse = set(int(h) for h in perm[:n_diffuse])
     specs = []
     for h in range(H):
+        if h in diffuse and cfg.structured_pe:
+            n_f = int(rng.integers(1, 4))
+            ms = rng.choice(np.arange(1, 9), size=n_f, replace=False)
+            total = float(rng.uniform(1.5, 5.0))
+            w = rng.dirichlet(np.ones(n_f))
+            ph = rng.uniform(0.0, 2 * math.pi, size=n_f)
+            specs.append(HeadSpec("structured", smooth=tuple((int(m), float(total * wi), float(p))
+                                                             for m, wi, p in zip(ms, w, ph))))
+            continue
         if h in diffuse:
             specs.append(HeadSpec("diffuse"))
             continue
@@ -193,7 +223,18 @@ def _key_parts(cfg: LayerConfig, g: int, device) -> Tuple[torch.Tensor, torch.Te
     loc = (c[LOCAL_WINDOW:] - c[:n]).float()           # sum of LOCAL_WINDOW consecutive white rows
     loc = loc * (math.sqrt(nl) / loc.norm(dim=1, keepdim=True).clamp_min(1e-20))
     sl = torch.randn(n, ns, generator=gen, device=device, dtype=torch.float32)
-    sl = sl * (8.0 / sl.norm(dim=1, keepdim=True).clamp_min(1e-20))
+    if cfg.structured_pe:
+        nsm = SMOOTH_DIMS[1] - SMOOTH_DIMS[0]
+        sl = sl[:, : ns - nsm]
+        sl = sl * (8.0 / sl.norm(dim=1, keepdim=True).clamp_min(1e-20))
+        j = torch.arange(n, device=device, dtype=torch.float64)
+        cols = []
+        for m in range(1, nsm // 2 + 1):
+            ang = (2 * math.pi * m / n) * j
+            cols += [torch.cos(ang), torch.sin(ang)]
+        sl = torch.cat([sl, (SMOOTH_SCALE * torch.stack(cols, dim=1)).float()], dim=1)
+    else:
+        sl = sl * (8.0 / sl.norm(dim=1, keepdim=True).clamp_min(1e-20))
     tags = torch.zeros(n, HEAD_DIM - SINK_DIM, device=device, dtype=torch.float32)
     tags[: min(N_SINKS, n), 0] = TAG
     for c_i, col in enumerate(kv_group_columns(cfg, g)):
@@ -207,6 +248,13 @@ def _query_head(cfg: LayerConfig, h: int, spec: HeadSpec, parts, device) -> torc
     rt = math.sqrt(d)
     if spec.kind == "diffuse":
         return torch.randn(n, d, generator=gen, device=device, dtype=torch.float32) / rt
+    if spec.kind == "structured":
+        q = torch.randn(n, d, generator=gen, device=device, dtype=torch.float32) / rt
+        for m, amp, ph in spec.smooth:   # s * q . k = amp * cos(2 pi m j / n - ph) on the smooth code
+            c = SMOOTH_DIMS[0] + 2 * (m - 1)
+            q[:, c] += amp * rt / SMOOTH_SCALE * math.cos(ph)
+            q[:, c + 1] += amp * rt / SMOOTH_SCALE * math.sin(ph)
+        return q
     q = torch.zeros(n, d, device=device, dtype=torch.float32)
     if spec.kind == "flat":
         return q
@@ -219,11 +267,13 @@ def _query_head(cfg: LayerConfig, h: int, spec: HeadSpec, parts, device) -> torc
     nl = LOCAL_DIMS[1] - LOCAL_DIMS[0]
     a_loc = (LOCAL_PEAK + spec.s_loc) * rt / nl
     q[:, LOCAL_DIMS[0]:LOCAL_DIMS[1]] += a_loc * loc
+    # slash code width (structured-PE configs keep the smooth code out of the slash boost)
+    ns = SLASH_DIMS[1] - SLASH_DIMS[0] - ((SMOOTH_DIMS[1] - SMOOTH_DIMS[0]) if cfg.structured_pe else 0)
     for o, s in zip(spec.slash_offsets, spec.s_slash):
         if o >= n:
             continue
         b = (math.log(n / 64.0) + s) * rt / 64.0
-        q[o:, SLASH_DIMS[0]:SLASH_DIMS[1]] += b * sl[: n - o]
+        q[o:, SLASH_DIMS[0]:SLASH_DIMS[0] + ns] += b * sl[: n - o, :ns]
     q[:, SINK_DIM] += (math.log(n / N_SINKS) + spec.s_sink) * rt / TAG
     for v, s in zip(spec.verticals, spec.s_vert):
         q[:, VERT_DIM0 + v] += (math.log(n) + s) * rt / TAG
