@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--skip-512k", action="store_true")
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--steps-512k", type=int, default=2)
+    ap.add_argument("--sweep", action="store_true",
+                    help="also run the length sweep 8k..512k on the paper-like structured-PE workload "
+                         "(CRISP, dense and FlexPrefill) and report the crossover with dense")
     ap.add_argument("--skip-comparators", action="store_true",
                     help="skip the FlexPrefill comparator, ablation and noise-floor variant timings")
     ap.add_argument("--config", type=int, default=2, help="headline config id (2 = 128k Llama GQA layer)")
@@ -211,6 +214,31 @@ def floor_variants_measure(cfg, res, steps, warmup, label):
         out[name] = {"ms_per_layer": t["median"], "density": pairs / dense_pairs, "executed_pairs": pairs}
         log(f"{label}: floor {name} {t['median']:.3f} ms/layer, density {pairs / dense_pairs:.4f}")
     return out
+
+
+def pe_sweep_measure():
+    """Length sweep on the structured-PE workload (the regime of the paper's latency table):
+    CRISP, the dense baseline and the FlexPrefill comparator at each length, and the shortest
+    length at which CRISP beats dense (the context-length gate's threshold)."""
+    import torch
+    from workloads import PE_SWEEP_LENGTHS, structured_pe_config
+
+    rows = []
+    for n in sorted(PE_SWEEP_LENGTHS):
+        cfg = structured_pe_config(n)
+        steps = 5 if n <= 131072 else 2
+        res = layer_measure(cfg, steps, 1, f"sweep {n // 1024}k")
+        fp = comparator_measure(cfg, res, steps, 1, f"sweep {n // 1024}k", mixes=False)["flexprefill"]
+        rows.append({"seq_len": n, "workload": cfg.name, "crisp_ms": res["ms_per_layer"],
+                     "dense_ms": res["dense_ms_per_layer"], "speedup_vs_dense": res["speedup_vs_dense"],
+                     "density": res["density"], "routes": res["routes"], "stage_ms": res["stage_ms"],
+                     "flexprefill_ms": fp["ms_per_layer"], "flexprefill_density": fp["density"],
+                     "crisp_speedup_vs_flexprefill": fp["crisp_speedup_vs_this"],
+                     "sparse_attn_mfma_frac": res["sparse_attn_mfma_frac"]})
+        del res
+        torch.cuda.empty_cache()
+    faster = [r["seq_len"] for r in rows if r["crisp_ms"] < r["dense_ms"]]
+    return {"rows": rows, "crisp_beats_dense_from": min(faster) if faster else None}
 
 
 def cpu_baseline(cfg, res, budget_s=25.0):
@@ -408,6 +436,7 @@ def main():
             torch.cuda.empty_cache()
         except Exception as e:  # noqa: BLE001 -- the headline line must still be printed
             extra = {"error": repr(e)}
+    sweep = pe_sweep_measure() if args.sweep else None
     cpu = None
     if not args.skip_cpu:
         cpu = cpu_baseline(cfg, res)
@@ -436,6 +465,8 @@ def main():
         "at_512k": extra,
         "attn_src_sha": attn_src,
     }
+    if sweep is not None:
+        record["pe_sweep"] = sweep
     print(json.dumps(record))
 
 

@@ -61,7 +61,7 @@ typedef enum {
   CRISP_EHIP = 3          /* a HIP launch failed; see crisp_last_error() */
 } crisp_status;
 
-enum { CRISP_ROUTE_VS = 0, CRISP_ROUTE_PE = 1 };
+enum { CRISP_ROUTE_VS = 0, CRISP_ROUTE_PE = 1, CRISP_ROUTE_DENSE = 2 /* context-length gate */ };
 
 /* crisp_params.route_mode: what decides a head's route.
  *   CRISP_ROUTE_BY_CSTRUCT  C_struct >= tau_proxy (Alg. 2, the paper's method)
@@ -102,7 +102,9 @@ typedef struct {
  *   route_mode     CRISP_ROUTE_BY_CSTRUCT (default) or CRISP_ROUTE_BY_JSD
  *   vs_mode        CRISP_VS_FLOOR (default) or CRISP_VS_GAMMA (uses gamma)
  *   tau_jsd        D_JS route threshold, finite; default 0.1 (the paper gives none)
- *   floor_mode     CRISP_FLOOR_MEAN (default) or CRISP_FLOOR_MEDIAN (App. H)        */
+ *   floor_mode     CRISP_FLOOR_MEAN (default) or CRISP_FLOOR_MEDIAN (App. H)
+ *   dense_below_len  context-length gate (Sec. 5, short contexts): crisp_prefill_attn
+ *                  runs dense causal attention when seq_len < this; 0 (default) never */
 typedef struct {
   float alpha;
   float tau_proxy;
@@ -115,6 +117,7 @@ typedef struct {
   int32_t vs_mode;
   float tau_jsd;
   int32_t floor_mode;
+  int32_t dense_below_len;
 } crisp_params;
 
 /* Fills *p with the paper's defaults listed above. */
@@ -204,7 +207,9 @@ crisp_status crisp_sparse_attn(const crisp_shape* shape, float softmax_scale,
  * receive the route and block lists (col_idx capacity crisp_col_capacity per
  * head); if they are all null the library keeps them in the workspace (then
  * `workspace_bytes` must be crisp_prefill_workspace_size).  Mixed null/non-null
- * is CRISP_EINVAL. */
+ * is CRISP_EINVAL.  Below the context-length gate (seq_len < dense_below_len) the layer
+ * is dense causal attention: route[h] = CRISP_ROUTE_DENSE and every row lists all its
+ * causal blocks. */
 crisp_status crisp_prefill_attn(const crisp_shape* shape, const crisp_params* params,
                                 const crisp_bf16* q, const crisp_bf16* k, const crisp_bf16* v,
                                 crisp_bf16* o, int8_t* route_or_null, int32_t* row_ptr_or_null,

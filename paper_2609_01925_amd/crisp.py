@@ -30,7 +30,7 @@ class CrispParams(ctypes.Structure):
     _fields_ = [("alpha", ctypes.c_float), ("tau_proxy", ctypes.c_float), ("gamma", ctypes.c_float),
                 ("w_sink", ctypes.c_int32), ("w_local", ctypes.c_int32), ("k_min_blocks", ctypes.c_int32),
                 ("softmax_scale", ctypes.c_float), ("route_mode", ctypes.c_int32), ("vs_mode", ctypes.c_int32),
-                ("tau_jsd", ctypes.c_float), ("floor_mode", ctypes.c_int32)]
+                ("tau_jsd", ctypes.c_float), ("floor_mode", ctypes.c_int32), ("dense_below_len", ctypes.c_int32)]
 
 
 class CrispError(RuntimeError):
@@ -86,9 +86,9 @@ def _check(status: int, what: str):
 
 def make_params(alpha=1.0, tau_proxy=0.2, gamma=0.95, w_sink=128, w_local=128, k_min_blocks=0,
                 softmax_scale=0.0, route_mode=ROUTE_BY_CSTRUCT, vs_mode=VS_FLOOR, tau_jsd=0.1,
-                floor_mode=FLOOR_MEAN) -> CrispParams:
+                floor_mode=FLOOR_MEAN, dense_below_len=0) -> CrispParams:
     return CrispParams(alpha, tau_proxy, gamma, w_sink, w_local, k_min_blocks, softmax_scale, route_mode, vs_mode,
-                       tau_jsd, floor_mode)
+                       tau_jsd, floor_mode, dense_below_len)
 
 
 def flexprefill_params(gamma=0.95, tau_jsd=0.1, **kw) -> CrispParams:

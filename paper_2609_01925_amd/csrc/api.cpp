@@ -68,6 +68,7 @@ crisp_status check_params(const crisp_params* p, const Dims& d) {
   if (!isfinite(p->tau_jsd)) return fail(CRISP_EINVAL, "tau_jsd must be finite");
   if (p->floor_mode != CRISP_FLOOR_MEAN && p->floor_mode != CRISP_FLOOR_MEDIAN)
     return fail(CRISP_EINVAL, "floor_mode %d unknown", p->floor_mode);
+  if (p->dense_below_len < 0) return fail(CRISP_EINVAL, "dense_below_len must be >= 0");
   (void)d;
   return CRISP_OK;
 }
@@ -176,6 +177,7 @@ void crisp_params_default(crisp_params* p) {
   p->vs_mode = CRISP_VS_FLOOR;
   p->tau_jsd = 0.1f;
   p->floor_mode = CRISP_FLOOR_MEAN;
+  p->dense_below_len = 0;
 }
 
 int64_t crisp_col_capacity(const crisp_shape* shape) {
@@ -345,6 +347,15 @@ crisp_status crisp_prefill_attn(const crisp_shape* shape, const crisp_params* pa
   const size_t need = given ? e.route : e.total;
   if (workspace_bytes < need) return fail(CRISP_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, need);
   char* ws = (char*)workspace;
+  if (d.n < params->dense_below_len) {  // context-length gate: the layer is dense attention
+    if (given)
+      CHECK(hip_status(launch_dense_lists(d, route_or_null, row_ptr_or_null, col_idx_or_null, d.cap,
+                                          (hipStream_t)stream),
+                       "crisp_prefill_attn dense lists launch"));
+    return hip_status(launch_attn(d, scale_of(params->softmax_scale), q, k, v, nullptr, nullptr, 0, true, o, nullptr,
+                                  (hipStream_t)stream),
+                      "crisp_prefill_attn dense attention launch");
+  }
   float* cs = (float*)(ws + e.cs);
   float* pv = (float*)(ws + e.pv);
   float* ps = (float*)(ws + e.ps);

@@ -48,6 +48,10 @@ hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, flo
                          const float* p_v, const float* p_s, int8_t* route, int32_t* row_ptr, int32_t* col_idx,
                          int64_t col_cap, uint8_t* dir_mask, char* ws, hipStream_t stream);
 
+// route = dense and full causal CSR lists (col_cap >= nb (nb + 1) / 2).
+hipError_t launch_dense_lists(const Dims& d, int8_t* route, int32_t* row_ptr, int32_t* col_idx, int64_t col_cap,
+                              hipStream_t stream);
+
 // D_JS per query head into jsd[hq]; leaves K_bar of every KV group in ws.
 hipError_t launch_jsd(const Dims& d, float scale, const uint16_t* q, const uint16_t* k, const float* p_v,
                       float* jsd, char* ws, hipStream_t stream);

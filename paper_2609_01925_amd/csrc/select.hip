@@ -756,6 +756,28 @@ __global__ __launch_bounds__(256) void sel_csr_fill(SelArgs a) {
 
 }  // namespace
 
+// Full causal lists (the context-length gate): route = dense, row qb = 0..qb.
+// grid (nb, hq), 256 threads.
+__global__ __launch_bounds__(256) void sel_dense_lists(int8_t* route, int32_t* row_ptr, int32_t* col_idx, int nb,
+                                                       int64_t col_cap) {
+  const int qb = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+  const int base = (int)((int64_t)qb * (qb + 1) / 2);
+  if (tid == 0) {
+    row_ptr[(size_t)h * (nb + 1) + qb] = base;
+    if (qb == nb - 1) row_ptr[(size_t)h * (nb + 1) + nb] = base + qb + 1;
+    if (qb == 0) route[h] = 2;
+  }
+  int32_t* out = col_idx + (size_t)h * col_cap + base;
+  for (int i = tid; i <= qb; i += 256) out[i] = i;
+}
+
+hipError_t launch_dense_lists(const Dims& d, int8_t* route, int32_t* row_ptr, int32_t* col_idx, int64_t col_cap,
+                              hipStream_t stream) {
+  if (d.n == 0 || d.hq == 0) return hipSuccess;
+  hipLaunchKernelGGL(sel_dense_lists, dim3(d.nb, d.hq), dim3(256), 0, stream, route, row_ptr, col_idx, d.nb, col_cap);
+  return hipGetLastError();
+}
+
 hipError_t launch_jsd(const Dims& d, float scale, const uint16_t* q, const uint16_t* k, const float* p_v,
                       float* jsd, char* ws, hipStream_t stream) {
   if (d.n == 0 || d.hq == 0) return hipSuccess;

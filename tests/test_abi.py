@@ -42,7 +42,7 @@ def test_params_default_matches_paper():
     assert (p.alpha, p.w_sink, p.w_local, p.k_min_blocks, p.softmax_scale) == (1.0, 128, 128, 0, 0.0)
     assert abs(p.tau_proxy - 0.2) < 1e-7 and abs(p.gamma - 0.95) < 1e-7
     assert (p.route_mode, p.vs_mode) == (C.ROUTE_BY_CSTRUCT, C.VS_FLOOR) and abs(p.tau_jsd - 0.1) < 1e-7
-    assert ctypes.sizeof(C.CrispParams) == 44 and p.floor_mode == C.FLOOR_MEAN
+    assert ctypes.sizeof(C.CrispParams) == 48 and p.floor_mode == C.FLOOR_MEAN and p.dense_below_len == 0
     f = C.flexprefill_params()
     assert (f.route_mode, f.vs_mode) == (C.ROUTE_BY_JSD, C.VS_GAMMA)
 
@@ -76,7 +76,7 @@ def _estimate(sh, p, q=P_ALIGNED, k=P_ALIGNED, ws=P_ALIGNED, ws_bytes=1 << 40):
                                          ("w_sink", -1), ("w_local", -3), ("k_min_blocks", -2),
                                          ("softmax_scale", -1.0), ("tau_proxy", math.inf), ("route_mode", 2),
                                          ("route_mode", -1), ("vs_mode", 2), ("tau_jsd", math.nan),
-                                         ("floor_mode", 2)])
+                                         ("floor_mode", 2), ("dense_below_len", -1)])
 def test_bad_params_rejected(field, value):
     sh = C.CrispShape(2, 1, 4096, 128, 128)
     p = C.crisp_params_default()

@@ -318,6 +318,27 @@ def test_median_floor_stress_config4():
                  where="med stress")
 
 
+@pytest.mark.parametrize("n,block", [(4000, 128), (777, 64)])
+def test_context_length_gate_is_dense(n, block):
+    """Below the gate, prefill equals the dense kernel bit for bit and reports dense routes and
+    full causal lists; at the gate length it runs the sparse path again."""
+    C = _crisp()
+    _say(f"context-length gate n={n} B={block}")
+    cfg = custom_config(n, 4, 2, block=block, config_id=180 + n % 31)
+    q, k, v, _ = make_layer(cfg, device=DEV)
+    gated = C.make_params(dense_below_len=n + 1)
+    o1, route, rp, ci = C.crisp_prefill_attn(q, k, v, gated, block, return_lists=True)
+    o2 = C.crisp_dense_attn(q, k, v, block)
+    o3 = C.crisp_prefill_attn(q, k, v, gated, block)
+    o4, route4, _, _ = C.crisp_prefill_attn(q, k, v, C.make_params(dense_below_len=n), block, return_lists=True)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(o3, o2)
+    assert (route.cpu() == 2).all() and (route4.cpu() != 2).all()
+    nb = O.n_blocks(n, block)
+    for h in range(4):
+        assert PR.csr_to_sets(rp.cpu().numpy(), ci.cpu().numpy(), h, nb) == O.dense_causal_sets(nb)
+
+
 def test_flexprefill_prefill_matches_stagewise():
     """crisp_prefill_attn in the comparator mode (pattern search inside, pooled K reused) gives the
     lists and output of the stage-by-stage calls."""
