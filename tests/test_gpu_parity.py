@@ -251,6 +251,57 @@ def test_config1_sampled():
     _check_layer(C, cfg, C.make_params(), heads=heads, qbs_per_head=qsel, where="c1")
 
 
+@pytest.mark.parametrize("cid", [2, 3])
+def test_full_size_layer_in_bench_launch(cid):
+    """The headline layers at full size (128k Llama, 512k Qwen-like), run as bench.py runs them
+    (crisp_prefill_attn over the whole layer with the prefill workspace), checked on one VS
+    and one PE head against the oracle: scores, route, block lists, and attention rows of
+    sampled query blocks."""
+    C = _crisp()
+    cfg = CONFIGS[cid]
+    block, G = cfg.block, cfg.group
+    nb = O.n_blocks(cfg.seq_len, block)
+    _say(f"full size {cfg.name}: generate and run the layer")
+    q, k, v, specs = make_layer(cfg, device=DEV)
+    params = C.make_params(alpha=cfg.alpha)
+    ws = C.workspace(C.shape_of(q, k, block), DEV, prefill=True)
+    o = torch.empty_like(q)
+    C.crisp_prefill_attn(q, k, v, params, block, ws=ws, out=o)
+    o2, route, rp, ci = C.crisp_prefill_attn(q, k, v, params, block, return_lists=True)
+    cs, pv, ps = C.crisp_estimate(q, k, params, block)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o2)
+    route, rp, ci = route.cpu().numpy(), rp.cpu().numpy(), ci.cpu().numpy()
+    cs, pv, ps = cs.cpu().numpy(), pv.cpu().numpy(), ps.cpu().numpy()
+    op = _oracle_params(params, block)
+    hv = next(h for h in range(cfg.n_q_heads) if specs[h].kind == "concentrated")
+    hp = next(h for h in range(cfg.n_q_heads) if specs[h].kind == "diffuse")
+    for h, qbs in ((hv, [0, nb // 2, nb - 1]), (hp, [1, nb // 8])):
+        w = f"{cfg.name} h{h} ({specs[h].kind})"
+        _say(f"  oracle for {w}")
+        Qh, Kh, Vh = to_f64(q[h]), to_f64(k[h // G]), to_f64(v[h // G])
+        res = O.crisp_head(Qh, Kh, None, block, op, attend=False)
+        PR.compare_scores(cs[h], pv[h], ps[h], res, where=w)
+        assert route[h] == res.route, f"{w}: route gpu {route[h]} oracle {res.route}"
+        gsets = PR.csr_to_sets(rp, ci, h, nb)
+        PR.check_structure(gsets, nb, where=w)
+        _say(f"  selection and attention rows for {w}")
+        if res.route == O.ROUTE_VS:
+            assert gsets == [sorted(set(s_)) for s_ in gsets]
+            diff = [qb for qb in range(nb) if set(gsets[qb]) != set(res.sets[qb])]
+            if diff:   # the direction sets may differ only inside the E1/E2 bands
+                ex_v = PR.vs_direction_exempt(res.p_v, op.alpha, op.k_min(block))[1]
+                ex_s = PR.vs_direction_exempt(res.p_s, op.alpha, op.k_min(block))[1]
+                for qb in diff:
+                    for kb in set(gsets[qb]) ^ set(res.sets[qb]):
+                        assert kb in ex_v or (nb - 1 - (qb - kb)) in ex_s, f"{w}: row {qb} block {kb}"
+        else:
+            PR.compare_pe(gsets, res, op.gamma, where=w)
+        ref = O.sparse_attention(Qh, Kh, Vh, gsets, block, op.scale(128), qbs=qbs)
+        PR.compare_attention(to_f64(o[h]), ref, rows=PR.qb_rows(qbs, block, cfg.seq_len), where=w + " attn")
+        del Qh, Kh, Vh, res, gsets
+
+
 @pytest.mark.parametrize("alpha,block", [(0.5, 64), (1.0, 128), (2.0, 128), (1.0, 64)])
 def test_stress_config4(alpha, block):
     C = _crisp()
