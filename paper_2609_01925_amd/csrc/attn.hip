@@ -25,10 +25,16 @@
 // lane does too at most): until then P may exceed 1 by at most 2^8, which fp32
 // and bf16 hold exactly as well, and the O accumulators are left untouched.
 //
-// Sparse lists are processed by a persistent grid that pulls units from per-XCD
-// longest-first work lists (built by attn_schedule from the list lengths), so
-// long PE rows start first, short VS rows fill the tail, and the K/V tiles of a
-// KV group stay in one XCD's L2.
+// Sparse lists are processed longest first from work lists that attn_schedule
+// builds from the list lengths, so long PE rows start first and short VS rows
+// fill the tail.  Below 512k tokens a persistent grid pulls units from one list
+// per KV group, and the K/V tiles of a group stay in the caches of the XCDs that
+// serve it.  From 512k tokens on, rows are long enough that the workgroups of a
+// persistent grid drift apart along the key axis (the two workgroups sharing a
+// CU do not advance at the same rate, and each keeps its place for the whole
+// layer), so concurrent readers of a K/V tile no longer meet in L2: there the
+// grid has one workgroup per unit, each taking the next unit of a single
+// longest-first list, and units that start together advance together.
 #include <type_traits>
 
 #include "crisp_device.h"
@@ -43,6 +49,7 @@ constexpr int kTileBytes = BK * 256;         // one K or V tile: 64 rows x 128 b
 constexpr int kRingBytes = 2 * kTileBytes;   // one ring (K or V): 2 stages
 constexpr float kSumLimit = 256.0f;          // a lane's tile sum of P above this forces a rescale
 constexpr int kCostBuckets = 8192;
+constexpr int kOneShotMinLen = 1 << 19;  // from this length on, sparse lists run one unit per workgroup
 
 struct AttnArgs {
   const uint16_t* q;
@@ -54,6 +61,7 @@ struct AttnArgs {
   int64_t col_cap;
   const int32_t* order;  // persistent mode: units sorted longest first
   int* counter;          // persistent mode: next position in `order`
+  int one_shot;          // 1: one unit per workgroup, all units in one queue
   int n, nb, hq, hkv, G;
   float c;        // softmax scale * log2(e)
   int map_mode;   // static grid: 0 natural order, 1 H_kv % 8 == 0, 2 8 % H_kv == 0
@@ -89,6 +97,23 @@ __device__ __forceinline__ bool map_unit(const AttnArgs& a, int bid, int& h, int
   if (qb < 0) return false;
   h = g * a.G + (u % a.G);
   return true;
+}
+
+// Persistent grid: queue slot of head h's KV group, and the slot the workgroups
+// on XCD x pop from first (XCDs beyond the groups' share start at an empty slot
+// and go straight to taking work from the others).
+__device__ __forceinline__ int unit_queue(const AttnArgs& a, int h) {
+  if (a.one_shot) return 0;
+  const int g = h / a.G;
+  if (a.hkv >= kNumXcd) return g % kNumXcd;
+  return g * (kNumXcd / a.hkv);
+}
+
+__device__ __forceinline__ int home_queue(const AttnArgs& a, int x) {
+  if (a.one_shot) return 0;
+  if (a.hkv >= kNumXcd) return x;
+  const int r = kNumXcd / a.hkv;  // XCDs per group
+  return x < a.hkv * r ? (x / r) * r : x;
 }
 
 // Workgroup geometry for query blocks of BQ rows: QH halves of 32 queries per
@@ -526,7 +551,7 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
   // take work from the other queues in turn.  Every queue ends, so every
   // workgroup exits once all units are taken.
   int* s_unit = reinterpret_cast<int*>(smem + 2 * kRingBytes);
-  const int x0 = blockIdx.x % kNumXcd;
+  const int x0 = home_queue(a, blockIdx.x % kNumXcd);
   const int* start = a.counter + 8;
   for (;;) {
     __syncthreads();  // the previous unit is done with LDS and the unit slot
@@ -545,15 +570,20 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
     const int unit = *s_unit;
     if (unit < 0) break;
     attn_unit<BQ, DENSE>(a, unit / a.nb, unit % a.nb, lds0, off, fe, tid);
+    if (a.one_shot) break;
   }
 #endif  // __HIP_DEVICE_COMPILE__
 }
 
-// Work lists for the persistent sparse kernel: one queue per XCD.  Unit (h, qb)
-// goes to the queue of the XCD its KV group is bound to (group g -> XCD g when
-// there are >= 8 KV groups; with fewer groups each group spans 8 / H_kv XCDs,
-// split by query-block parity), so that XCD's L2 serves the group's K/V tiles to
-// all of the group's heads.  Within a queue units are ordered longest first (a
+// Work lists for the sparse kernel.  One-unit-per-workgroup mode keeps a single
+// queue (slot 0).  Persistent mode keeps one queue per KV group, in queue
+// slot g % 8 when there are >= 8 groups.  With fewer groups each group owns
+// r = 8 / H_kv XCDs that all pop from one shared queue (slot g * r): they then
+// work on the same query blocks at the same time, so the K/V tiles one XCD
+// brings in from HBM are still in the shared last-level cache when the other
+// XCDs of the group ask for them (separate queues let the XCDs of a group drift
+// apart over a long layer, and each then streams K/V from HBM on its own).
+// Within an XCD the group's heads share its L2.  Units are ordered longest first (a
 // counting sort of list lengths: exact up to 768 blocks, then in steps of 16).
 // One workgroup builds all queues and resets their counters; the order within
 // one length is arbitrary (it only decides which workgroup runs a unit, never a
@@ -561,12 +591,7 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
 // units at int offset 64.
 constexpr int kQueueBuckets = kCostBuckets / kNumXcd;  // 1024 cost buckets per XCD queue
 
-__device__ __forceinline__ int unit_xcd(const AttnArgs& a, int h, int qb) {
-  const int g = h / a.G;
-  if (a.hkv >= kNumXcd) return g % kNumXcd;
-  const int r = kNumXcd / a.hkv;  // XCDs per group
-  return (g * r + qb % r) % kNumXcd;
-}
+
 
 __device__ __forceinline__ int cost_bucket(int64_t c) {
   c = c < 0 ? 0 : c;
@@ -586,7 +611,7 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
     const int h = u / a.nb, qb = u % a.nb;
     const int32_t* rp = a.row_ptr + (size_t)h * (a.nb + 1);
     const int c = cost_bucket((int64_t)rp[qb + 1] - (int64_t)rp[qb]);
-    return unit_xcd(a, h, qb) * kQueueBuckets + (kQueueBuckets - 1 - c);
+    return unit_queue(a, h) * kQueueBuckets + (kQueueBuckets - 1 - c);
   };
   for (int u = tid; u < total; u += 1024) atomicAdd(&hist[key(u)], 1);
   __syncthreads();
@@ -656,7 +681,7 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
   AttnArgs a;
   a.q = q; a.k = k; a.v = v; a.o = o;
   a.row_ptr = row_ptr; a.col_idx = col_idx; a.col_cap = col_cap;
-  a.order = nullptr; a.counter = nullptr;
+  a.order = nullptr; a.counter = nullptr; a.one_shot = 0;
   a.n = d.n; a.nb = d.nb; a.hq = d.hq; a.hkv = d.hkv; a.G = d.G;
   a.c = scale * kLog2e;
   int grid;
@@ -676,8 +701,9 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
     hipLaunchKernelGGL(attn_schedule, dim3(1), dim3(1024), 0, stream, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    a.one_shot = d.n >= kOneShotMinLen ? 1 : 0;
     const int pg = d.B == 128 ? persistent_grid<128>() : persistent_grid<64>();
-    grid = pg < d.hq * d.nb ? pg : d.hq * d.nb;
+    grid = a.one_shot || pg > d.hq * d.nb ? d.hq * d.nb : pg;
   }
   if (d.B == 128) return dense ? launch_t<128, true>(a, grid, stream) : launch_t<128, false>(a, grid, stream);
   return dense ? launch_t<64, true>(a, grid, stream) : launch_t<64, false>(a, grid, stream);

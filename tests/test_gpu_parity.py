@@ -302,6 +302,34 @@ def test_full_size_layer_in_bench_launch(cid):
         del Qh, Kh, Vh, res, gsets
 
 
+@pytest.mark.parametrize("block", [64, 128])
+def test_long_layer_one_unit_per_workgroup(block):
+    """From 512k tokens on the sparse kernel runs one unit per workgroup from a single
+    longest-first list; below that, a persistent grid.  At a ragged length past 512k, with
+    a few heads of one KV group, the result equals the fixed-order launch bit for bit (every
+    unit is computed the same way whichever workgroup takes it), and sampled rows of the
+    longest query blocks match the oracle."""
+    C = _crisp()
+    n = (1 << 19) + 77
+    cfg = custom_config(n, 3, 1, block=block, config_id=180 + block // 64)
+    _say(f"one unit per workgroup: {cfg.name}")
+    q, k, v, _ = make_layer(cfg, device=DEV)
+    o, route, rp, ci = C.crisp_prefill_attn(q, k, v, C.make_params(), block, return_lists=True)
+    fixed = C.crisp_sparse_attn(q, k, v, rp, ci, block, balance=False)
+    torch.cuda.synchronize()
+    assert torch.equal(o, fixed)
+    nb = O.n_blocks(n, block)
+    rpn, cin = rp.cpu().numpy(), ci.cpu().numpy()
+    for h in range(cfg.n_q_heads):
+        gsets = PR.csr_to_sets(rpn, cin, h, nb)
+        PR.check_structure(gsets, nb, where=f"{cfg.name} h{h}")
+        qbs = [nb - 1] if h else [0, nb - 2, nb - 1]
+        Qh, Kh, Vh = to_f64(q[h]), to_f64(k[0]), to_f64(v[0])
+        ref = O.sparse_attention(Qh, Kh, Vh, gsets, block, 1.0 / math.sqrt(128), qbs=qbs)
+        PR.compare_attention(to_f64(o[h]), ref, rows=PR.qb_rows(qbs, block, n), where=f"{cfg.name} h{h}")
+        del Qh, Kh, Vh
+
+
 @pytest.mark.parametrize("alpha,block", [(0.5, 64), (1.0, 128), (2.0, 128), (1.0, 64)])
 def test_stress_config4(alpha, block):
     C = _crisp()
