@@ -44,9 +44,16 @@ namespace crisp {
 
 namespace {
 
-constexpr int BK = 64;                       // keys per tile
-constexpr int kTileBytes = BK * 256;         // one K or V tile: 64 rows x 128 bf16
-constexpr int kRingBytes = 2 * kTileBytes;   // one ring (K or V): 2 stages
+// Key tiles: 64 keys for 128-row query blocks.  64-row blocks have two-wave
+// workgroups, which need four to a CU for two waves per SIMD, so their tiles
+// have 32 keys (32 KB of rings per workgroup instead of 64 KB).
+template <int BQ>
+struct Tile {
+  static constexpr int kBK = BQ == 128 ? 64 : 32;  // keys per tile
+  static constexpr int kNMB = kBK / 32;            // 32-key sub-blocks per tile
+  static constexpr int kBytes = kBK * 256;         // one K or V tile: kBK rows x 128 bf16
+  static constexpr int kRing = 2 * kBytes;         // one ring (K or V): 2 stages
+};
 constexpr float kSumLimit = 256.0f;          // a lane's tile sum of P above this forces a rescale
 constexpr int kCostBuckets = 8192;
 constexpr int kOneShotMinLen = 1 << 19;  // from this length on, sparse lists run one unit per workgroup
@@ -201,14 +208,14 @@ __device__ __forceinline__ void dma16(i32x4 rsrc, int voff, int soff, int lds_ad
   asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rsrc), "s"(so), "{m0}"(m0));
 }
 
-// One tensor's tile into the LDS stage at address stage.
-template <int NW>
+// One tensor's tile of BK keys into the LDS stage at address stage.
+template <int NW, int BK>
 __device__ __forceinline__ void fetch_tile(const Fetch<NW>& f, i32x4 rsrc, int stage, int key0, int w) {
 #pragma unroll
   for (int x = 0; x < Fetch<NW>::kPerWave; ++x) {
     const int wp = w + NW * x;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) dma16(rsrc, f.voff[x], (key0 + 16 * i) * 256, stage + (16 * i + 4 * wp) * 256);
+    for (int i = 0; i < BK / 16; ++i) dma16(rsrc, f.voff[x], (key0 + 16 * i) * 256, stage + (16 * i + 4 * wp) * 256);
   }
 }
 
@@ -227,8 +234,8 @@ __device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt((7 << 4)
 // queries of half h (lane column).  qk_sub computes sub-block MB for every half;
 // rows 32..63 have the same swizzle as rows 0..31, so sub-block 1 is +32 rows,
 // and each K operand read serves every half.
-template <int QH, int MB>
-__device__ __forceinline__ void qk_sub(int kbuf, const bf16x8 (&qf)[QH][8], const Offsets& off, f32x16 (&s)[QH][2]) {
+template <int QH, int NMB, int MB>
+__device__ __forceinline__ void qk_sub(int kbuf, const bf16x8 (&qf)[QH][8], const Offsets& off, f32x16 (&s)[QH][NMB]) {
 #pragma unroll
   for (int h = 0; h < QH; ++h) s[h][MB] = zero16();
 #pragma unroll
@@ -241,9 +248,10 @@ __device__ __forceinline__ void qk_sub(int kbuf, const bf16x8 (&qf)[QH][8], cons
 
 // Sets masked scores to -inf: keys after the lane's query (causal, which also
 // covers keys past n), and every key of an invalid list entry.
-__device__ __forceinline__ void mask_tile(f32x16 (&s)[2], int key0, int qabs, bool valid, int l) {
+template <int NMB>
+__device__ __forceinline__ void mask_tile(f32x16 (&s)[NMB], int key0, int qabs, bool valid, int l) {
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+  for (int mb = 0; mb < NMB; ++mb)
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int key = key0 + 32 * mb + 8 * (i >> 2) + 4 * (l >> 5) + (i & 3);
@@ -274,9 +282,10 @@ __device__ __forceinline__ void exp_sub(const f32x16& s, float c, float mc, bf16
 }
 
 // l + the lane's sum of the tile's (bf16) probabilities.
-__device__ __forceinline__ float sum_tile(const bf16x8 (&pb)[2][2], float l) {
+template <int NMB>
+__device__ __forceinline__ float sum_tile(const bf16x8 (&pb)[NMB][2], float l) {
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+  for (int mb = 0; mb < NMB; ++mb)
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
@@ -291,10 +300,10 @@ __device__ __forceinline__ float sum_tile(const bf16x8 (&pb)[2][2], float l) {
 
 // O^T[h] (128 d x 32 queries) += V^T P^T[h] for one tile; each V^T operand (two
 // transposing reads) serves every half.
-template <int QH>
-__device__ __forceinline__ void pv_tile(int vbuf, const Offsets& off, const bf16x8 (&pb)[QH][2][2], f32x16 (&o)[QH][4]) {
+template <int QH, int NMB>
+__device__ __forceinline__ void pv_tile(int vbuf, const Offsets& off, const bf16x8 (&pb)[QH][NMB][2], f32x16 (&o)[QH][4]) {
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+  for (int mb = 0; mb < NMB; ++mb)
 #pragma unroll
     for (int ss = 0; ss < 2; ++ss) {
       const int vb = vbuf + (32 * mb + 16 * ss) * 256;
@@ -313,6 +322,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
                                           const Fetch<Geo<BQ>::kWaves>& fe, int tid) {
   constexpr int QH = Geo<BQ>::kQH;
   constexpr int NW = Geo<BQ>::kWaves;
+  constexpr int BK = Tile<BQ>::kBK, NMB = Tile<BQ>::kNMB;
   constexpr int TPB = BQ / BK;  // tiles per key block
   const int l = tid & 63, w = tid >> 6;
   const int g = head / a.G;
@@ -371,9 +381,9 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
     bool vv, mm;
     return tile_key0(j, vv, mm);
   };
-  // ring stages by parity: K at lds0 + {0, 16 KB}, V at lds0 + 32 KB + {0, 16 KB}
-  auto kst = [&](int parity) { return lds0 + parity * kTileBytes; };
-  auto vst = [&](int parity) { return lds0 + kRingBytes + parity * kTileBytes; };
+  // ring stages by parity: K at lds0 + {0, 1} tiles, V after the K ring
+  auto kst = [&](int parity) { return lds0 + parity * Tile<BQ>::kBytes; };
+  auto vst = [&](int parity) { return lds0 + Tile<BQ>::kRing + parity * Tile<BQ>::kBytes; };
 
   bf16x8 qf[QH][8];
 #pragma unroll
@@ -397,7 +407,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
     l_run[h] = 0.f;
   }
 
-  f32x16 s[QH][2];
+  f32x16 s[QH][NMB];
   if (T > 0) {
     // Step j (parity P): tile j's scores S(j) are in registers and P(j-1) is
     // formed.  At the top, K(j+1) and V(j-1), issued in step j-1 (or the
@@ -408,13 +418,13 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
     // stays at most 2^8 (so does every one of them); otherwise the (rare) branch
     // raises the running max to the tile's row max, rescales O and l, and forms
     // them again.  Last, the scores of tile j+1 replace S(j).
-    auto step = [&](int j, auto par, auto first, const bf16x8 (&pp)[QH][2][2], bf16x8 (&pn)[QH][2][2]) {
+    auto step = [&](int j, auto par, auto first, const bf16x8 (&pp)[QH][NMB][2], bf16x8 (&pn)[QH][NMB][2]) {
       constexpr int P = decltype(par)::value;
       wait_dma();
       __syncthreads();
 
-      if (j + 2 < T) fetch_tile<NW>(fe, rk, kst(P), key0_of(j + 2), w);
-      fetch_tile<NW>(fe, rv, vst(P), key0_of(j), w);
+      if (j + 2 < T) fetch_tile<NW, BK>(fe, rk, kst(P), key0_of(j + 2), w);
+      fetch_tile<NW, BK>(fe, rv, vst(P), key0_of(j), w);
       {
         bool vj, mj;
         const int kj = tile_key0(j, vj, mj);
@@ -428,21 +438,27 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
 #pragma unroll
       for (int h = 0; h < QH; ++h) {
         const float mc = m_run[h] == -__builtin_inff() ? 0.f : m_run[h] * a.c;
-        exp_sub(s[h][0], a.c, mc, pn[h][0]);
-        exp_sub(s[h][1], a.c, mc, pn[h][1]);
-        ts[h] = sum_tile(pn[h], 0.f);
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) exp_sub(s[h][mb], a.c, mc, pn[h][mb]);
+        ts[h] = sum_tile<NMB>(pn[h], 0.f);
         grow = grow || !(ts[h] <= kSumLimit) || m_run[h] == -__builtin_inff();
       }
-      if (!decltype(first)::value) pv_tile<QH>(vst(1 - P), off, pp, o);
+      if (!decltype(first)::value) pv_tile<QH, NMB>(vst(1 - P), off, pp, o);
       // Keeps the probabilities formed here, beside the PV product, rather than
       // letting the compiler sink them into the no-rescale path.
 #pragma unroll
-      for (int h = 0; h < QH; ++h)
-        asm volatile("" ::"v"(pn[h][0][0]), "v"(pn[h][0][1]), "v"(pn[h][1][0]), "v"(pn[h][1][1]), "v"(ts[h]));
+      for (int h = 0; h < QH; ++h) {
+#pragma unroll
+        for (int mb = 0; mb < NMB; ++mb) asm volatile("" ::"v"(pn[h][mb][0]), "v"(pn[h][mb][1]));
+        asm volatile("" ::"v"(ts[h]));
+      }
       if (__ballot(grow)) {
 #pragma unroll
         for (int h = 0; h < QH; ++h) {
-          const float mx = half_max(vmax(max16(s[h][0]), max16(s[h][1])));
+          float mt = max16(s[h][0]);
+#pragma unroll
+          for (int mb = 1; mb < NMB; ++mb) mt = vmax(mt, max16(s[h][mb]));
+          const float mx = half_max(mt);
           const float m_new = vmax(m_run[h], mx);
           const float alpha = m_run[h] == -__builtin_inff() ? 0.f : fast_exp2((m_run[h] - m_new) * a.c);
           l_run[h] *= alpha;
@@ -452,9 +468,9 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
             for (int i = 0; i < 16; ++i) o[h][db][i] *= alpha;
           m_run[h] = m_new;
           const float mcn = m_new == -__builtin_inff() ? 0.f : m_new * a.c;
-          exp_sub(s[h][0], a.c, mcn, pn[h][0]);
-          exp_sub(s[h][1], a.c, mcn, pn[h][1]);
-          ts[h] = sum_tile(pn[h], 0.f);
+#pragma unroll
+          for (int mb = 0; mb < NMB; ++mb) exp_sub(s[h][mb], a.c, mcn, pn[h][mb]);
+          ts[h] = sum_tile<NMB>(pn[h], 0.f);
         }
       }
 #pragma unroll
@@ -463,8 +479,8 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
       // targets; those scores are never used.  The scheduler interleaves the
       // K operand reads with the MFMAs in its LDS/MFMA pipelining mode.
       __builtin_amdgcn_iglp_opt(0);
-      qk_sub<QH, 0>(kst(1 - P), qf, off, s);
-      qk_sub<QH, 1>(kst(1 - P), qf, off, s);
+      qk_sub<QH, NMB, 0>(kst(1 - P), qf, off, s);
+      if constexpr (NMB > 1) qk_sub<QH, NMB, 1>(kst(1 - P), qf, off, s);
       if (!DENSE && (((j + 1) / TPB) >> 6) != chunk0) {  // tile j+1 starts the next chunk
         ++chunk0;
         if ((chunk0 + 1) & 1)
@@ -477,15 +493,15 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
     using Odd = std::integral_constant<int, 1>;
 
     // prologue: K(0), K(1), then the scores of tile 0
-    fetch_tile<NW>(fe, rk, kst(0), key0_of(0), w);
-    if (T > 1) fetch_tile<NW>(fe, rk, kst(1), key0_of(1), w);
+    fetch_tile<NW, BK>(fe, rk, kst(0), key0_of(0), w);
+    if (T > 1) fetch_tile<NW, BK>(fe, rk, kst(1), key0_of(1), w);
     wait_dma();
     __syncthreads();
-    qk_sub<QH, 0>(kst(0), qf, off, s);
-    qk_sub<QH, 1>(kst(0), qf, off, s);
+    qk_sub<QH, NMB, 0>(kst(0), qf, off, s);
+    if constexpr (NMB > 1) qk_sub<QH, NMB, 1>(kst(0), qf, off, s);
     // two P buffers with fixed registers: steps alternate between them, and the
     // parity of every step is known where it is expanded
-    bf16x8 pa[QH][2][2], pz[QH][2][2];
+    bf16x8 pa[QH][NMB][2], pz[QH][NMB][2];
     step(0, Even{}, std::true_type{}, pz, pa);
     int j = 1;
     for (; j + 1 < T; j += 2) {
@@ -497,11 +513,11 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
       step(j, Odd{}, std::false_type{}, pa, pz);
       wait_dma();
       __syncthreads();
-      pv_tile<QH>(vst(1), off, pz, o);
+      pv_tile<QH, NMB>(vst(1), off, pz, o);
     } else {
       wait_dma();
       __syncthreads();
-      pv_tile<QH>(vst(0), off, pa, o);
+      pv_tile<QH, NMB>(vst(0), off, pa, o);
     }
   }
 
@@ -533,7 +549,7 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
 #if defined(__HIP_DEVICE_COMPILE__)
   // The rings are the kernel's only LDS object, so they start at LDS address 0
   // (LDS-DMA destinations are then 1 KB aligned); the work-queue slot sits after them.
-  __shared__ __attribute__((aligned(1024))) char smem[2 * kRingBytes + 16];
+  __shared__ __attribute__((aligned(1024))) char smem[2 * Tile<BQ>::kRing + 16];
   const int lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);  // LDS address of the rings
   constexpr int NW = Geo<BQ>::kWaves;
   const int tid = threadIdx.x;
@@ -550,7 +566,7 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
   // Pop from this XCD's queue (workgroup i runs on XCD i % 8); when it is empty,
   // take work from the other queues in turn.  Every queue ends, so every
   // workgroup exits once all units are taken.
-  int* s_unit = reinterpret_cast<int*>(smem + 2 * kRingBytes);
+  int* s_unit = reinterpret_cast<int*>(smem + 2 * Tile<BQ>::kRing);
   const int x0 = home_queue(a, blockIdx.x % kNumXcd);
   const int* start = a.counter + 8;
   for (;;) {
@@ -678,6 +694,15 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
                        const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, bool dense,
                        uint16_t* o, void* sched, hipStream_t stream) {
   if (d.n == 0 || d.hq == 0) return hipSuccess;
+  if (dense && d.B == 64) {
+    // Dense causal attention does not depend on the query block size: 128-row
+    // blocks visit the same 64-key tiles in the same order, plus, for the first
+    // half of each block, one fully masked tile that adds exact zeros.
+    Dims d2 = d;
+    d2.B = 128;
+    d2.nb = (d.n + 127) / 128;
+    return launch_attn(d2, scale, q, k, v, row_ptr, col_idx, col_cap, dense, o, sched, stream);
+  }
   AttnArgs a;
   a.q = q; a.k = k; a.v = v; a.o = o;
   a.row_ptr = row_ptr; a.col_idx = col_idx; a.col_cap = col_cap;
@@ -706,7 +731,7 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
     grid = a.one_shot || pg > d.hq * d.nb ? d.hq * d.nb : pg;
   }
   if (d.B == 128) return dense ? launch_t<128, true>(a, grid, stream) : launch_t<128, false>(a, grid, stream);
-  return dense ? launch_t<64, true>(a, grid, stream) : launch_t<64, false>(a, grid, stream);
+  return launch_t<64, false>(a, grid, stream);  // dense 64-row layers run as 128-row ones (above)
 }
 
 }  // namespace crisp
