@@ -143,6 +143,41 @@ def compare_pe(gpu_sets, ores: O.HeadResult, gamma: float, where=""):
     assert n_bad == 0, f"{where}: {n_bad} PE pairs differ outside the E4 band, first {first}, t*={float(tstar)}"
 
 
+def check_pe_threshold(row_ptr_h: np.ndarray, col_idx_h: np.ndarray, At: np.ndarray, gamma: float, where=""):
+    """PE parity for layers too large for the oracle's full pair sort (Alg. 4).  P_sel is
+    the prefix of the A_tilde-descending order whose mass first reaches gamma, so with t*
+    the value of its last pair: every causal pair above t* is selected and every pair below
+    it is not, except the forced {0, qb} blocks (R18).  The E4 band is exempt: values within
+    BAND of t*, and, when the mass sum is within BAND of gamma at the cut, of the next
+    value too.  Ties at t* are ordered by flat index in the oracle; they lie in the band.
+    row_ptr_h, col_idx_h: one head's CSR; At: the oracle's [N_b, N_b] A_tilde."""
+    nb = At.shape[0]
+    causal = np.tri(nb, dtype=bool)
+    vals = At.astype(np.float32)
+    desc = np.sort(vals[causal])[::-1]
+    csum = np.cumsum(desc.astype(np.float64))
+    g = float(np.float32(gamma))
+    hit = np.nonzero(csum >= g)[0]
+    kstar = int(hit[0]) + 1 if len(hit) else len(desc)
+    tstar = float(desc[kstar - 1])
+    lo, hi = tstar * (1 - BAND), tstar * (1 + BAND)
+    near_cut = (kstar >= 2 and abs(csum[kstar - 2] - g) <= BAND * g) or abs(csum[kstar - 1] - g) <= BAND * g
+    if near_cut and kstar < len(desc):
+        lo = min(lo, float(desc[kstar]) * (1 - BAND))
+    mask = np.zeros((nb, nb), dtype=bool)
+    mask[np.repeat(np.arange(nb), np.diff(row_ptr_h)), col_idx_h[:row_ptr_h[-1]]] = True
+    assert not (mask & ~causal).any(), f"{where}: pair above the diagonal"
+    forced = np.zeros((nb, nb), dtype=bool)
+    forced[:, 0] = True
+    forced[np.arange(nb), np.arange(nb)] = True
+    assert mask[forced].all(), f"{where}: forced block missing"
+    missing = causal & (vals > hi) & ~mask
+    extra = causal & ~forced & (vals < lo) & mask
+    assert not missing.any(), f"{where}: {int(missing.sum())} pairs above t*={tstar:.4g} not selected"
+    assert not extra.any(), f"{where}: {int(extra.sum())} pairs below t*={tstar:.4g} selected"
+    return kstar, tstar
+
+
 def compare_attention(o_gpu: np.ndarray, o_ref: np.ndarray, rows=None, where=""):
     if rows is not None:
         o_gpu, o_ref = o_gpu[rows], o_ref[rows]

@@ -343,6 +343,87 @@ def test_long_layer_one_unit_per_workgroup(block):
         del Qh, Kh, Vh
 
 
+def _check_rows_on_gpu(rp, ci, nb, where):
+    """Structural invariants of one head's CSR, on the device: rows non-empty, ascending and
+    unique, within [0, qb], first entry 0 and last entry qb."""
+    r = rp.long()
+    tot = int(r[-1])
+    c = ci[:tot].long()
+    starts, ends = r[:-1], r[1:]
+    assert bool((ends > starts).all()), f"{where}: empty row"
+    qbs = torch.arange(nb, device=c.device)
+    assert bool((c[starts] == 0).all()) and bool((c[ends - 1] == qbs).all()), f"{where}: forced blocks"
+    rowid = torch.repeat_interleave(qbs, ends - starts)
+    assert bool((c >= 0).all()) and bool((c <= rowid).all()), f"{where}: block outside [0, qb]"
+    same_row = rowid[1:] == rowid[:-1]
+    assert bool((c[1:][same_row] > c[:-1][same_row]).all()), f"{where}: row not ascending"
+
+
+def test_max_length_layer():
+    """The longest supported layer: 2^21 tokens (N_b = 16384 at B = 128), 17 query heads on
+    one KV head.  Head 16's CSR region starts past 2^31 entries, so every offset on the path
+    must be 64-bit.  Every head: structural invariants.  Head 16 and the last head of the
+    other route: scores and route against the oracle, a VS head's sets exactly (E1/E2), a
+    PE head's pairs against the oracle's A_tilde threshold (E4; the full pair sort is too
+    large here), and sampled attention rows."""
+    C = _crisp()
+    n, block, hq = 1 << 21, 128, 17
+    nb = n // block
+    cfg = custom_config(n, hq, 1, block=block, config_id=190)
+    _say(f"max length: {cfg.name}: generate and run the layer")
+    q, k, v, specs = make_layer(cfg, device=DEV)
+    params = C.make_params()
+    o, route, rp, ci = C.crisp_prefill_attn(q, k, v, params, block, return_lists=True)
+    cs, pv, ps = C.crisp_estimate(q, k, params, block)
+    torch.cuda.synchronize()
+    assert ci.shape[1] * (hq - 1) > 2 ** 31 - 1
+    for h in range(hq):
+        _check_rows_on_gpu(rp[h], ci[h], nb, f"max length h{h}")
+    route = route.cpu().numpy()
+    cs, pv, ps = cs.cpu().numpy(), pv.cpu().numpy(), ps.cpu().numpy()
+    op = _oracle_params(params, block)
+    s = op.scale(128)
+    last = hq - 1
+    other = max(h for h in range(hq) if specs[h].kind != specs[last].kind)
+    Kh, Vh = to_f64(k[0]), to_f64(v[0])
+    for h in (last, other):
+        w = f"max length h{h} ({specs[h].kind})"
+        _say(f"  oracle for {w}")
+        Qh = to_f64(q[h])
+        ahat = O.proxy_attention(Qh, Kh, block, s)
+        res = O.HeadResult(route=0, c_struct=O.c_struct(ahat, n, op.w_sink, op.w_local), p_v=None, p_s=None)
+        _, _, res.p_v, res.p_s = O.vs_scores(ahat, n, block)
+        del ahat
+        res.route = O.route(res.c_struct, op.tau_proxy)
+        PR.compare_scores(cs[h], pv[h], ps[h], res, where=w)
+        assert route[h] == res.route, f"{w}: route gpu {route[h]} oracle {res.route}"
+        rph = rp[h].cpu().numpy().astype(np.int64)
+        cih = ci[h, :int(rph[-1])].cpu().numpy()
+        if res.route == O.ROUTE_VS:
+            km = op.k_min(block)
+            sets = O.vs_block_sets(O.vs_select(res.p_v, op.alpha, km), O.vs_select(res.p_s, op.alpha, km), nb)
+            gsets = [cih[rph[qb]:rph[qb + 1]].tolist() for qb in range(nb)]
+            ex_v = PR.vs_direction_exempt(res.p_v, op.alpha, km)[1]
+            ex_s = PR.vs_direction_exempt(res.p_s, op.alpha, km)[1]
+            for qb in range(nb):
+                for kb in set(gsets[qb]) ^ set(sets[qb]):
+                    assert kb in ex_v or (nb - 1 - (qb - kb)) in ex_s, f"{w}: row {qb} block {kb}"
+            qbs = [0, nb // 2, nb - 1]
+        else:
+            At = O.pe_scores(Qh, Kh, block, s)
+            PR.check_pe_threshold(rph, cih, At, op.gamma, where=w)
+            del At
+            qbs = [1, nb // 64]
+            gsets = [[] for _ in range(nb)]
+            for qb in qbs:
+                gsets[qb] = cih[rph[qb]:rph[qb + 1]].tolist()
+        _say(f"  attention rows for {w}")
+        ref = O.sparse_attention(Qh, Kh, Vh, gsets, block, s, qbs=qbs)
+        rows = PR.qb_rows(qbs, block, n)
+        PR.compare_attention(to_f64(o[h][torch.from_numpy(rows).to(DEV)]), ref[rows], where=w + " attn")
+        del Qh, ref
+
+
 @pytest.mark.parametrize("alpha,block", [(0.5, 64), (1.0, 128), (2.0, 128), (1.0, 64)])
 def test_stress_config4(alpha, block):
     C = _crisp()
