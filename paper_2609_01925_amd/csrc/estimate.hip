@@ -50,16 +50,22 @@ __device__ __forceinline__ void load_q_hat(const EstArgs& a, int h, int r, int l
   }
 }
 
-__device__ __forceinline__ void load_k_tile(char* buf, const uint16_t* Kg, int key0, int n, int tid) {
+// K tile of 64 keys (keys at or past n read as 0): 16 bytes x 4 per thread into
+// registers, then into an LDS buffer.  The next tile is loaded into registers
+// before the current one's MFMAs, so its latency overlaps them.
+__device__ __forceinline__ void load_k_regs(u32x4 (&t)[4], const uint16_t* Kg, int key0, int n, int tid) {
   const int c = tid & 15;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int r = (tid >> 4) + 16 * i;
-    const int key = key0 + r;
-    u32x4 val = u32x4{0, 0, 0, 0};
-    if (key < n) val = *reinterpret_cast<const u32x4*>(Kg + (size_t)key * kHeadDim + 8 * c);
-    *reinterpret_cast<u32x4*>(buf + lds_off(r, 8 * c)) = val;
+    const int key = key0 + (tid >> 4) + 16 * i;
+    t[i] = key < n ? *reinterpret_cast<const u32x4*>(Kg + (size_t)key * kHeadDim + 8 * c) : u32x4{0, 0, 0, 0};
   }
+}
+
+__device__ __forceinline__ void store_k_regs(char* buf, const u32x4 (&t)[4], int tid) {
+  const int c = tid & 15;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(buf + lds_off((tid >> 4) + 16 * i, 8 * c)) = t[i];
 }
 
 __device__ __forceinline__ void scores(const char* kbuf, const bf16x8 (&qf)[8], int l, f32x16 (&s)[2]) {
@@ -92,9 +98,12 @@ __global__ __launch_bounds__(NT) void est_rowstats(EstArgs a) {
   key_hi = key_hi < a.n ? key_hi : a.n;
   float m_run = -__builtin_inff(), l_run = 0.f;
   int buf = 0;
+  u32x4 pre[4];
+  if (key_lo < key_hi) load_k_regs(pre, Kg, key_lo, a.n, tid);
   for (int key0 = key_lo; key0 < key_hi; key0 += BK, buf ^= 1) {
     char* kb = smem + buf * kTileBytes;
-    load_k_tile(kb, Kg, key0, a.n, tid);
+    store_k_regs(kb, pre, tid);
+    if (key0 + BK < key_hi) load_k_regs(pre, Kg, key0 + BK, a.n, tid);
     __syncthreads();
     f32x16 s[2];
     scores(kb, qf, l, s);
@@ -125,20 +134,28 @@ __global__ __launch_bounds__(NT) void est_rowstats(EstArgs a) {
   }
 }
 
-// Combine the per-range row statistics.
-__global__ __launch_bounds__(128) void est_combine(EstArgs a) {
-  const int h = blockIdx.x, r = threadIdx.x;
-  if (r >= a.b) return;
-  const float* src = a.rowstat + ((size_t)h * a.splits * 128 + r) * 2;
+// Combine the per-range row statistics: eight lanes per proxy row, each taking every
+// eighth range, then a max and a sum over the eight (fixed order).  grid (hq, 4),
+// 256 threads = 32 rows x 8 lanes.
+__global__ __launch_bounds__(256) void est_combine(EstArgs a) {
+  const int h = blockIdx.x, j = threadIdx.x & 7;
+  const int r = 32 * blockIdx.y + (threadIdx.x >> 3);
+  const float2* src = reinterpret_cast<const float2*>(a.rowstat) + (size_t)h * a.splits * 128 + r;
   float M = -__builtin_inff();
-  for (int sp = 0; sp < a.splits; ++sp) M = fmaxf(M, src[(size_t)sp * 256]);
+  for (int sp = j; sp < a.splits; sp += 8) M = fmaxf(M, src[(size_t)sp * 128].x);
+#pragma unroll
+  for (int o = 1; o < 8; o <<= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
   float L = 0.f;
-  for (int sp = 0; sp < a.splits; ++sp) {
-    const float m = src[(size_t)sp * 256];
-    if (m != -__builtin_inff()) L += src[(size_t)sp * 256 + 1] * fast_exp2((m - M) * a.c);
+  for (int sp = j; sp < a.splits; sp += 8) {
+    const float2 ml = src[(size_t)sp * 128];
+    if (ml.x != -__builtin_inff()) L += ml.y * fast_exp2((ml.x - M) * a.c);
   }
-  a.rowfinal[((size_t)h * 128 + r) * 2] = M;
-  a.rowfinal[((size_t)h * 128 + r) * 2 + 1] = L;
+#pragma unroll
+  for (int o = 1; o < 8; o <<= 1) L += __shfl_xor(L, o, 64);
+  if (j == 0 && r < a.b) {
+    a.rowfinal[((size_t)h * 128 + r) * 2] = M;
+    a.rowfinal[((size_t)h * 128 + r) * 2 + 1] = L;
+  }
 }
 
 __device__ __forceinline__ void block_reduce4(float4 v, float4* red, int tid, float4* out) {
@@ -180,6 +197,8 @@ __global__ __launch_bounds__(NT) void est_reduce(EstArgs a) {
   const int J1 = (J0 + a.bps < a.nb) ? J0 + a.bps : a.nb;
   const int diag_off = a.b - 1 - r;  // key k of row r lies on the diagonal through (last row, k + diag_off)
   int buf = 0;
+  u32x4 pre[4];
+  if (J0 < J1) load_k_regs(pre, Kg, J0 * a.B, a.n, tid);
   for (int J = J0; J < J1; ++J) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     const int blo = J * a.B;
@@ -187,7 +206,9 @@ __global__ __launch_bounds__(NT) void est_reduce(EstArgs a) {
     const int split_at = (J + 1) * a.B;  // diagonal keys >= this fall into slash block J + 1
     for (int key0 = blo; key0 < bhi; key0 += BK, buf ^= 1) {
       char* kb = smem + buf * kTileBytes;
-      load_k_tile(kb, Kg, key0, a.n, tid);
+      store_k_regs(kb, pre, tid);
+      const int next = key0 + BK < bhi ? key0 + BK : (J + 1 < J1 ? (J + 1) * a.B : a.n);
+      if (next < a.n) load_k_regs(pre, Kg, next, a.n, tid);
       __syncthreads();
       f32x16 s[2];
       scores(kb, qf, l, s);
@@ -261,7 +282,7 @@ hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, 
   a.c_struct = c_struct; a.p_v = p_v; a.p_s = p_s;
   const int grid = d.hq * sp.splits;
   hipLaunchKernelGGL(est_rowstats, dim3(grid), dim3(NT), 0, stream, a);
-  hipLaunchKernelGGL(est_combine, dim3(d.hq), dim3(128), 0, stream, a);
+  hipLaunchKernelGGL(est_combine, dim3(d.hq, 4), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(est_reduce, dim3(grid), dim3(NT), 0, stream, a);
   hipLaunchKernelGGL(est_finalize, dim3(d.hq), dim3(256), 0, stream, a);
   return hipGetLastError();

@@ -112,6 +112,42 @@ __device__ int block_sum_1024(int x, int* wtot) {
   return s;
 }
 
+// Digit search of a radix select, by one whole wave: bins[0 .. nbins) (nbins a
+// multiple of 64) hold non-negative weights (counts or fixed-point masses) of the
+// candidates whose higher digits match, visited from bin nbins - 1 down.  Returns
+// the first bin at which the cumulative weight reaches need (>= 1), with *before
+// the weight of the bins above it, or -1 when the total stays below need.  Lane l
+// sums its own run of nbins / 64 bins; a prefix scan over the lanes finds the run
+// that crosses need, and only that lane walks its run.
+template <typename T>
+__device__ int wave_descend_find(const T* bins, int nbins, T need, T* before) {
+  const int l = lane_id();
+  const int per = nbins / 64;
+  const int top = nbins - 1 - per * l;
+  T own = 0;
+  for (int i = 0; i < per; ++i) own += bins[top - i];
+  T incl = own;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const T y = __shfl_up(incl, o, 64);
+    if (l >= o) incl += y;
+  }
+  const uint64_t hit = __ballot(incl >= need);
+  if (hit == 0) return -1;
+  const int lw = __builtin_ctzll(hit);
+  int d = 0;
+  T cum = incl - own;
+  if (l == lw) {
+    d = top;
+    for (int i = 0; i < per - 1; ++i, --d) {
+      if (cum + bins[d] >= need) break;
+      cum += bins[d];
+    }
+  }
+  *before = __shfl(cum, lw, 64);
+  return __shfl(d, lw, 64);
+}
+
 // k-th largest bit pattern (k >= 1) among fbits(p[0..nb)).
 __device__ uint32_t kth_largest(const float* p, int nb, int k, uint32_t* hist, int* sh) {
   const int tid = threadIdx.x;
@@ -125,14 +161,13 @@ __device__ uint32_t kth_largest(const float* p, int nb, int k, uint32_t* hist, i
       if ((b & pmask) == prefix) atomicAdd(&hist[(b >> shift) & 255u], 1u);
     }
     __syncthreads();
-    if (tid == 0) {
-      int cum = 0, d = 255;
-      for (; d > 0; --d) {
-        if (cum + (int)hist[d] >= rem) break;
-        cum += hist[d];
+    if (tid < 64) {
+      uint32_t cum = 0;
+      const int d = wave_descend_find<uint32_t>(hist, 256, (uint32_t)rem, &cum);
+      if (tid == 0) {  // the k-th largest exists, so d >= 0
+        sh[0] = d < 0 ? 0 : d;
+        sh[1] = rem - (int)cum;
       }
-      sh[0] = d;
-      sh[1] = rem - cum;
     }
     __syncthreads();
     prefix |= (uint32_t)sh[0] << shift;
@@ -194,15 +229,13 @@ __device__ int gamma_prefix(const float* p, int nb, float gamma, uint32_t* t_out
       if ((b & pmask) == prefix) atomicAdd(&hist[(b >> shift) & (uint32_t)(bins - 1)], fixed_mass(b));
     }
     __syncthreads();
-    if (tid == 0) {
+    if (tid < 64) {
       unsigned long long cum = 0;
-      int d = bins - 1;
-      for (; d >= 0; --d) {
-        if (cum + hist[d] >= need) break;
-        cum += hist[d];
+      const int d = wave_descend_find<unsigned long long>(hist, bins, need, &cum);
+      if (tid == 0) {
+        sh64[0] = d < 0 ? ~0ull : (unsigned long long)d;
+        sh64[1] = d < 0 ? 0ull : need - cum;
       }
-      sh64[0] = d < 0 ? ~0ull : (unsigned long long)d;
-      sh64[1] = d < 0 ? 0ull : need - cum;
     }
     __syncthreads();
     if (sh64[0] == ~0ull) {
@@ -563,7 +596,7 @@ __global__ __launch_bounds__(256) void sel_radix_hist(SelArgs a, int pass) {
 
 // Picks the digit where the descending cumulative mass reaches `need`.  grid hq, 256 threads.
 __global__ __launch_bounds__(256) void sel_radix_scan(SelArgs a, int pass) {
-  __shared__ unsigned long long part[256];
+  __shared__ unsigned long long bins[kRadixBins];
   const int h = blockIdx.x, tid = threadIdx.x;
   if (a.route[h] != 1) return;
   RState st = a.rstate[h];
@@ -572,38 +605,26 @@ __global__ __launch_bounds__(256) void sel_radix_scan(SelArgs a, int pass) {
   radix_digit(pass, shift, nbits);
   const int nbins = 1 << nbits;
   unsigned long long* H = a.rhist + (size_t)h * kRadixBins;
-  // thread tid owns bins [top - 8 tid - 7, top - 8 tid] (descending)
-  const int per = nbins / 256;
-  unsigned long long s = 0;
-  for (int i = 0; i < per; ++i) s += H[nbins - 1 - (tid * per + i)];
-  part[tid] = s;
+  for (int i = tid; i < nbins; i += 256) bins[i] = H[i];
   __syncthreads();
-  if (tid == 0) {
+  if (tid < 64) {
     unsigned long long cum = 0;
-    int t = 0;
-    for (; t < 256; ++t) {
-      if (cum + part[t] >= st.need) break;
-      cum += part[t];
-    }
-    if (t == 256) {
-      st.all = 1;  // total mass below gamma: keep every pair
-      st.ceq = ~0ull;
-    } else {
-      int bin = nbins - 1 - t * per;
-      for (int i = 0; i < per; ++i, --bin) {
-        if (cum + H[bin] >= st.need) break;
-        cum += H[bin];
+    const int bin = wave_descend_find<unsigned long long>(bins, nbins, st.need, &cum);
+    if (tid == 0) {
+      if (bin < 0) {
+        st.all = 1;  // total mass below gamma: keep every pair
+        st.ceq = ~0ull;
+      } else {
+        st.need -= cum;
+        st.prefix |= (uint32_t)bin << shift;
+        if (pass == 2) {
+          const unsigned long long ft = fixed_mass(st.prefix);
+          st.ceq = ft ? (st.need + ft - 1) / ft : ~0ull;
+        }
       }
-      st.need -= cum;
-      st.prefix |= (uint32_t)bin << shift;
-      if (pass == 2) {
-        const unsigned long long ft = fixed_mass(st.prefix);
-        st.ceq = ft ? (st.need + ft - 1) / ft : ~0ull;
-      }
+      a.rstate[h] = st;
     }
-    a.rstate[h] = st;
   }
-  __syncthreads();
   for (int i = tid; i < kRadixBins; i += 256) H[i] = 0ull;
 }
 
