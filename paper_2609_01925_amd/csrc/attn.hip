@@ -29,12 +29,15 @@
 // builds from the list lengths, so long PE rows start first and short VS rows
 // fill the tail.  Below 512k tokens a persistent grid pulls units from one list
 // per KV group, and the K/V tiles of a group stay in the caches of the XCDs that
-// serve it.  From 512k tokens on, rows are long enough that the workgroups of a
-// persistent grid drift apart along the key axis (the two workgroups sharing a
-// CU do not advance at the same rate, and each keeps its place for the whole
-// layer), so concurrent readers of a K/V tile no longer meet in L2: there the
-// grid has one workgroup per unit, each taking the next unit of a single
-// longest-first list, and units that start together advance together.
+// serve it; rows much longer than the layer's work per workgroup are split into
+// chunks whose partial results attn_combine merges.  From 512k tokens on, rows
+// are long enough that the workgroups of a persistent grid drift apart along the
+// key axis (the two workgroups sharing a CU do not advance at the same rate, and
+// each keeps its place for the whole layer), so concurrent readers of a K/V tile
+// no longer meet in L2: there the grid has one workgroup per unit, and every
+// workgroup takes the next unit of the group lists in order (one KV group after
+// the other, longest first within a group), so units that start together
+// advance together over the same group's K/V.
 #include <type_traits>
 
 #include "crisp_device.h"
@@ -57,6 +60,9 @@ struct Tile {
 constexpr float kSumLimit = 256.0f;          // a lane's tile sum of P above this forces a rescale
 constexpr int kCostBuckets = 8192;
 constexpr int kOneShotMinLen = 1 << 19;  // from this length on, sparse lists run one unit per workgroup
+constexpr int kSplitSlots = 1024;        // most partial-result slots of one launch
+constexpr int kMinChunk = 8;             // shortest chunk of a split row, in list entries
+constexpr int kItemUnitBits = 21;        // work item = unit | chunk << 21
 
 struct AttnArgs {
   const uint16_t* q;
@@ -69,6 +75,11 @@ struct AttnArgs {
   const int32_t* order;  // persistent mode: units sorted longest first
   int* counter;          // persistent mode: next position in `order`
   int one_shot;          // 1: one unit per workgroup, all units in one queue
+  int* slot_base;        // split rows: first partial slot of the row's chunks, else -1
+  int* split_rows;       // the split rows (any order)
+  float* parts;          // partial results per slot: O[BQ][128], m[BQ], l[BQ] (fp32)
+  int split_slots;       // partial slots available (0: rows are never split)
+  int grid;              // workgroups of the persistent grid
   int n, nb, hq, hkv, G;
   float c;        // softmax scale * log2(e)
   int map_mode;   // static grid: 0 natural order, 1 H_kv % 8 == 0, 2 8 % H_kv == 0
@@ -106,11 +117,11 @@ __device__ __forceinline__ bool map_unit(const AttnArgs& a, int bid, int& h, int
   return true;
 }
 
-// Persistent grid: queue slot of head h's KV group, and the slot the workgroups
-// on XCD x pop from first (XCDs beyond the groups' share start at an empty slot
-// and go straight to taking work from the others).
+// Queue slot of head h's KV group, and the slot the workgroups on XCD x pop from
+// first (XCDs beyond the groups' share start at an empty slot and go straight to
+// taking work from the others; with one unit per workgroup every workgroup
+// starts at slot 0, so the slots are emptied in order).
 __device__ __forceinline__ int unit_queue(const AttnArgs& a, int h) {
-  if (a.one_shot) return 0;
   const int g = h / a.G;
   if (a.hkv >= kNumXcd) return g % kNumXcd;
   return g * (kNumXcd / a.hkv);
@@ -121,6 +132,16 @@ __device__ __forceinline__ int home_queue(const AttnArgs& a, int x) {
   if (a.hkv >= kNumXcd) return x;
   const int r = kNumXcd / a.hkv;  // XCDs per group
   return x < a.hkv * r ? (x / r) * r : x;
+}
+
+// Entries of row (head, qb) of a sparse list, with row_ptr clamped to [0, col_cap]
+// exactly as the attention reads it.
+__device__ __forceinline__ int row_len(const AttnArgs& a, int head, int qb) {
+  const int32_t* rp = a.row_ptr + (size_t)head * (a.nb + 1);
+  int64_t b0 = rp[qb], e0 = rp[qb + 1];
+  b0 = b0 < 0 ? 0 : (b0 > a.col_cap ? a.col_cap : b0);
+  e0 = e0 < b0 ? b0 : (e0 > a.col_cap ? a.col_cap : e0);
+  return (int)(e0 - b0);
 }
 
 // Workgroup geometry for query blocks of BQ rows: QH halves of 32 queries per
@@ -316,10 +337,13 @@ __device__ __forceinline__ void pv_tile(int vbuf, const Offsets& off, const bf16
     }
 }
 
-// One (head, query block) unit.
+// One (head, query block) unit, or one chunk of a split row's list: entries
+// [chunk * csize, chunk * csize + csize) when part is given, whose unnormalised
+// O, row max and row sum then go to the partial slot part instead of o.
 template <int BQ, bool DENSE>
 __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, int lds0, const Offsets& off,
-                                          const Fetch<Geo<BQ>::kWaves>& fe, int tid) {
+                                          const Fetch<Geo<BQ>::kWaves>& fe, int tid, int chunk = 0, int csize = 0,
+                                          float* part = nullptr) {
   constexpr int QH = Geo<BQ>::kQH;
   constexpr int NW = Geo<BQ>::kWaves;
   constexpr int BK = Tile<BQ>::kBK, NMB = Tile<BQ>::kNMB;
@@ -346,6 +370,11 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
     beg = (int)b0;
     cnt = (int)(e0 - b0);
     cols = a.col_idx + (size_t)head * cap;
+    if (part != nullptr) {
+      const int lo = chunk * csize;
+      beg += lo;
+      cnt = cnt - lo < csize ? cnt - lo : csize;
+    }
   }
   const int T = cnt * TPB;
 
@@ -521,6 +550,28 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
     }
   }
 
+  if (!DENSE && part != nullptr) {
+    // partial result of one chunk: O unnormalised, the row max (of raw scores) and sum
+#pragma unroll
+    for (int h = 0; h < QH; ++h) {
+      const float l_tot = half_sum(l_run[h]);
+      const int r = qabs[h] - q0;
+      float* po = part + (size_t)r * kHeadDim;
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          const int d = 32 * db + 8 * i4 + 4 * (l >> 5);
+          *reinterpret_cast<float4*>(po + d) =
+              make_float4(o[h][db][4 * i4], o[h][db][4 * i4 + 1], o[h][db][4 * i4 + 2], o[h][db][4 * i4 + 3]);
+        }
+      if ((l >> 5) == 0) {
+        part[BQ * kHeadDim + r] = m_run[h];
+        part[BQ * kHeadDim + BQ + r] = l_tot;
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int h = 0; h < QH; ++h) {
     const float l_tot = half_sum(l_run[h]);
@@ -569,45 +620,74 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
   int* s_unit = reinterpret_cast<int*>(smem + 2 * Tile<BQ>::kRing);
   const int x0 = home_queue(a, blockIdx.x % kNumXcd);
   const int* start = a.counter + 8;
+  const int csize = a.counter[17];  // chunk length of split rows
+  constexpr size_t kSlotFloats = (size_t)BQ * (kHeadDim + 2);
+  // Queues this workgroup has seen run dry (thread 0): they are never tried again.
+  // A queue whose counter already reads past its end is skipped without an atomic
+  // (a stale read only costs an extra atomic: counters never decrease).
+  unsigned dry = 0u;
   for (;;) {
     __syncthreads();  // the previous unit is done with LDS and the unit slot
     if (tid == 0) {
       int unit = -1;
       for (int t = 0; t < kNumXcd && unit < 0; ++t) {
         const int x = (x0 + t) % kNumXcd;
+        if (dry & (1u << x)) continue;
         const int len = start[x + 1] - start[x];
-        if (len <= 0) continue;
+        if (len <= 0 || __hip_atomic_load(a.counter + x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= len) {
+          dry |= 1u << x;
+          continue;
+        }
         const int pos = atomicAdd(a.counter + x, 1);
-        if (pos < len) unit = a.order[start[x] + pos];
+        if (pos < len)
+          unit = a.order[start[x] + pos];
+        else
+          dry |= 1u << x;
       }
       *s_unit = unit;
     }
     __syncthreads();
-    const int unit = *s_unit;
-    if (unit < 0) break;
-    attn_unit<BQ, DENSE>(a, unit / a.nb, unit % a.nb, lds0, off, fe, tid);
+    const int item = *s_unit;
+    if (item < 0) break;
+    const int unit = item & ((1 << kItemUnitBits) - 1), chunk = item >> kItemUnitBits;
+    float* part = nullptr;
+    if (a.split_slots > 0) {
+      const int sb = a.slot_base[unit];
+      if (sb >= 0) part = a.parts + (size_t)(sb + chunk) * kSlotFloats;
+    }
+    attn_unit<BQ, DENSE>(a, unit / a.nb, unit % a.nb, lds0, off, fe, tid, chunk, csize, part);
     if (a.one_shot) break;
   }
 #endif  // __HIP_DEVICE_COMPILE__
 }
 
-// Work lists for the sparse kernel.  One-unit-per-workgroup mode keeps a single
-// queue (slot 0).  Persistent mode keeps one queue per KV group, in queue
-// slot g % 8 when there are >= 8 groups.  With fewer groups each group owns
-// r = 8 / H_kv XCDs that all pop from one shared queue (slot g * r): they then
-// work on the same query blocks at the same time, so the K/V tiles one XCD
-// brings in from HBM are still in the shared last-level cache when the other
-// XCDs of the group ask for them (separate queues let the XCDs of a group drift
-// apart over a long layer, and each then streams K/V from HBM on its own).
-// Within an XCD the group's heads share its L2.  Units are ordered longest first (a
-// counting sort of list lengths: exact up to 768 blocks, then in steps of 16).
-// One workgroup builds all queues and resets their counters; the order within
-// one length is arbitrary (it only decides which workgroup runs a unit, never a
-// result).  Layout of the schedule area: int counters[8], int start[9], then the
-// units at int offset 64.
+// Work lists for the sparse kernel: one queue per KV group, in queue slot g % 8
+// when there are >= 8 groups.  With fewer groups each group owns r = 8 / H_kv
+// XCDs that all pop from one shared queue (slot g * r): they then work on the
+// same query blocks at the same time, so the K/V tiles one XCD brings in from HBM
+// are still in the shared last-level cache when the other XCDs of the group ask
+// for them (separate queues let the XCDs of a group drift apart over a long
+// layer, and each then streams K/V from HBM on its own).  Within an XCD the
+// group's heads share its L2.  One-unit-per-workgroup mode empties the slots in
+// order.  Items are ordered longest first within a queue (a counting sort of
+// list lengths: exact up to 768 entries, then in steps of 16).
+//
+// Split rows (persistent mode): a workgroup runs a row's tiles one after the
+// other, so when the longest row holds more entries than the layer's work per
+// workgroup (short layers, few heads), that row alone would set the kernel's
+// time.  With G' = min(grid, slots / 2) and T the total of all rows' entries,
+// rows longer than C = max(ceil(T / G'), 8, ceil(N_b / 1024)) are cut into
+// ceil(L / C) chunks, each a work item of its own that leaves a partial result
+// in a slot; attn_combine merges them.  Chunks number at most T / C + (rows
+// longer than C) <= 2 G' <= slots.  The decision depends only on the lists and
+// the grid, so results do not depend on timing.
+//
+// One workgroup builds everything and resets the queue counters; the order
+// within one length is arbitrary (it only decides which workgroup runs an item,
+// never a result).  Schedule area: int counters[8], int start[9], int C (at 17,
+// INT_MAX when no row is split), int split rows (at 18); items from int offset
+// 64; then slot_base[units], split_rows[slots / 2] and the partial slots.
 constexpr int kQueueBuckets = kCostBuckets / kNumXcd;  // 1024 cost buckets per XCD queue
-
-
 
 __device__ __forceinline__ int cost_bucket(int64_t c) {
   c = c < 0 ? 0 : c;
@@ -618,29 +698,66 @@ __device__ __forceinline__ int cost_bucket(int64_t c) {
 __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
   __shared__ int hist[kCostBuckets];
   __shared__ int part[1024];
+  __shared__ unsigned long long s_tot;
+  __shared__ int s_max, s_slots, s_split;
   const int tid = threadIdx.x;
   const int total = a.hq * a.nb;
   for (int i = tid; i < kCostBuckets; i += 1024) hist[i] = 0;
+  if (tid == 0) {
+    s_tot = 0ull;
+    s_max = 0;
+    s_slots = 0;
+    s_split = 0;
+  }
   __syncthreads();
-  // key: queue-major, longest first inside a queue
-  auto key = [&](int u) {
-    const int h = u / a.nb, qb = u % a.nb;
-    const int32_t* rp = a.row_ptr + (size_t)h * (a.nb + 1);
-    const int c = cost_bucket((int64_t)rp[qb + 1] - (int64_t)rp[qb]);
-    return unit_queue(a, h) * kQueueBuckets + (kQueueBuckets - 1 - c);
+  int C = 0x7fffffff;
+  if (a.split_slots > 0) {
+    unsigned long long t = 0;
+    int mx = 0;
+    for (int u = tid; u < total; u += 1024) {
+      const int L = row_len(a, u / a.nb, u % a.nb);
+      t += (unsigned long long)L;
+      mx = L > mx ? L : mx;
+    }
+    atomicAdd(&s_tot, t);
+    atomicMax(&s_max, mx);
+    __syncthreads();
+    long long gp = a.split_slots / 2;
+    gp = a.grid < gp ? a.grid : gp;
+    gp = gp < 1 ? 1 : gp;
+    long long c = (long long)((s_tot + (unsigned long long)gp - 1) / (unsigned long long)gp);
+    c = c > kMinChunk ? c : kMinChunk;
+    const long long cmin = (a.nb + 1023) / 1024;
+    c = c > cmin ? c : cmin;
+    if (s_max > c) C = (int)c;
+  }
+  auto key = [&](int h, int len) {
+    return unit_queue(a, h) * kQueueBuckets + (kQueueBuckets - 1 - cost_bucket(len));
   };
-  for (int u = tid; u < total; u += 1024) atomicAdd(&hist[key(u)], 1);
+  for (int u = tid; u < total; u += 1024) {
+    const int h = u / a.nb;
+    const int L = row_len(a, h, u % a.nb);
+    if (L > C) {
+      const int k = (L + C - 1) / C;
+      for (int c = 0; c < k; ++c) atomicAdd(&hist[key(h, L - c * C < C ? L - c * C : C)], 1);
+      a.slot_base[u] = atomicAdd(&s_slots, k);
+      a.split_rows[atomicAdd(&s_split, 1)] = u;
+    } else {
+      atomicAdd(&hist[key(h, L)], 1);
+      if (a.split_slots > 0) a.slot_base[u] = -1;
+    }
+  }
   __syncthreads();
   // exclusive scan over the keys, 8 per thread
   constexpr int per = kCostBuckets / 1024;
   int loc[per];
-  int s = 0;
+  int sum = 0;
 #pragma unroll
   for (int i = 0; i < per; ++i) {
-    loc[i] = s;
-    s += hist[tid * per + i];
+    loc[i] = sum;
+    sum += hist[tid * per + i];
   }
-  part[tid] = s;
+  part[tid] = sum;
   __syncthreads();
   for (int o = 1; o < 1024; o <<= 1) {
     const int x = tid >= o ? part[tid - o] : 0;
@@ -648,7 +765,8 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
     part[tid] += x;
     __syncthreads();
   }
-  const int base = part[tid] - s;
+  const int base = part[tid] - sum;
+  const int n_items = part[1023];
 #pragma unroll
   for (int i = 0; i < per; ++i) hist[tid * per + i] = base + loc[i];
   __syncthreads();
@@ -657,11 +775,78 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
     a.counter[tid] = 0;
     a.counter[8 + tid] = hist[tid * kQueueBuckets];
   }
-  if (tid == 0) a.counter[8 + kNumXcd] = total;
+  if (tid == 0) {
+    a.counter[8 + kNumXcd] = n_items;
+    a.counter[17] = C;
+    a.counter[18] = s_split;
+  }
   __syncthreads();
   for (int u = tid; u < total; u += 1024) {
-    const int pos = atomicAdd(&hist[key(u)], 1);
-    const_cast<int32_t*>(a.order)[pos] = u;
+    const int h = u / a.nb;
+    const int L = row_len(a, h, u % a.nb);
+    if (L > C) {
+      const int k = (L + C - 1) / C;
+      for (int c = 0; c < k; ++c) {
+        const int pos = atomicAdd(&hist[key(h, L - c * C < C ? L - c * C : C)], 1);
+        const_cast<int32_t*>(a.order)[pos] = u | (c << kItemUnitBits);
+      }
+    } else {
+      const int pos = atomicAdd(&hist[key(h, L)], 1);
+      const_cast<int32_t*>(a.order)[pos] = u;
+    }
+  }
+}
+
+// Merges the chunks of each split row in chunk order:
+//   O = sum_c w_c O_c / sum_c w_c l_c,  w_c = 2^((m_c - M) c),  M = max_c m_c
+// (chunks whose keys are all masked have m_c = -inf and weigh nothing).  grid
+// slots / 2 (workgroups past the number of split rows exit), 256 threads: BQ
+// query rows x 256 / BQ lanes, each lane 128 * BQ / 256 dims.
+template <int BQ>
+__global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
+  const int i = blockIdx.x;
+  if (i >= a.counter[18]) return;
+  const int C = a.counter[17];
+  const int u = a.split_rows[i];
+  const int head = u / a.nb, qb = u % a.nb;
+  const int k = (row_len(a, head, qb) + C - 1) / C;
+  constexpr int TPR = 256 / BQ, DPT = kHeadDim / TPR;
+  constexpr size_t kSlotFloats = (size_t)BQ * (kHeadDim + 2);
+  const int r = threadIdx.x / TPR, d0 = (threadIdx.x % TPR) * DPT;
+  const float* base = a.parts + (size_t)a.slot_base[u] * kSlotFloats;
+  float M = -__builtin_inff();
+  for (int c = 0; c < k; ++c) M = fmaxf(M, base[c * kSlotFloats + BQ * kHeadDim + r]);
+  float acc[DPT];
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) acc[e] = 0.f;
+  float lsum = 0.f;
+  for (int c = 0; c < k; ++c) {
+    const float* sl = base + c * kSlotFloats;
+    const float m = sl[BQ * kHeadDim + r];
+    if (m == -__builtin_inff()) continue;
+    const float w = fast_exp2((m - M) * a.c);
+    lsum += w * sl[BQ * kHeadDim + BQ + r];
+    const float4* po = reinterpret_cast<const float4*>(sl + (size_t)r * kHeadDim + d0);
+#pragma unroll
+    for (int e = 0; e < DPT / 4; ++e) {
+      const float4 v = po[e];
+      acc[4 * e] += w * v.x;
+      acc[4 * e + 1] += w * v.y;
+      acc[4 * e + 2] += w * v.z;
+      acc[4 * e + 3] += w * v.w;
+    }
+  }
+  const int q = qb * BQ + r;
+  if (q >= a.n) return;
+  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+  uint16_t* orow = a.o + ((size_t)head * a.n + q) * kHeadDim + d0;
+#pragma unroll
+  for (int e = 0; e < DPT / 4; ++e) {
+    const bf16x2 lo = pack_bf16(acc[4 * e] * inv, acc[4 * e + 1] * inv);
+    const bf16x2 hi = pack_bf16(acc[4 * e + 2] * inv, acc[4 * e + 3] * inv);
+    bf16x4 v4;
+    v4[0] = lo[0]; v4[1] = lo[1]; v4[2] = hi[0]; v4[3] = hi[1];
+    *reinterpret_cast<bf16x4*>(orow + 4 * e) = v4;
   }
 }
 
@@ -688,7 +873,32 @@ int persistent_grid() {
 
 }  // namespace
 
-size_t attn_schedule_bytes(const Dims& d) { return ((size_t)d.hq * d.nb + 64) * sizeof(int32_t); }
+// Schedule area of the sparse kernel: header and items, then (when rows may be
+// split: persistent mode, fewer than 2^21 units) slot_base, split_rows and the
+// partial slots.  Slots: min(1024, 2 x units).
+struct SchedLayout {
+  int slots;
+  size_t slot_base, split_rows, parts, total;
+};
+
+SchedLayout sched_layout(const Dims& d) {
+  SchedLayout s;
+  const size_t units = (size_t)d.hq * d.nb;
+  const bool split = d.n < kOneShotMinLen && units < ((size_t)1 << kItemUnitBits);
+  s.slots = split ? (int)(2 * units < (size_t)kSplitSlots ? 2 * units : (size_t)kSplitSlots) : 0;
+  size_t off = (64 + units + (size_t)s.slots) * sizeof(int32_t);
+  s.slot_base = off;
+  if (s.slots > 0) off += units * sizeof(int32_t);
+  s.split_rows = off;
+  off += (size_t)(s.slots / 2) * sizeof(int32_t);
+  off = (off + 255) & ~(size_t)255;
+  s.parts = off;
+  off += (size_t)s.slots * d.B * (kHeadDim + 2) * sizeof(float);
+  s.total = off;
+  return s;
+}
+
+size_t attn_schedule_bytes(const Dims& d) { return sched_layout(d).total; }
 
 hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                        const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, bool dense,
@@ -707,6 +917,7 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
   a.q = q; a.k = k; a.v = v; a.o = o;
   a.row_ptr = row_ptr; a.col_idx = col_idx; a.col_cap = col_cap;
   a.order = nullptr; a.counter = nullptr; a.one_shot = 0;
+  a.slot_base = nullptr; a.split_rows = nullptr; a.parts = nullptr; a.split_slots = 0; a.grid = 0;
   a.n = d.n; a.nb = d.nb; a.hq = d.hq; a.hkv = d.hkv; a.G = d.G;
   a.c = scale * kLog2e;
   int grid;
@@ -721,17 +932,35 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
     grid = d.hq * d.nb;
   }
   if (!dense && sched != nullptr) {
-    a.counter = reinterpret_cast<int*>(sched);
-    a.order = reinterpret_cast<const int32_t*>(sched) + 64;
+    char* sc = reinterpret_cast<char*>(sched);
+    const SchedLayout sl = sched_layout(d);
+    a.counter = reinterpret_cast<int*>(sc);
+    a.order = reinterpret_cast<const int32_t*>(sc) + 64;
+    a.one_shot = d.n >= kOneShotMinLen ? 1 : 0;
+    a.split_slots = sl.slots;
+    if (sl.slots > 0) {
+      a.slot_base = reinterpret_cast<int*>(sc + sl.slot_base);
+      a.split_rows = reinterpret_cast<int*>(sc + sl.split_rows);
+      a.parts = reinterpret_cast<float*>(sc + sl.parts);
+    }
+    const int pg = d.B == 128 ? persistent_grid<128>() : persistent_grid<64>();
+    grid = a.one_shot || pg > d.hq * d.nb ? d.hq * d.nb : pg;
+    a.grid = grid;
     hipLaunchKernelGGL(attn_schedule, dim3(1), dim3(1024), 0, stream, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    a.one_shot = d.n >= kOneShotMinLen ? 1 : 0;
-    const int pg = d.B == 128 ? persistent_grid<128>() : persistent_grid<64>();
-    grid = a.one_shot || pg > d.hq * d.nb ? d.hq * d.nb : pg;
   }
-  if (d.B == 128) return dense ? launch_t<128, true>(a, grid, stream) : launch_t<128, false>(a, grid, stream);
-  return launch_t<64, false>(a, grid, stream);  // dense 64-row layers run as 128-row ones (above)
+  hipError_t e;
+  if (d.B == 128)
+    e = dense ? launch_t<128, true>(a, grid, stream) : launch_t<128, false>(a, grid, stream);
+  else
+    e = launch_t<64, false>(a, grid, stream);  // dense 64-row layers run as 128-row ones (above)
+  if (e != hipSuccess || a.split_slots == 0) return e;
+  if (d.B == 128)
+    hipLaunchKernelGGL(attn_combine<128>, dim3(a.split_slots / 2), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(attn_combine<64>, dim3(a.split_slots / 2), dim3(256), 0, stream, a);
+  return hipGetLastError();
 }
 
 }  // namespace crisp

@@ -96,15 +96,18 @@ def test_sparse_attention_on_given_lists(n, block, junk):
     rp, ci, sets = _random_lists(hq, nb, seed=7, junk=junk)
     o = C.crisp_sparse_attn(q.to(DEV), k.to(DEV), v.to(DEV), torch.from_numpy(rp).to(DEV),
                             torch.from_numpy(ci).to(DEV), block)
+    o_again = C.crisp_sparse_attn(q.to(DEV), k.to(DEV), v.to(DEV), torch.from_numpy(rp).to(DEV),
+                                  torch.from_numpy(ci).to(DEV), block)
     o_fixed = C.crisp_sparse_attn(q.to(DEV), k.to(DEV), v.to(DEV), torch.from_numpy(rp).to(DEV),
                                   torch.from_numpy(ci).to(DEV), block, balance=False)
     torch.cuda.synchronize()
-    assert torch.equal(o, o_fixed)   # the work order never changes a result
-    og = to_f64(o)
+    assert torch.equal(o, o_again)   # which workgroup runs an item never changes a result
     Q, K, V = to_f64(q), to_f64(k), to_f64(v)
-    for h in range(hq):
-        ref = O.sparse_attention(Q[h], K[h // 2], V[h // 2], sets[h], block, 1 / math.sqrt(128))
-        PR.compare_attention(og[h], ref, where=f"sparse h{h}")
+    for name, out in (("work list", o), ("fixed order", o_fixed)):
+        og = to_f64(out)
+        for h in range(hq):
+            ref = O.sparse_attention(Q[h], K[h // 2], V[h // 2], sets[h], block, 1 / math.sqrt(128))
+            PR.compare_attention(og[h], ref, where=f"sparse {name} h{h}")
 
 
 @pytest.mark.parametrize("block", [128, 64])
@@ -128,7 +131,8 @@ def test_full_lists_equal_dense_bitwise(block):
             rp[h, qb] = off
             off += qb + 1
         rp[h, nb] = off
-    o_s = C.crisp_sparse_attn(q, k, v, torch.from_numpy(rp).to(DEV), torch.from_numpy(ci).to(DEV), block)
+    o_s = C.crisp_sparse_attn(q, k, v, torch.from_numpy(rp).to(DEV), torch.from_numpy(ci).to(DEV), block,
+                              balance=False)
     o_d = C.crisp_dense_attn(q, k, v, block)
     torch.cuda.synchronize()
     if block == 128:
@@ -140,6 +144,71 @@ def test_full_lists_equal_dense_bitwise(block):
     for h in range(hq):
         ref = O.sparse_attention(Q[h], K[0], V[0], sets, block, 1 / math.sqrt(128))
         PR.compare_attention(og[h], ref, where=f"full lists B=64 h{h}")
+
+
+def _csr_from_rows(rows, nb):
+    rp = np.zeros((1, nb + 1), np.int32)
+    flat = [x for r in rows for x in r]
+    ci = np.zeros((1, max(nb * (nb + 1) // 2, len(flat))), np.int32)
+    ci[0, :len(flat)] = flat
+    rp[0, 1:] = np.cumsum([len(r) for r in rows])
+    return rp, ci
+
+
+@pytest.mark.parametrize("case", ["full-b128", "full-b64-ragged", "junk-first-chunk"])
+def test_split_rows(case):
+    """Rows far longer than the layer's work per workgroup are split into chunks whose
+    partial results are merged (online-softmax merge of (O, m, l) in chunk order).  Few heads
+    with full causal lists force it; the merged rows match the oracle, runs are bitwise
+    repeatable, and the split rows round differently from the unsplit fixed-order launch
+    (which shows the split path ran).  junk-first-chunk: a row's first chunk holds only
+    invalid entries (m = -inf, weighing nothing in the merge)."""
+    C = _crisp()
+    _say(f"split rows {case}")
+    if case == "junk-first-chunk":
+        # rows from N_b / 2 on: even ones [-5] * 60 + [0, qb] (first chunk all invalid, then
+        # merged with weight exactly 1), odd ones ten valid blocks at each end around 40
+        # invalid entries (both chunks count)
+        n, block, hq = 8192, 128, 1
+        nb = n // block
+        rows, sets = [], []
+        for qb in range(nb):
+            if qb < nb // 2:
+                r = sorted({0, qb})
+            elif qb % 2 == 0:
+                r = [-5] * 60 + [0, qb]
+            else:
+                r = list(range(10)) + [-5] * 40 + list(range(qb - 9, qb + 1))
+            rows.append(r)
+            sets.append(sorted({x for x in r if 0 <= x <= qb}))
+        rp, ci = _csr_from_rows(rows, nb)
+        long_rows = [qb for qb in range(nb // 2, nb) if qb % 2]
+    else:
+        n, block, hq = (16384, 128, 1) if case == "full-b128" else (8000, 64, 2)
+        nb = O.n_blocks(n, block)
+        sets = O.dense_causal_sets(nb)
+        rp = np.zeros((hq, nb + 1), np.int32)
+        ci = np.zeros((hq, nb * (nb + 1) // 2), np.int32)
+        for h in range(hq):
+            ci[h] = np.concatenate([np.asarray(s_, np.int32) for s_ in sets])
+            rp[h, 1:] = np.cumsum([len(s_) for s_ in sets])
+        long_rows = list(range(nb - nb // 4, nb))
+    q, k, v = _rand(hq, n, seed=21), _rand(1, n, seed=22), _rand(1, n, seed=23)
+    args = (q.to(DEV), k.to(DEV), v.to(DEV), torch.from_numpy(rp).to(DEV), torch.from_numpy(ci).to(DEV), block)
+    o1 = C.crisp_sparse_attn(*args)
+    o2 = C.crisp_sparse_attn(*args)
+    o_fixed = C.crisp_sparse_attn(*args, balance=False)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
+    rows_idx = torch.from_numpy(PR.qb_rows(long_rows, block, n)).to(DEV)
+    assert not torch.equal(o1[:, rows_idx], o_fixed[:, rows_idx]), "no row was split"
+    Q, K, V = to_f64(q), to_f64(k)[0], to_f64(v)[0]
+    qbs = sorted({0, 1, nb // 2, long_rows[0], nb - 2, nb - 1})
+    rows = PR.qb_rows(qbs, block, n)
+    for h in range(hq):
+        ref = O.sparse_attention(Q[h], K, V, sets, block, 1 / math.sqrt(128), qbs=qbs)
+        PR.compare_attention(to_f64(o1[h]), ref, rows=rows, where=f"{case} h{h}")
+        PR.compare_attention(to_f64(o1[h]), to_f64(o_fixed[h]), rows=rows, where=f"{case} h{h} vs fixed")
 
 
 def test_attention_custom_scale_and_empty_rows():
