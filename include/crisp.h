@@ -193,8 +193,12 @@ crisp_status crisp_sparse_workspace_size(const crisp_shape* shape, size_t* bytes
  * [0, col_cap_per_head], so a malformed list cannot cause an out-of-bounds access.
  * A row with no visible key gets o = 0.  softmax_scale 0 means 1/sqrt(d).
  * workspace_or_null (crisp_sparse_workspace_size bytes) holds a longest-first
- * work list that balances rows of very different lengths over the GPU; with
- * NULL the rows are processed in a fixed order (same results, less balance). */
+ * work list that balances rows of very different lengths over the GPU and, for
+ * layers shorter than 512k tokens, slots for partial results: a row far longer
+ * than the layer's work per workgroup is split into chunks whose softmax partials
+ * are merged in chunk order.  Results are repeatable for given lists; a split row
+ * differs from an unsplit one by floating-point rounding only.  With NULL the rows
+ * are processed whole, in a fixed order. */
 crisp_status crisp_sparse_attn(const crisp_shape* shape, float softmax_scale,
                                const crisp_bf16* q, const crisp_bf16* k, const crisp_bf16* v,
                                const int32_t* row_ptr, const int32_t* col_idx,

@@ -140,10 +140,39 @@ def _stream(device) -> ctypes.c_void_p:
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
-def _inputs(*ts: torch.Tensor):
+def _inputs(q: torch.Tensor, k: torch.Tensor, v: Optional[torch.Tensor] = None):
+    """q [H_q, n, d], k and v [H_kv, n, d]: contiguous bf16 on one CUDA device.  The C ABI
+    sees only pointers, so every size it will read is checked here."""
+    ts = (q, k) if v is None else (q, k, v)
     for t in ts:
         if not (t.is_cuda and t.dtype == torch.bfloat16 and t.is_contiguous() and t.dim() == 3):
             raise ValueError("q, k, v must be contiguous 3-d bf16 CUDA tensors [heads, seq, head_dim]")
+        if t.device != q.device:
+            raise ValueError("q, k, v must be on one device")
+    if k.shape[1:] != q.shape[1:]:
+        raise ValueError(f"k {tuple(k.shape)} does not match q {tuple(q.shape)} in seq_len and head_dim")
+    if v is not None and v.shape != k.shape:
+        raise ValueError(f"v {tuple(v.shape)} must have k's shape {tuple(k.shape)}")
+
+
+def _tensor(t: torch.Tensor, name: str, dtype, shape, device):
+    """A caller-given buffer: contiguous, of the given dtype and shape (None: any size in that
+    dimension) on the given device."""
+    ok = t.is_cuda and t.device == device and t.dtype == dtype and t.is_contiguous() and t.dim() == len(shape)
+    ok = ok and all(w is None or t.shape[i] == w for i, w in enumerate(shape))
+    if not ok:
+        raise ValueError(f"{name} must be a contiguous {dtype} CUDA tensor of shape {shape} on {device}, "
+                         f"got {t.dtype} {tuple(t.shape)} on {t.device}")
+
+
+def _tensor_out(out: torch.Tensor, q: torch.Tensor) -> torch.Tensor:
+    _tensor(out, "out", torch.bfloat16, tuple(q.shape), q.device)
+    return out
+
+
+def _ws(ws: torch.Tensor, device) -> torch.Tensor:
+    _tensor(ws, "ws", torch.uint8, (None,), device)
+    return ws
 
 
 def workspace(shape: CrispShape, device, prefill: bool = False) -> torch.Tensor:
@@ -161,7 +190,7 @@ def crisp_estimate(q: torch.Tensor, k: torch.Tensor, params: CrispParams, block:
     cs = torch.empty(q.shape[0], dtype=torch.float32, device=dev)
     pv = torch.empty(q.shape[0], nb, dtype=torch.float32, device=dev)
     ps = torch.empty(q.shape[0], nb, dtype=torch.float32, device=dev)
-    ws = workspace(sh, dev) if ws is None else ws
+    ws = workspace(sh, dev) if ws is None else _ws(ws, dev)
     _check(lib.crisp_estimate(ctypes.byref(sh), ctypes.byref(params), _ptr(q), _ptr(k), _ptr(cs), _ptr(pv), _ptr(ps),
                               _ptr(ws), ws.numel(), _stream(dev)), "crisp_estimate")
     return cs, pv, ps
@@ -173,8 +202,9 @@ def crisp_jsd(q: torch.Tensor, k: torch.Tensor, p_v: torch.Tensor, params: Crisp
     _inputs(q, k)
     sh = shape_of(q, k, block)
     dev = q.device
+    _tensor(p_v, "p_v", torch.float32, (q.shape[0], n_blocks(q.shape[1], block)), dev)
     jsd = torch.empty(q.shape[0], dtype=torch.float32, device=dev)
-    ws = workspace(sh, dev) if ws is None else ws
+    ws = workspace(sh, dev) if ws is None else _ws(ws, dev)
     _check(lib.crisp_jsd(ctypes.byref(sh), ctypes.byref(params), _ptr(q), _ptr(k), _ptr(p_v), _ptr(jsd), _ptr(ws),
                          ws.numel(), _stream(dev)), "crisp_jsd")
     return jsd
@@ -190,12 +220,15 @@ def crisp_route_select(q: torch.Tensor, k: torch.Tensor, c_struct: torch.Tensor,
     sh = shape_of(q, k, block)
     nb = n_blocks(q.shape[1], block)
     dev = q.device
+    _tensor(c_struct, "c_struct", torch.float32, (q.shape[0],), dev)
+    _tensor(p_v, "p_v", torch.float32, (q.shape[0], nb), dev)
+    _tensor(p_s, "p_s", torch.float32, (q.shape[0], nb), dev)
     cap = max(crisp_col_capacity(sh), 1)
     route = torch.empty(q.shape[0], dtype=torch.int8, device=dev)
     row_ptr = torch.empty(q.shape[0], nb + 1, dtype=torch.int32, device=dev)
     col_idx = torch.empty(q.shape[0], cap, dtype=torch.int32, device=dev)
     dmask = torch.empty(q.shape[0], 2, nb, dtype=torch.uint8, device=dev) if want_mask else None
-    ws = workspace(sh, dev) if ws is None else ws
+    ws = workspace(sh, dev) if ws is None else _ws(ws, dev)
     _check(lib.crisp_route_select(ctypes.byref(sh), ctypes.byref(params), _ptr(q), _ptr(k), _ptr(c_struct),
                                   _ptr(p_v), _ptr(p_s), _ptr(route), _ptr(row_ptr), _ptr(col_idx), cap,
                                   _ptr(dmask), _ptr(ws), ws.numel(), _stream(dev)), "crisp_route_select")
@@ -210,7 +243,11 @@ def crisp_sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, row_ptr
     workspace (fixed row order)."""
     _inputs(q, k, v)
     sh = shape_of(q, k, block)
-    o = torch.empty_like(q) if out is None else out
+    _tensor(row_ptr, "row_ptr", torch.int32, (q.shape[0], n_blocks(q.shape[1], block) + 1), q.device)
+    _tensor(col_idx, "col_idx", torch.int32, (q.shape[0], None), q.device)
+    o = torch.empty_like(q) if out is None else _tensor_out(out, q)
+    if balance and ws is not None:
+        _ws(ws, q.device)
     if balance and ws is None:
         ws = torch.empty(max(crisp_sparse_workspace_size(sh), 256), dtype=torch.uint8, device=q.device)
     if not balance:
@@ -226,7 +263,7 @@ def crisp_dense_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, block: i
     """Dense causal baseline with the same kernel -> o bf16 [H_q, n, d]."""
     _inputs(q, k, v)
     sh = shape_of(q, k, block)
-    o = torch.empty_like(q) if out is None else out
+    o = torch.empty_like(q) if out is None else _tensor_out(out, q)
     _check(lib.crisp_dense_attn(ctypes.byref(sh), softmax_scale, _ptr(q), _ptr(k), _ptr(v), _ptr(o),
                                 _stream(q.device)), "crisp_dense_attn")
     return o
@@ -239,7 +276,9 @@ def crisp_prefill_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, params
     _inputs(q, k, v)
     sh = shape_of(q, k, block)
     dev = q.device
-    o = torch.empty_like(q) if out is None else out
+    o = torch.empty_like(q) if out is None else _tensor_out(out, q)
+    if ws is not None:
+        _ws(ws, dev)
     if return_lists:
         nb = n_blocks(q.shape[1], block)
         cap = max(crisp_col_capacity(sh), 1)

@@ -642,3 +642,33 @@ def test_empty_layer_is_noop():
     k = torch.zeros(1, 0, 128, dtype=torch.bfloat16, device=DEV)
     C.crisp_prefill_attn(q, k, k, C.make_params(), 128)
     torch.cuda.synchronize()
+
+
+def test_binding_rejects_mismatched_tensors():
+    """The C ABI sees only pointers, so the binding checks every tensor's dtype, shape and
+    device before a call: a mismatch raises ValueError and nothing is launched."""
+    C = _crisp()
+    _say("binding validation")
+    n, block = 1024, 128
+    q, k, v = _rand(4, n).to(DEV), _rand(2, n).to(DEV), _rand(2, n).to(DEV)
+    nb = O.n_blocks(n, block)
+    rp = torch.zeros(4, nb + 1, dtype=torch.int32, device=DEV)
+    ci = torch.zeros(4, nb * (nb + 1) // 2, dtype=torch.int32, device=DEV)
+    bad = [
+        lambda: C.crisp_dense_attn(q, k, v[:, : n // 2].contiguous()),                       # v shorter than k
+        lambda: C.crisp_dense_attn(q, k, _rand(1, n).to(DEV)),                                # v heads != k heads
+        lambda: C.crisp_dense_attn(q, _rand(2, n // 2).to(DEV), _rand(2, n // 2).to(DEV)),   # k shorter than q
+        lambda: C.crisp_dense_attn(q, k, v, out=torch.empty(4, n, 64, dtype=torch.bfloat16, device=DEV)),
+        lambda: C.crisp_sparse_attn(q, k, v, rp[:, :-1].contiguous(), ci),                  # row_ptr one short
+        lambda: C.crisp_sparse_attn(q, k, v, rp.long(), ci),                                 # wrong dtype
+        lambda: C.crisp_sparse_attn(q, k, v, rp[:2].contiguous(), ci[:2].contiguous()),     # too few heads
+        lambda: C.crisp_sparse_attn(q, k, v, rp, ci, ws=torch.empty(64, dtype=torch.float32, device=DEV)),
+        lambda: C.crisp_prefill_attn(q, k, v, C.make_params(), block, out=q.float()),
+        lambda: C.crisp_jsd(q, k, torch.zeros(4, nb + 1, device=DEV), C.make_params(), block),
+        lambda: C.crisp_route_select(q, k, torch.zeros(3, device=DEV), torch.zeros(4, nb, device=DEV),
+                                     torch.zeros(4, nb, device=DEV), C.make_params(), block),
+    ]
+    for i, call in enumerate(bad):
+        with pytest.raises(ValueError):
+            call()
+    torch.cuda.synchronize()
