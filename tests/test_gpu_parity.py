@@ -672,3 +672,37 @@ def test_binding_rejects_mismatched_tensors():
         with pytest.raises(ValueError):
             call()
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("n,block", [(6000, 128), (4100, 64)])
+def test_prefill_in_a_hip_graph(n, block):
+    """The whole prefill (estimate, route/select, work lists, attention, merge of split rows)
+    enqueues only kernels on the caller's stream -- no allocation, copy, memset or host
+    synchronisation -- so it can be captured in a HIP graph.  Each replay, with eager work
+    and synchronisations between replays, gives the eager result bit for bit."""
+    C = _crisp()
+    _say(f"prefill in a HIP graph n={n} B={block}")
+    cfg = custom_config(n, 4, 2, block=block, config_id=195 + block // 64)
+    q, k, v, _ = make_layer(cfg, device=DEV)
+    params = C.make_params()
+    ws = C.workspace(C.shape_of(q, k, block), DEV, prefill=True)
+    o_eager = C.crisp_prefill_attn(q, k, v, params, block, ws=ws, out=torch.empty_like(q))
+    torch.cuda.synchronize()
+    o = torch.zeros_like(q)
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):  # warm-up on the capture stream
+        C.crisp_prefill_attn(q, k, v, params, block, ws=ws, out=o)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        C.crisp_prefill_attn(q, k, v, params, block, ws=ws, out=o)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        o.zero_()
+        C.crisp_dense_attn(q, k, v, block, out=torch.empty_like(q))  # unrelated eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o, o_eager), f"replay {rep} differs from the eager result"
