@@ -283,7 +283,7 @@ def cpu_baseline(cfg, res, budget_s=25.0):
     att_time, att_pairs, units = 0.0, 0, 0
     rng = np.random.default_rng(0)
     hs = list(sets.keys())
-    while time.perf_counter() - t0 < budget_s and units < 64:
+    while time.perf_counter() - t0 < budget_s and units < 512:
         h = hs[units % len(hs)]
         Qh, s = sets[h]
         qb = int(rng.integers(0, nb))
