@@ -3,7 +3,7 @@
 //
 // A workgroup computes one (query head, query block) unit at a time: BQ = B
 // query rows, BQ / 32 waves, each wave owning 32 query rows.  Keys are
-// streamed in tiles of 64.  Per tile and wave:
+// streamed in tiles of 64 (32 for 64-row blocks, below).  Per 64-key tile and wave:
 //   S^T (64 keys x 32 queries) = K_tile Q^T      16 x v_mfma_f32_32x32x16_bf16
 //   online softmax in fp32 (exp2, log2(e) folded into the scale)
 //   O^T (128 d x 32 queries) += V^T P^T          16 x v_mfma_f32_32x32x16_bf16
@@ -16,14 +16,16 @@
 // K and V tiles move from global memory straight into LDS with LDS-DMA loads
 // (buffer_load ... lds), two 2-deep rings (K, V) of 16 KB stages: 64 KB per
 // workgroup, so two workgroups share a CU and every SIMD interleaves two waves.
+// A 64-row block has a two-wave workgroup, so four must share a CU: its tiles
+// have 32 keys (32 KB of rings).
 // Step j of a unit overlaps three things: tile j's probabilities are formed
 // (against the running max) beside the PV product of tile j-1, then the scores
 // of tile j+1 are computed beside the row sums.  Each ring stage is refilled
 // one step before it is read, and the loop is expanded two steps at a time so
 // that every stage address is a compile-time immediate.  The running max is
-// only raised when some lane's tile sum of P exceeds 2^8 (then every P of that
-// lane does too at most): until then P may exceed 1 by at most 2^8, which fp32
-// and bf16 hold exactly as well, and the O accumulators are left untouched.
+// only raised when some lane's tile sum of P exceeds 2^8 (no P of a lane exceeds
+// its sum): until then P may exceed 1 by at most 2^8, which fp32 and bf16 hold
+// as exactly as values below 1, and the O accumulators are left untouched.
 //
 // Sparse lists are processed longest first from work lists that attn_schedule
 // builds from the list lengths, so long PE rows start first and short VS rows
@@ -687,7 +689,7 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
 // never a result).  Schedule area: int counters[8], int start[9], int C (at 17,
 // INT_MAX when no row is split), int split rows (at 18); items from int offset
 // 64; then slot_base[units], split_rows[slots / 2] and the partial slots.
-constexpr int kQueueBuckets = kCostBuckets / kNumXcd;  // 1024 cost buckets per XCD queue
+constexpr int kQueueBuckets = kCostBuckets / kNumXcd;  // 1024 cost buckets per queue
 
 __device__ __forceinline__ int cost_bucket(int64_t c) {
   c = c < 0 ? 0 : c;
