@@ -186,12 +186,10 @@ __global__ __launch_bounds__(NT) void est_reduce(EstArgs a) {
   const bool row_ok = r < a.b;
   bf16x8 qf[8];
   load_q_hat(a, h, r, l, qf);
-  float M = 0.f, invL = 0.f;
-  if (row_ok) {
-    M = a.rowfinal[((size_t)h * 128 + r) * 2];
-    invL = 1.f / a.rowfinal[((size_t)h * 128 + r) * 2 + 1];
-  }
-  const float mc = M * a.c;
+  // A_hat = 2^(s c - M c) / L = 2^(s c - mcl) with mcl = M c + log2 L; rows past b
+  // (64-row blocks) get mcl = +inf, so every entry of theirs is exactly 0.
+  float mcl = __builtin_inff();
+  if (row_ok) mcl = a.rowfinal[((size_t)h * 128 + r) * 2] * a.c + log2f(a.rowfinal[((size_t)h * 128 + r) * 2 + 1]);
   const uint16_t* Kg = a.k + (size_t)(h / a.G) * a.n * kHeadDim;
   const int J0 = sp * a.bps;
   const int J1 = (J0 + a.bps < a.nb) ? J0 + a.bps : a.nb;
@@ -200,10 +198,10 @@ __global__ __launch_bounds__(NT) void est_reduce(EstArgs a) {
   u32x4 pre[4];
   if (J0 < J1) load_k_regs(pre, Kg, J0 * a.B, a.n, tid);
   for (int J = J0; J < J1; ++J) {
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    float lo = 0.f, hi = 0.f, anc = 0.f;  // diagonal mass staying in J / moving to J + 1; anchor mass
     const int blo = J * a.B;
     const int bhi = blo + a.B < a.n ? blo + a.B : a.n;
-    const int split_at = (J + 1) * a.B;  // diagonal keys >= this fall into slash block J + 1
+    const int ksplit = (J + 1) * a.B - diag_off;  // keys >= this lie on diagonals of slash block J + 1
     for (int key0 = blo; key0 < bhi; key0 += BK, buf ^= 1) {
       char* kb = smem + buf * kTileBytes;
       store_k_regs(kb, pre, tid);
@@ -212,19 +210,32 @@ __global__ __launch_bounds__(NT) void est_reduce(EstArgs a) {
       __syncthreads();
       f32x16 s[2];
       scores(kb, qf, l, s);
+      // Tiles wholly before the first proxy row, inside the block and outside both anchor
+      // windows (all but a few) need no per-entry masks and no anchor sum.
+      const bool plain = key0 + BK - 1 <= a.n - a.b && key0 + BK <= bhi && key0 >= a.w_sink &&
+                         key0 + BK <= a.n - a.w_local;
+      if (plain) {
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+        for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = key_of(key0, mb, i, l);
-          float p = 0.f;
-          if (row_ok && key <= qi && key < bhi) p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc)) * invL;
-          acc.x += p;
-          if (key + diag_off < split_at) acc.y += p; else acc.z += p;
-          if (key < a.w_sink || key >= a.n - a.w_local) acc.w += p;
-        }
+          for (int i = 0; i < 16; ++i) {
+            const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mcl));
+            if (key_of(key0, mb, i, l) < ksplit) lo += p; else hi += p;
+          }
+      } else {
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int key = key_of(key0, mb, i, l);
+            float p = 0.f;
+            if (key <= qi && key < bhi) p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mcl));
+            if (key < ksplit) lo += p; else hi += p;
+            if (key < a.w_sink || key >= a.n - a.w_local) anc += p;
+          }
+      }
     }
-    block_reduce4(acc, red, tid, a.parts + (size_t)h * a.nb + J);
+    block_reduce4(make_float4(lo + hi, lo, hi, anc), red, tid, a.parts + (size_t)h * a.nb + J);
   }
 }
 
