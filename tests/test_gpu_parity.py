@@ -336,12 +336,29 @@ def test_config1_sampled():
     _check_layer(C, cfg, C.make_params(), heads=heads, qbs_per_head=qsel, where="c1")
 
 
+def _check_head_lists(res, gsets, nb, op, block, where):
+    """One head's block lists against the oracle's: VS rows exact outside the E1/E2 bands,
+    PE pairs exact outside the E4 band."""
+    PR.check_structure(gsets, nb, where=where)
+    if res.route == O.ROUTE_VS:
+        assert gsets == [sorted(set(s_)) for s_ in gsets]
+        diff = [qb for qb in range(nb) if set(gsets[qb]) != set(res.sets[qb])]
+        if diff:   # the direction sets may differ only inside the E1/E2 bands
+            ex_v = PR.vs_direction_exempt(res.p_v, op.alpha, op.k_min(block))[1]
+            ex_s = PR.vs_direction_exempt(res.p_s, op.alpha, op.k_min(block))[1]
+            for qb in diff:
+                for kb in set(gsets[qb]) ^ set(res.sets[qb]):
+                    assert kb in ex_v or (nb - 1 - (qb - kb)) in ex_s, f"{where}: row {qb} block {kb}"
+    else:
+        PR.compare_pe(gsets, res, op.gamma, where=where)
+
+
 @pytest.mark.parametrize("cid", [2, 3])
 def test_full_size_layer_in_bench_launch(cid):
     """The headline layers at full size (128k Llama, 512k Qwen-like), run as bench.py runs them
-    (crisp_prefill_attn over the whole layer with the prefill workspace), checked on one VS
-    and one PE head against the oracle: scores, route, block lists, and attention rows of
-    sampled query blocks."""
+    (crisp_prefill_attn over the whole layer with the prefill workspace): every head's scores,
+    route and block lists against the oracle (list invariants checked on the device too), and
+    the attention rows of sampled query blocks of a VS and a PE head."""
     C = _crisp()
     cfg = CONFIGS[cid]
     block, G = cfg.block, cfg.group
@@ -352,39 +369,50 @@ def test_full_size_layer_in_bench_launch(cid):
     ws = C.workspace(C.shape_of(q, k, block), DEV, prefill=True)
     o = torch.empty_like(q)
     C.crisp_prefill_attn(q, k, v, params, block, ws=ws, out=o)
-    o2, route, rp, ci = C.crisp_prefill_attn(q, k, v, params, block, return_lists=True)
+    o2, route_d, rp_d, ci_d = C.crisp_prefill_attn(q, k, v, params, block, return_lists=True)
     cs, pv, ps = C.crisp_estimate(q, k, params, block)
     torch.cuda.synchronize()
     assert torch.equal(o, o2)
-    route, rp, ci = route.cpu().numpy(), rp.cpu().numpy(), ci.cpu().numpy()
+    for h in range(cfg.n_q_heads):
+        _check_rows_on_gpu(rp_d[h], ci_d[h], nb, f"{cfg.name} h{h}")
+    route, rp = route_d.cpu().numpy(), rp_d.cpu().numpy()
     cs, pv, ps = cs.cpu().numpy(), pv.cpu().numpy(), ps.cpu().numpy()
     op = _oracle_params(params, block)
     hv = next(h for h in range(cfg.n_q_heads) if specs[h].kind == "concentrated")
     hp = next(h for h in range(cfg.n_q_heads) if specs[h].kind == "diffuse")
-    for h, qbs in ((hv, [0, nb // 2, nb - 1]), (hp, [1, nb // 8])):
+    full_lists = range(cfg.n_q_heads)
+    Kc, Vc = {}, {}
+    for h in range(cfg.n_q_heads):
+        g = h // G
+        if g not in Kc:
+            Kc = {g: to_f64(k[g])}
+            Vc = {g: to_f64(v[g])}
         w = f"{cfg.name} h{h} ({specs[h].kind})"
-        _say(f"  oracle for {w}")
-        Qh, Kh, Vh = to_f64(q[h]), to_f64(k[h // G]), to_f64(v[h // G])
-        res = O.crisp_head(Qh, Kh, None, block, op, attend=False)
+        Qh = to_f64(q[h])
+        if h in full_lists:
+            _say(f"  oracle for {w}")
+            res = O.crisp_head(Qh, Kc[g], None, block, op, attend=False)
+        else:
+            ahat = O.proxy_attention(Qh, Kc[g], block, op.scale(128))
+            res = O.HeadResult(route=0, c_struct=O.c_struct(ahat, cfg.seq_len, op.w_sink, op.w_local),
+                               p_v=None, p_s=None)
+            _, _, res.p_v, res.p_s = O.vs_scores(ahat, cfg.seq_len, block)
+            res.route = O.route(res.c_struct, op.tau_proxy)
+            del ahat
         PR.compare_scores(cs[h], pv[h], ps[h], res, where=w)
         assert route[h] == res.route, f"{w}: route gpu {route[h]} oracle {res.route}"
-        gsets = PR.csr_to_sets(rp, ci, h, nb)
-        PR.check_structure(gsets, nb, where=w)
-        _say(f"  selection and attention rows for {w}")
-        if res.route == O.ROUTE_VS:
-            assert gsets == [sorted(set(s_)) for s_ in gsets]
-            diff = [qb for qb in range(nb) if set(gsets[qb]) != set(res.sets[qb])]
-            if diff:   # the direction sets may differ only inside the E1/E2 bands
-                ex_v = PR.vs_direction_exempt(res.p_v, op.alpha, op.k_min(block))[1]
-                ex_s = PR.vs_direction_exempt(res.p_s, op.alpha, op.k_min(block))[1]
-                for qb in diff:
-                    for kb in set(gsets[qb]) ^ set(res.sets[qb]):
-                        assert kb in ex_v or (nb - 1 - (qb - kb)) in ex_s, f"{w}: row {qb} block {kb}"
-        else:
-            PR.compare_pe(gsets, res, op.gamma, where=w)
-        ref = O.sparse_attention(Qh, Kh, Vh, gsets, block, op.scale(128), qbs=qbs)
-        PR.compare_attention(to_f64(o[h]), ref, rows=PR.qb_rows(qbs, block, cfg.seq_len), where=w + " attn")
-        del Qh, Kh, Vh, res, gsets
+        if h in full_lists:
+            cih = ci_d[h, :int(rp[h, nb])].cpu().numpy()
+            gsets = [cih[rp[h, qb]:rp[h, qb + 1]].tolist() for qb in range(nb)]
+            _check_head_lists(res, gsets, nb, op, block, w)
+            if h in (hv, hp):
+                qbs = [0, nb // 2, nb - 1] if h == hv else [1, nb // 8]
+                _say(f"  attention rows for {w}")
+                ref = O.sparse_attention(Qh, Kc[g], Vc[g], gsets, block, op.scale(128), qbs=qbs)
+                PR.compare_attention(to_f64(o[h]), ref, rows=PR.qb_rows(qbs, block, cfg.seq_len), where=w + " attn")
+                del ref
+            del gsets
+        del Qh, res
 
 
 @pytest.mark.parametrize("block", [64, 128])
