@@ -551,6 +551,17 @@ def test_flexprefill_ragged_and_gamma(n, block, hq, hkv, gamma):
     _check_layer(C, cfg, C.flexprefill_params(gamma=gamma), where=f"fp n{n}")
 
 
+def test_flexprefill_full_size_128k():
+    """The comparator (App. A) at the headline 128k layer: every head's D_JS, route (E5),
+    gamma VS masks (E6, and bit-exact on the GPU's own scores) or PE pairs (E4), and the
+    attention rows of each head's last query block."""
+    C = _crisp()
+    _say("FlexPrefill comparator at 128k, every head")
+    cfg = CONFIGS[2]
+    _check_layer(C, cfg, C.flexprefill_params(alpha=cfg.alpha), qbs_per_head=lambda h, nb: [nb - 1],
+                 where="fp128k")
+
+
 def test_flexprefill_config1_sampled():
     C = _crisp()
     _say("FlexPrefill mode, config 1 (32k), 8 heads, sampled query blocks")
