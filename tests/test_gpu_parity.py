@@ -15,6 +15,7 @@ from oracle import crisp_oracle as O
 from tests import parity as PR
 from tests.helpers import to_f64
 from workloads import CONFIGS, custom_config, make_layer, stress_config
+from workloads.synth import structured_pe_config
 
 pytestmark = pytest.mark.gpu
 
@@ -549,6 +550,17 @@ def test_flexprefill_ragged_and_gamma(n, block, hq, hkv, gamma):
     _say(f"FlexPrefill mode n={n} B={block} hq={hq} hkv={hkv} gamma={gamma}")
     cfg = custom_config(n, hq, hkv, block=block, config_id=150 + n % 89)
     _check_layer(C, cfg, C.flexprefill_params(gamma=gamma), where=f"fp n{n}")
+
+
+@pytest.mark.parametrize("seq_len", [65536])
+def test_structured_pe_workload(seq_len):
+    """The paper-like workload of the length sweep (structured PE heads whose pooled scores
+    concentrate, Llama GQA shape): every head's scores, route and lists against the oracle,
+    and the attention rows of two query blocks per head."""
+    C = _crisp()
+    cfg = structured_pe_config(seq_len)
+    _say(f"structured-PE workload {cfg.name}, every head")
+    _check_layer(C, cfg, C.make_params(), qbs_per_head=lambda h, nb: [nb // 3, nb - 1], where=cfg.name)
 
 
 def test_flexprefill_full_size_128k():
