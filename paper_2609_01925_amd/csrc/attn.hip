@@ -254,19 +254,24 @@ __device__ __forceinline__ bf16x4 lds_ld_tr(int addr) {
 __device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
 
 // S^T for one tile: s[h][mb] holds keys 32 mb + (C-layout row) against the 32
-// queries of half h (lane column).  qk_sub computes sub-block MB for every half;
-// rows 32..63 have the same swizzle as rows 0..31, so sub-block 1 is +32 rows,
-// and each K operand read serves every half.
-template <int QH, int NMB, int MB>
-__device__ __forceinline__ void qk_sub(int kbuf, const bf16x8 (&qf)[QH][8], const Offsets& off, f32x16 (&s)[QH][NMB]) {
+// queries of half h (lane column).  Rows 32..63 have the same swizzle as rows
+// 0..31, so sub-block mb is +32 mb rows, and each K operand read serves every
+// half.  The sub-blocks' accumulation chains are interleaved step by step (each
+// chain still sums in kk order), so consecutive MFMAs are independent.
+template <int QH, int NMB>
+__device__ __forceinline__ void qk_tile(int kbuf, const bf16x8 (&qf)[QH][8], const Offsets& off, f32x16 (&s)[QH][NMB]) {
 #pragma unroll
-  for (int h = 0; h < QH; ++h) s[h][MB] = zero16();
+  for (int h = 0; h < QH; ++h)
 #pragma unroll
-  for (int kk = 0; kk < 8; ++kk) {
-    const bf16x8 ak = lds_ld16(kbuf + 32 * 256 * MB + off.k[kk]);
+    for (int mb = 0; mb < NMB; ++mb) s[h][mb] = zero16();
 #pragma unroll
-    for (int h = 0; h < QH; ++h) s[h][MB] = mfma32(ak, qf[h][kk], s[h][MB]);
-  }
+  for (int kk = 0; kk < 8; ++kk)
+#pragma unroll
+    for (int mb = 0; mb < NMB; ++mb) {
+      const bf16x8 ak = lds_ld16(kbuf + 32 * 256 * mb + off.k[kk]);
+#pragma unroll
+      for (int h = 0; h < QH; ++h) s[h][mb] = mfma32(ak, qf[h][kk], s[h][mb]);
+    }
 }
 
 // Sets masked scores to -inf: keys after the lane's query (causal, which also
@@ -304,9 +309,11 @@ __device__ __forceinline__ void exp_sub(const f32x16& s, float c, float mc, bf16
     }
 }
 
-// l + the lane's sum of the tile's (bf16) probabilities.
+// The lane's sum of the tile's (bf16) probabilities, in two partial sums (the
+// halves hh of each sub-block) so that the dot2 chain is half as long.
 template <int NMB>
-__device__ __forceinline__ float sum_tile(const bf16x8 (&pb)[NMB][2], float l) {
+__device__ __forceinline__ float sum_tile(const bf16x8 (&pb)[NMB][2]) {
+  float part[2] = {0.f, 0.f};
 #pragma unroll
   for (int mb = 0; mb < NMB; ++mb)
 #pragma unroll
@@ -316,9 +323,9 @@ __device__ __forceinline__ float sum_tile(const bf16x8 (&pb)[NMB][2], float l) {
         bf16x2 pr;
         pr[0] = pb[mb][hh][e];
         pr[1] = pb[mb][hh][e + 1];
-        l = dot2_bf16_sum(pr, l);
+        part[hh] = dot2_bf16_sum(pr, part[hh]);
       }
-  return l;
+  return part[0] + part[1];
 }
 
 // O^T[h] (128 d x 32 queries) += V^T P^T[h] for one tile; each V^T operand (two
@@ -471,7 +478,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
         const float mc = m_run[h] == -__builtin_inff() ? 0.f : m_run[h] * a.c;
 #pragma unroll
         for (int mb = 0; mb < NMB; ++mb) exp_sub(s[h][mb], a.c, mc, pn[h][mb]);
-        ts[h] = sum_tile<NMB>(pn[h], 0.f);
+        ts[h] = sum_tile<NMB>(pn[h]);
         grow = grow || !(ts[h] <= kSumLimit) || m_run[h] == -__builtin_inff();
       }
       if (!decltype(first)::value) pv_tile<QH, NMB>(vst(1 - P), off, pp, o);
@@ -501,7 +508,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
           const float mcn = m_new == -__builtin_inff() ? 0.f : m_new * a.c;
 #pragma unroll
           for (int mb = 0; mb < NMB; ++mb) exp_sub(s[h][mb], a.c, mcn, pn[h][mb]);
-          ts[h] = sum_tile<NMB>(pn[h], 0.f);
+          ts[h] = sum_tile<NMB>(pn[h]);
         }
       }
 #pragma unroll
@@ -510,8 +517,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
       // targets; those scores are never used.  The scheduler interleaves the
       // K operand reads with the MFMAs in its LDS/MFMA pipelining mode.
       __builtin_amdgcn_iglp_opt(0);
-      qk_sub<QH, NMB, 0>(kst(1 - P), qf, off, s);
-      if constexpr (NMB > 1) qk_sub<QH, NMB, 1>(kst(1 - P), qf, off, s);
+      qk_tile<QH, NMB>(kst(1 - P), qf, off, s);
       if (!DENSE && (((j + 1) / TPB) >> 6) != chunk0) {  // tile j+1 starts the next chunk
         ++chunk0;
         if ((chunk0 + 1) & 1)
@@ -528,8 +534,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
     if (T > 1) fetch_tile<NW, BK>(fe, rk, kst(1), key0_of(1), w);
     wait_dma();
     __syncthreads();
-    qk_sub<QH, NMB, 0>(kst(0), qf, off, s);
-    if constexpr (NMB > 1) qk_sub<QH, NMB, 1>(kst(0), qf, off, s);
+    qk_tile<QH, NMB>(kst(0), qf, off, s);
     // two P buffers with fixed registers: steps alternate between them, and the
     // parity of every step is known where it is expanded
     bf16x8 pa[QH][NMB][2], pz[QH][NMB][2];
