@@ -12,11 +12,13 @@ Stage -> pins:
   route (Alg. 2)                  P4 flat head routes PE; sink head routes VS; tie rule
   a_v / a_s / p (Alg. 3)          P5 closed form for p_v, brute-force diagonal walk for a_s, P8 identities
   floor and top-k (Alg. 3, Sec. 4.3)  P5 exact set, P6 exact sets at alpha 0.5 / 2, P7 metamorphic
-  PE scores and cutoff (Alg. 4)   P4 closed-form A_tilde and K*, brute-force cutoff, P7 gamma monotone
+  PE scores and cutoff (Alg. 4)   P4 closed-form A_tilde and K*, P12 loop-by-loop pooled scores,
+                                  brute-force cutoff, P7 gamma monotone
   block sets                      P9 structure, slash geometry walk
   sparse attention (Eq. 1)        P1 all blocks == dense SDPA, P2 explicit-mask softmax
   JSD pattern search (App. A)     P10 closed forms and scipy for D_JS, closed-form pooled estimate
-                                  (flat and sink heads), routes by visible-key counting
+                                  (flat and sink heads), loop-by-loop pooled estimate, routes by
+                                  visible-key counting
   gamma VS selection (App. A)     P10 explicit cases, brute-force minimal subsets, mass-cliff count
   median noise floor (App. H)     P11 odd/even closed forms, clumpy-noise case, brute-force median
 """
@@ -627,3 +629,67 @@ def test_p11_median_floor_brute_force():
             assert float(mu) == float((np.float32(lo) + np.float32(hi)) * np.float32(0.5))
         S = O.vs_select(p, 1.0, 0, "median")
         assert S == sorted(J for J in range(nb) if p[J] > mu) or len(S) == 0 and not (p > mu).any()
+
+
+def _pooled_scores_brute(q, k, block, scale):
+    """Alg. 4 written out with loops: block means (a partial last block averaged over the rows
+    it has), dot products, a row softmax over kb <= qb, then division by the total."""
+    n, d = len(q), len(q[0])
+    nb = -(-n // block)
+    def mean_rows(x, J):
+        rows = range(J * block, min((J + 1) * block, n))
+        return [sum(x[i][c] for i in rows) / len(rows) for c in range(d)]
+    qbar = [mean_rows(q, J) for J in range(nb)]
+    kbar = [mean_rows(k, J) for J in range(nb)]
+    abar = [[0.0] * nb for _ in range(nb)]
+    for a in range(nb):
+        logits = [scale * sum(qbar[a][c] * kbar[b][c] for c in range(d)) for b in range(a + 1)]
+        m = max(logits)
+        e = [math.exp(x - m) for x in logits]
+        z = sum(e)
+        for b in range(a + 1):
+            abar[a][b] = e[b] / z
+    total = sum(sum(r) for r in abar)
+    return [[x / total for x in r] for r in abar]
+
+
+@pytest.mark.parametrize("n,block,d,seed", [(18, 4, 6, 41), (32, 8, 5, 42), (9, 3, 7, 43)])
+def test_p12_pooled_scores_brute_force(n, block, d, seed):
+    """P12: pooled PE scores (Alg. 4) against the loop-by-loop statement, on random Q != K (so a
+    swapped or transposed product, a wrong scale, sum pooling or a column softmax all fail)."""
+    rng = np.random.default_rng(seed)
+    q = bf16_round(rng.standard_normal((n, d)) * 2.0)
+    k = bf16_round(rng.standard_normal((n, d)) * 2.0 + 0.5)
+    scale = 0.7
+    At = O.pe_scores(q, k, block, scale)
+    want = np.array(_pooled_scores_brute(q.tolist(), k.tolist(), block, scale))
+    assert np.allclose(At, want, rtol=1e-12, atol=1e-15)
+    # the mistakes above do change the result on these inputs
+    assert not np.allclose(O.pe_scores(k, q, block, scale), want, rtol=1e-6, atol=1e-9)
+    assert not np.allclose(O.pe_scores(q, k, block, 2 * scale), want, rtol=1e-6, atol=1e-9)
+
+
+@pytest.mark.parametrize("n,block,d,seed", [(18, 4, 6, 44), (30, 8, 5, 45), (5, 8, 4, 46)])
+def test_p10_pooled_estimate_brute_force(n, block, d, seed):
+    """The pattern search's pooled estimate (App. A) against the loop-by-loop statement on
+    random Q != K: the mean of the last b = min(B, n) query rows against each key block's mean
+    (a partial last block over its own rows), scaled, softmax over the blocks."""
+    rng = np.random.default_rng(seed)
+    q = bf16_round(rng.standard_normal((n, d)) * 2.0)
+    k = bf16_round(rng.standard_normal((n, d)) * 2.0 - 0.3)
+    scale = 0.6
+    b = min(block, n)
+    qp = [sum(q[i][c] for i in range(n - b, n)) / b for c in range(d)]
+    nb = -(-n // block)
+    z = []
+    for J in range(nb):
+        rows = range(J * block, min((J + 1) * block, n))
+        kb = [sum(k[i][c] for i in rows) / len(rows) for c in range(d)]
+        z.append(scale * sum(qp[c] * kb[c] for c in range(d)))
+    e = [math.exp(x - max(z)) for x in z]
+    want = np.array([x / sum(e) for x in e])
+    got = O.pooled_estimate(q, k, block, scale)
+    assert np.allclose(got, want, rtol=1e-12, atol=1e-15)
+    if n > b:   # pooling the first b rows instead of the last would differ
+        qf = [sum(q[i][c] for i in range(b)) / b for c in range(d)]
+        assert not np.allclose(qf, qp)
