@@ -67,6 +67,7 @@ struct SelArgs {
 };
 
 constexpr int kRadixBins = 2048;
+constexpr int64_t kSmallCap = 32768;  // causal pairs per head up to which one workgroup finds the PE cutoff
 constexpr double kFix = 1152921504606846976.0;  // 2^60
 
 __device__ __forceinline__ uint32_t fbits(float x) {
@@ -628,6 +629,62 @@ __global__ __launch_bounds__(256) void sel_radix_scan(SelArgs a, int pass) {
   for (int i = tid; i < kRadixBins; i += 256) H[i] = 0ull;
 }
 
+// PE cutoff of a small layer (at most kSmallCap causal pairs per head) in one
+// workgroup per head: the three digit passes of sel_radix_hist / sel_radix_scan
+// with the histograms in LDS.  The masses are the same fixed-point integers, so
+// t*, the remaining mass and the count of pairs equal to t* are the same; one
+// launch replaces seven.  grid hq, 1024 threads.
+__global__ __launch_bounds__(1024) void sel_radix_small(SelArgs a) {
+  __shared__ unsigned long long bins[kRadixBins];
+  __shared__ RState sst;
+  const int h = blockIdx.x, tid = threadIdx.x;
+  if (a.route[h] != 1) return;
+  if (tid == 0) {
+    sst.prefix = 0;
+    sst.all = 0;
+    sst.need = (unsigned long long)ceil((double)a.gamma * kFix);
+    if (sst.need == 0) sst.need = 1;
+    sst.ceq = 0;
+    sst.pad = 0;
+  }
+  const float* At = a.atil + (size_t)h * a.cap;
+  for (int pass = 0; pass < 3; ++pass) {
+    int shift, nbits;
+    radix_digit(pass, shift, nbits);
+    const int nbins = 1 << nbits;
+    for (int i = tid; i < nbins; i += 1024) bins[i] = 0ull;
+    __syncthreads();  // bins cleared; sst of the previous pass visible
+    if (sst.all) break;
+    const int hi = shift + nbits;
+    const uint64_t want = (uint64_t)sst.prefix >> hi;
+    const uint32_t dmask = (uint32_t)nbins - 1u;
+    for (int64_t i = tid; i < a.cap; i += 1024) {
+      const uint32_t b = fbits(At[i]);
+      if (((uint64_t)b >> hi) == want) atomicAdd(&bins[(b >> shift) & dmask], fixed_mass(b));
+    }
+    __syncthreads();
+    if (tid < 64) {
+      unsigned long long cum = 0;
+      const int bin = wave_descend_find<unsigned long long>(bins, nbins, sst.need, &cum);
+      if (tid == 0) {
+        if (bin < 0) {
+          sst.all = 1;  // total mass below gamma: keep every pair
+          sst.ceq = ~0ull;
+        } else {
+          sst.need -= cum;
+          sst.prefix |= (uint32_t)bin << shift;
+          if (pass == 2) {
+            const unsigned long long ft = fixed_mass(sst.prefix);
+            sst.ceq = ft ? (sst.need + ft - 1) / ft : ~0ull;
+          }
+        }
+      }
+    }
+    __syncthreads();  // the search is done with the bins before the next pass clears them
+  }
+  if (tid == 0) a.rstate[h] = sst;
+}
+
 // Per-row counts.  VS: x = row size.  PE: x = #(> t*), y = #(== t*), z = flags
 // (1: block 0 > t*, 2: block 0 == t*, 4: block qb > t*, 8: block qb == t*).
 // grid (ceil(nb / 4), hq), 256 threads, one wave per row.
@@ -841,13 +898,17 @@ hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, flo
   const int nt = (nb + 63) / 64;
   hipLaunchKernelGGL(sel_pe_logits, dim3(nt * (nt + 1) / 2, d.hq), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(sel_pe_softmax, dim3(nb, d.hq), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(sel_radix_init, dim3(d.hq), dim3(256), 0, stream, a);
-  int64_t chunks = (d.cap + 16383) / 16384;
-  if (chunks > 1024) chunks = 1024;
-  if (chunks < 1) chunks = 1;
-  for (int pass = 0; pass < 3; ++pass) {
-    hipLaunchKernelGGL(sel_radix_hist, dim3((unsigned)chunks, d.hq), dim3(256), 0, stream, a, pass);
-    hipLaunchKernelGGL(sel_radix_scan, dim3(d.hq), dim3(256), 0, stream, a, pass);
+  if (d.cap <= kSmallCap) {
+    hipLaunchKernelGGL(sel_radix_small, dim3(d.hq), dim3(1024), 0, stream, a);
+  } else {
+    hipLaunchKernelGGL(sel_radix_init, dim3(d.hq), dim3(256), 0, stream, a);
+    int64_t chunks = (d.cap + 16383) / 16384;
+    if (chunks > 1024) chunks = 1024;
+    if (chunks < 1) chunks = 1;
+    for (int pass = 0; pass < 3; ++pass) {
+      hipLaunchKernelGGL(sel_radix_hist, dim3((unsigned)chunks, d.hq), dim3(256), 0, stream, a, pass);
+      hipLaunchKernelGGL(sel_radix_scan, dim3(d.hq), dim3(256), 0, stream, a, pass);
+    }
   }
   const int rows_grid = (nb + 3) / 4;
   hipLaunchKernelGGL(sel_csr_count, dim3(rows_grid, d.hq), dim3(256), 0, stream, a);
