@@ -764,16 +764,29 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
     loc[i] = sum;
     sum += hist[tid * per + i];
   }
-  part[tid] = sum;
-  __syncthreads();
-  for (int o = 1; o < 1024; o <<= 1) {
-    const int x = tid >= o ? part[tid - o] : 0;
-    __syncthreads();
-    part[tid] += x;
-    __syncthreads();
+  // inclusive scan of the per-thread sums: within each wave by shuffles, then the
+  // 16 wave totals by one wave
+  int incl = sum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(incl, o, 64);
+    if ((tid & 63) >= o) incl += y;
   }
-  const int base = part[tid] - sum;
-  const int n_items = part[1023];
+  if ((tid & 63) == 63) part[tid >> 6] = incl;
+  __syncthreads();
+  if (tid < 64) {
+    int wt = tid < 16 ? part[tid] : 0;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      const int y = __shfl_up(wt, o, 64);
+      if (tid >= o) wt += y;
+    }
+    if (tid < 16) part[16 + tid] = wt;  // inclusive wave totals
+  }
+  __syncthreads();
+  incl += (tid >> 6) ? part[16 + (tid >> 6) - 1] : 0;
+  const int base = incl - sum;
+  const int n_items = part[16 + 15];
 #pragma unroll
   for (int i = 0; i < per; ++i) hist[tid * per + i] = base + loc[i];
   __syncthreads();
