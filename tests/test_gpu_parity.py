@@ -318,6 +318,17 @@ def test_ragged_and_small_layers(n, block, hq, hkv):
     _check_layer(C, cfg, C.make_params(), where=f"n{n}")
 
 
+@pytest.mark.parametrize("n,hq,hkv,block", [(4000, 12, 3, 128), (3000, 10, 5, 64), (2500, 32, 16, 128)])
+def test_unusual_gqa_groupings(n, hq, hkv, block):
+    """KV-group counts that do not divide 8 (the sparse kernel's queues then leave some XCDs
+    without a home queue; they take work from the others) and more groups than XCDs (several
+    groups per queue), through the whole path against the oracle."""
+    C = _crisp()
+    _say(f"GQA grouping n={n} hq={hq} hkv={hkv} B={block}")
+    cfg = custom_config(n, hq, hkv, block=block, config_id=150 + hkv)
+    _check_layer(C, cfg, C.make_params(), qbs_per_head=lambda h, nb: [0, nb // 2, nb - 1], where=f"gqa{hq}x{hkv}")
+
+
 @pytest.mark.parametrize("tau", [0.0, 1.5])
 def test_forced_routes_and_params(tau):
     C = _crisp()
