@@ -48,8 +48,11 @@ def _oracle_params(p, block):
 # ------------------------------------------------------------------ attention kernel
 
 @pytest.mark.parametrize("n,block,hq,hkv", [(4096, 128, 2, 1), (1000, 128, 4, 2), (200, 64, 2, 2), (64, 128, 1, 1),
-                                            (1, 128, 1, 1), (4160, 64, 8, 8), (2048, 128, 16, 4)])
+                                            (1, 128, 1, 1), (4160, 64, 8, 8), (2048, 128, 16, 4),
+                                            (1500, 128, 6, 3), (1000, 64, 12, 12)])
 def test_dense_attention_matches_oracle(n, block, hq, hkv):
+    """Every workgroup-to-unit mapping of the fixed grid: KV-group counts dividing 8, multiples
+    of 8, and neither (3, 12)."""
     C = _crisp()
     _say(f"dense n={n} B={block} hq={hq} hkv={hkv}")
     q, k, v = _rand(hq, n, seed=1), _rand(hkv, n, seed=2), _rand(hkv, n, seed=3)
