@@ -774,3 +774,48 @@ def test_prefill_in_a_hip_graph(n, block):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(o, o_eager), f"replay {rep} differs from the eager result"
+
+
+# ------------------------------------------------------------------ stored values
+
+def test_golden_manifests_on_gpu():
+    """The GPU path against values stored in tests/golden/manifests.json (written by the
+    oracle-only script beside it): routes exact, C_struct to the stage tolerance, the
+    selection's pair count to 0.1% of the causal pairs (ties at the floor or the gamma cutoff
+    may fall either way), and for the layer whose attention is stored, the output's mean and
+    largest magnitude to the attention tolerances.  The stored values come from inputs
+    drawn by the generator on the CPU (its stream differs by device), so the same heads are
+    drawn on the CPU here and copied to the GPU; the other heads of each layer stay zero."""
+    import json
+    import os
+    from workloads import GEN_VERSION
+    C = _crisp()
+    with open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "manifests.json")) as f:
+        golden = json.load(f)
+    layers = {"tiny-4k": CONFIGS[0], "llama3-8b-32k-heads0-3": CONFIGS[1],
+              "stress-64k-a1-b128-adversarial": stress_config(1.0, 128)}
+    assert sorted(layers) == sorted(golden)
+    for name, cfg in layers.items():
+        rec = golden[name]
+        assert rec["generator"] == GEN_VERSION and rec["layer"] == cfg.name and rec["seq_len"] == cfg.seq_len
+        _say(f"golden manifest {name}")
+        heads = [int(h) for h in rec["heads"]]
+        q, k, v, _ = (t.to(DEV) if torch.is_tensor(t) else t for t in make_layer(cfg, heads=heads))
+        params = C.make_params(alpha=cfg.alpha)
+        cs, pv, ps, route, rp, ci, dm = _run_stages(C, q, k, v, params, cfg.block)
+        nb = O.n_blocks(cfg.seq_len, cfg.block)
+        attend = any("out_mean" in r for r in rec["heads"].values())
+        o = C.crisp_prefill_attn(q, k, v, params, cfg.block) if attend else None
+        torch.cuda.synchronize()
+        for hs, st in rec["heads"].items():
+            h = int(hs)
+            w = f"{name} h{h}"
+            assert (route[h] == O.ROUTE_VS) == (st["route"] == "VS"), f"{w}: route {route[h]} vs {st['route']}"
+            assert abs(float(cs[h]) - st["c_struct"]) <= PR.CS_ABS, f"{w}: C_struct {float(cs[h])} vs {st['c_struct']}"
+            pairs = sum(len(s) for s in PR.csr_to_sets(rp, ci, h, nb))
+            assert abs(pairs - st["pairs"]) <= 1e-3 * nb * (nb + 1) / 2, f"{w}: pairs {pairs} vs {st['pairs']}"
+            if attend:
+                og = to_f64(o[h])
+                assert abs(og.mean() - st["out_mean"]) <= 2e-3, f"{w}: output mean {og.mean()} vs {st['out_mean']}"
+                assert abs(np.abs(og).max() - st["out_max_abs"]) <= 2e-2, f"{w}: max |O| {np.abs(og).max()}"
+        del q, k, v, o
