@@ -122,11 +122,11 @@ def layer_measure(cfg, steps, warmup, label):
         f"dense {dense['median']:.3f} ms")
 
     d = 128
-    # algorithmic HBM bytes: the estimator reads each KV head's K twice (two passes); the
+    # algorithmic HBM bytes: the estimator reads each KV head's K once (one pass); the
     # selection pools Q of the PE heads and K of their groups, writes the pooled scores
     # A~ once, then reads/writes them in the softmax, reads them in the three radix passes
     # and the two CSR passes (32 bytes per causal pair per PE head), and writes the lists
-    est_gbs = 2.0 * cfg.n_kv_heads * cfg.seq_len * d * 2 / (est["median"] * 1e-3) / 1e9
+    est_gbs = cfg.n_kv_heads * cfg.seq_len * d * 2.0 / (est["median"] * 1e-3) / 1e9
     pe_heads = [h for h in range(cfg.n_q_heads) if int(route_c[h]) == 1]
     pe_groups = len({h // cfg.group for h in pe_heads})
     sel_bytes = ((len(pe_heads) + pe_groups) * cfg.seq_len * d * 2.0 + 32.0 * nb * (nb + 1) / 2 * len(pe_heads)
@@ -151,6 +151,10 @@ def layer_measure(cfg, steps, warmup, label):
         "dense_mfma_frac": dense_flop_exec / (dense["median"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
         "effective_tflops_dense_equiv": dense_useful / (crisp["median"] * 1e-3) / 1e12,
         "estimate_hbm_gbs": est_gbs, "estimate_hbm_frac": est_gbs / HBM_PEAK_GBS,
+        # the estimator's proxy scores on MFMA: 2 b n d FLOP per query head (b = block)
+        "estimate_tflops": 2.0 * cfg.n_q_heads * block * cfg.seq_len * d / (est["median"] * 1e-3) / 1e12,
+        "estimate_mfma_frac": 2.0 * cfg.n_q_heads * block * cfg.seq_len * d / (est["median"] * 1e-3) / 1e12
+        / MFMA_BF16_PEAK_TFLOPS,
         "select_hbm_gbs": sel_gbs, "select_hbm_frac": sel_gbs / HBM_PEAK_GBS,
     }
     res["_attn_launch_ms"] = att["median"]

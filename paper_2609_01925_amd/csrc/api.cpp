@@ -110,9 +110,9 @@ WsLayout ws_layout(const Dims& d) {
     return at;
   };
   const size_t hq = d.hq, hkv = d.hkv, nb = d.nb;
-  L.rowstat = take(hq * sp.splits * 128 * 2 * sizeof(float));
-  L.rowfinal = take(hq * 128 * 2 * sizeof(float));
-  L.parts = take(hq * nb * 4 * sizeof(float));
+  L.rowstat = take(hq * sp.splits * 128 * 4 * sizeof(float));
+  L.rowfinal = take(hq * 128 * sizeof(float));
+  L.parts = take(hq * nb * 128 * 4 * sizeof(float));
   L.masks = take(hq * 2 * nb);
   L.qbar = take(hq * nb * kHeadDim * sizeof(float));
   L.kbar = take(hkv * nb * kHeadDim * sizeof(float));

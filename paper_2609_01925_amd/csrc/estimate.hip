@@ -1,18 +1,19 @@
 // Stages 1-2: the last-block proxy attention and its reductions (Alg. 2, the
 // C_struct equation of Sec. 3.2, and the vertical / slash scores of Alg. 3).
 //
-// The proxy A_hat (b rows x n keys per head) is never materialised.  Keys are
-// split into ranges of whole blocks, one workgroup per (head, range):
-//   pass 1  S^T = K Q_hat^T on MFMA, causal mask, per-row running max / sum-exp
-//   combine per-row (max, sum) over ranges
-//   pass 2  recompute S^T, P = exp(S - max) / sum, and reduce per key block J:
-//             column mass      sum over rows and keys of J             -> p_v[J]
-//             diagonal mass    split by the slash block of the diagonal
-//                              through (last row, key + b - 1 - r):
-//                              J itself or J + 1                      -> p_s
-//             anchor mass      keys in [0, w_sink) or [n - w_local, n) -> C_struct
-//   finalize p_v, p_s, C_struct (deterministic: every partial is written once
-//            and summed in a fixed order; no floating-point atomics)
+// The proxy A_hat (b rows x n keys per head) is never materialised, and K is read
+// once.  Keys are split into ranges of whole blocks, one workgroup per (head, range):
+//   pass     S^T = K Q_hat^T on MFMA, causal mask, and per proxy row a running max
+//            with, under it, sums of exp2((s - max) c): over all keys, over the
+//            anchor keys ([0, w_sink) and [n - w_local, n)), and per key block J
+//            split by the slash block of the diagonal through (last row,
+//            key + b - 1 - r): J itself (lo) or J + 1 (hi).  Per (row, J) the pair
+//            (lo, hi) is stored with the max it was summed under.
+//   combine  per row: max M and sum L over ranges; C_struct = (1/b) sum_r anchor / L
+//   scale    p_v[J] = (1/b) sum_r (lo + hi) 2^((m - M) c) / L,
+//            p_s[J] = (1/b) sum_r (lo[J] + hi[J - 1]) scaled alike
+// Deterministic: every partial is written once and summed in a fixed order; no
+// floating-point atomics.
 #include "crisp_device.h"
 #include "crisp_internal.h"
 
@@ -30,9 +31,9 @@ struct EstArgs {
   int n, nb, B, b, hq, G, bps, splits;
   float c;  // softmax scale * log2(e)
   int w_sink, w_local;
-  float* rowstat;   // [hq][splits][128][2]  (max of raw scores, sum of exp2)
-  float* rowfinal;  // [hq][128][2]
-  float4* parts;    // [hq][nb]  (column, diagonal-low, diagonal-high, anchor)
+  float4* rowstat;  // [hq][splits][128]  (max of raw scores, sum of exp2, anchor sum, -)
+  float* rowfinal;  // [hq][128]  M c + log2 L per proxy row (+inf past b)
+  float4* parts;    // [hq][nb][128]  (diagonal-low, diagonal-high, max they were summed under, -)
   float* c_struct;
   float* p_v;
   float* p_s;
@@ -83,102 +84,15 @@ __device__ __forceinline__ int key_of(int key0, int mb, int i, int l) {
   return key0 + 32 * mb + 8 * (i >> 2) + 4 * (l >> 5) + (i & 3);
 }
 
-// Pass 1: per (head, key range) running max and sum of exp2((s - max) * c) per proxy row.
-__global__ __launch_bounds__(NT) void est_rowstats(EstArgs a) {
+// One pass over K: scores, causal mask, per-row running max, and under that running
+// max the row's sums of exp2((s - max) c): over all its keys (l), over the anchor
+// keys (anchor mass), and per key block J split by slash block (lo: keys whose
+// diagonal through the last proxy row stays in J, hi: those moving to J + 1).  When
+// the running max rises, the sums still open are scaled down to the new max; a
+// block's (lo, hi) is written with the max it was summed under when the block ends,
+// and the range's (max, l, anchor) when the range ends.
+__global__ __launch_bounds__(NT) void est_pass(EstArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[2 * kTileBytes];
-  const int h = blockIdx.x / a.splits, sp = blockIdx.x % a.splits;
-  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-  const int r = 32 * w + (l & 31);
-  const int qi = a.n - a.b + r;
-  bf16x8 qf[8];
-  load_q_hat(a, h, r, l, qf);
-  const uint16_t* Kg = a.k + (size_t)(h / a.G) * a.n * kHeadDim;
-  const int key_lo = sp * a.bps * a.B;
-  int key_hi = key_lo + a.bps * a.B;
-  key_hi = key_hi < a.n ? key_hi : a.n;
-  float m_run = -__builtin_inff(), l_run = 0.f;
-  int buf = 0;
-  u32x4 pre[4];
-  if (key_lo < key_hi) load_k_regs(pre, Kg, key_lo, a.n, tid);
-  for (int key0 = key_lo; key0 < key_hi; key0 += BK, buf ^= 1) {
-    char* kb = smem + buf * kTileBytes;
-    store_k_regs(kb, pre, tid);
-    if (key0 + BK < key_hi) load_k_regs(pre, Kg, key0 + BK, a.n, tid);
-    __syncthreads();
-    f32x16 s[2];
-    scores(kb, qf, l, s);
-    float mx = -__builtin_inff();
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        if (r >= a.b || key_of(key0, mb, i, l) > qi) s[mb][i] = -__builtin_inff();
-        mx = fmaxf(mx, s[mb][i]);
-      }
-    mx = fmaxf(mx, swap_halves(mx));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = m_new == -__builtin_inff() ? 0.f : m_new;
-    float ps = 0.f;
-#pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) ps += fast_exp2((s[mb][i] - m_use) * a.c);
-    l_run = l_run * fast_exp2((m_run - m_use) * a.c) + ps;
-    m_run = m_new;
-  }
-  l_run += swap_halves(l_run);
-  if (l < 32 && r < a.b) {
-    float* dst = a.rowstat + (((size_t)h * a.splits + sp) * 128 + r) * 2;
-    dst[0] = m_run;
-    dst[1] = l_run;
-  }
-}
-
-// Combine the per-range row statistics: eight lanes per proxy row, each taking every
-// eighth range, then a max and a sum over the eight (fixed order).  grid (hq, 4),
-// 256 threads = 32 rows x 8 lanes.
-__global__ __launch_bounds__(256) void est_combine(EstArgs a) {
-  const int h = blockIdx.x, j = threadIdx.x & 7;
-  const int r = 32 * blockIdx.y + (threadIdx.x >> 3);
-  const float2* src = reinterpret_cast<const float2*>(a.rowstat) + (size_t)h * a.splits * 128 + r;
-  float M = -__builtin_inff();
-  for (int sp = j; sp < a.splits; sp += 8) M = fmaxf(M, src[(size_t)sp * 128].x);
-#pragma unroll
-  for (int o = 1; o < 8; o <<= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
-  float L = 0.f;
-  for (int sp = j; sp < a.splits; sp += 8) {
-    const float2 ml = src[(size_t)sp * 128];
-    if (ml.x != -__builtin_inff()) L += ml.y * fast_exp2((ml.x - M) * a.c);
-  }
-#pragma unroll
-  for (int o = 1; o < 8; o <<= 1) L += __shfl_xor(L, o, 64);
-  if (j == 0 && r < a.b) {
-    a.rowfinal[((size_t)h * 128 + r) * 2] = M;
-    a.rowfinal[((size_t)h * 128 + r) * 2 + 1] = L;
-  }
-}
-
-__device__ __forceinline__ void block_reduce4(float4 v, float4* red, int tid, float4* out) {
-  v.x = wave_sum(v.x);
-  v.y = wave_sum(v.y);
-  v.z = wave_sum(v.z);
-  v.w = wave_sum(v.w);
-  if ((tid & 63) == 0) red[tid >> 6] = v;
-  __syncthreads();
-  if (tid == 0) {
-    float4 t = red[0];
-    for (int i = 1; i < NT / 64; ++i) {
-      t.x += red[i].x; t.y += red[i].y; t.z += red[i].z; t.w += red[i].w;
-    }
-    *out = t;
-  }
-  __syncthreads();
-}
-
-// Pass 2: normalised proxy entries reduced per key block.
-__global__ __launch_bounds__(NT) void est_reduce(EstArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * kTileBytes];
-  __shared__ float4 red[NT / 64];
   const int h = blockIdx.x / a.splits, sp = blockIdx.x % a.splits;
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
   const int r = 32 * w + (l & 31);
@@ -186,19 +100,16 @@ __global__ __launch_bounds__(NT) void est_reduce(EstArgs a) {
   const bool row_ok = r < a.b;
   bf16x8 qf[8];
   load_q_hat(a, h, r, l, qf);
-  // A_hat = 2^(s c - M c) / L = 2^(s c - mcl) with mcl = M c + log2 L; rows past b
-  // (64-row blocks) get mcl = +inf, so every entry of theirs is exactly 0.
-  float mcl = __builtin_inff();
-  if (row_ok) mcl = a.rowfinal[((size_t)h * 128 + r) * 2] * a.c + log2f(a.rowfinal[((size_t)h * 128 + r) * 2 + 1]);
   const uint16_t* Kg = a.k + (size_t)(h / a.G) * a.n * kHeadDim;
   const int J0 = sp * a.bps;
   const int J1 = (J0 + a.bps < a.nb) ? J0 + a.bps : a.nb;
   const int diag_off = a.b - 1 - r;  // key k of row r lies on the diagonal through (last row, k + diag_off)
+  float m_run = -__builtin_inff(), l_run = 0.f, anc = 0.f;
   int buf = 0;
   u32x4 pre[4];
   if (J0 < J1) load_k_regs(pre, Kg, J0 * a.B, a.n, tid);
   for (int J = J0; J < J1; ++J) {
-    float lo = 0.f, hi = 0.f, anc = 0.f;  // diagonal mass staying in J / moving to J + 1; anchor mass
+    float lo = 0.f, hi = 0.f;
     const int blo = J * a.B;
     const int bhi = blo + a.B < a.n ? blo + a.B : a.n;
     const int ksplit = (J + 1) * a.B - diag_off;  // keys >= this lie on diagonals of slash block J + 1
@@ -214,12 +125,38 @@ __global__ __launch_bounds__(NT) void est_reduce(EstArgs a) {
       // windows (all but a few) need no per-entry masks and no anchor sum.
       const bool plain = key0 + BK - 1 <= a.n - a.b && key0 + BK <= bhi && key0 >= a.w_sink &&
                          key0 + BK <= a.n - a.w_local;
+      if (!plain) {
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int key = key_of(key0, mb, i, l);
+            if (!row_ok || key > qi || key >= bhi) s[mb][i] = -__builtin_inff();
+          }
+      }
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[mb][i]);
+      mx = fmaxf(mx, swap_halves(mx));
+      if (mx > m_run) {  // the same in both lanes of a row
+        const float alpha = m_run == -__builtin_inff() ? 0.f : fast_exp2((m_run - mx) * a.c);
+        l_run *= alpha;
+        anc *= alpha;
+        lo *= alpha;
+        hi *= alpha;
+        m_run = mx;
+      }
+      const float mc = m_run == -__builtin_inff() ? 0.f : m_run * a.c;
+      float ps = 0.f;
       if (plain) {
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
-            const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mcl));
+            const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc));
+            ps += p;
             if (key_of(key0, mb, i, l) < ksplit) lo += p; else hi += p;
           }
       } else {
@@ -228,47 +165,120 @@ __global__ __launch_bounds__(NT) void est_reduce(EstArgs a) {
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
             const int key = key_of(key0, mb, i, l);
-            float p = 0.f;
-            if (key <= qi && key < bhi) p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mcl));
+            const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc));  // masked: exp2(-inf) = 0
+            ps += p;
             if (key < ksplit) lo += p; else hi += p;
             if (key < a.w_sink || key >= a.n - a.w_local) anc += p;
           }
       }
+      l_run += ps;
     }
-    block_reduce4(make_float4(lo + hi, lo, hi, anc), red, tid, a.parts + (size_t)h * a.nb + J);
+    lo += swap_halves(lo);
+    hi += swap_halves(hi);
+    if (l < 32 && row_ok) a.parts[((size_t)h * a.nb + J) * 128 + r] = make_float4(lo, hi, m_run, 0.f);
+  }
+  l_run += swap_halves(l_run);
+  anc += swap_halves(anc);
+  if (l < 32 && row_ok) a.rowstat[((size_t)h * a.splits + sp) * 128 + r] = make_float4(m_run, l_run, anc, 0.f);
+}
+
+// Merges a range's (max m, sums l and anchor under m) into a running (M, L, A).
+__device__ __forceinline__ void merge_stats(float& M, float& L, float& A, float m, float l, float anc, float c) {
+  if (m == -__builtin_inff()) return;
+  if (m > M) {
+    const float f = M == -__builtin_inff() ? 0.f : fast_exp2((M - m) * c);
+    L = L * f + l;
+    A = A * f + anc;
+    M = m;
+  } else {
+    const float f = fast_exp2((m - M) * c);
+    L += l * f;
+    A += anc * f;
   }
 }
 
-// p_v[J] = column mass / b;  p_s[J] = (diag-low[J] + diag-high[J-1]) / b;  C_struct = anchor mass / b.
-__global__ __launch_bounds__(256) void est_finalize(EstArgs a) {
-  __shared__ float red[256];
-  const int h = blockIdx.x, tid = threadIdx.x;
-  const float4* P = a.parts + (size_t)h * a.nb;
-  const float invb = 1.f / (float)a.b;
-  float anch = 0.f;
-  for (int J = tid; J < a.nb; J += 256) {
-    const float4 cur = P[J];
-    const float prev_hi = J > 0 ? P[J - 1].z : 0.f;
-    a.p_v[(size_t)h * a.nb + J] = cur.x * invb;
-    a.p_s[(size_t)h * a.nb + J] = (cur.y + prev_hi) * invb;
-    anch += cur.w;
+// Per query head: each proxy row's max M and sum L over all ranges (eight lanes per
+// row, each merging every eighth range in one pass, then a fixed-order butterfly),
+// the row's normaliser mcl = M c + log2 L for the block sums, and C_struct = (1/b)
+// sum over rows of the row's anchor mass / L, summed over rows in a fixed order.
+// 1024 threads.
+__global__ __launch_bounds__(1024) void est_combine(EstArgs a) {
+  __shared__ float red[128];
+  const int h = blockIdx.x, j = threadIdx.x & 7, r = threadIdx.x >> 3;
+  const float4* src = a.rowstat + (size_t)h * a.splits * 128 + r;
+  const bool row_ok = r < a.b;
+  float M = -__builtin_inff(), L = 0.f, A = 0.f;
+  if (row_ok)
+    for (int sp = j; sp < a.splits; sp += 8) {
+      const float4 st = src[(size_t)sp * 128];
+      merge_stats(M, L, A, st.x, st.y, st.z, a.c);
+    }
+#pragma unroll
+  for (int o = 1; o < 8; o <<= 1) {
+    const float m2 = __shfl_xor(M, o, 64), l2 = __shfl_xor(L, o, 64), a2 = __shfl_xor(A, o, 64);
+    merge_stats(M, L, A, m2, l2, a2, a.c);
   }
-  red[tid] = anch;
+  if (j == 0) {
+    a.rowfinal[(size_t)h * 128 + r] = row_ok ? M * a.c + log2f(L) : __builtin_inff();
+    red[r] = row_ok ? A / L : 0.f;
+  }
   __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (tid < s) red[tid] += red[tid + s];
-    __syncthreads();
+  if (threadIdx.x < 64) {
+    float t = red[threadIdx.x] + red[threadIdx.x + 64];
+    t = wave_sum(t);
+    if (threadIdx.x == 0) a.c_struct[h] = t / (float)a.b;
   }
-  if (tid == 0) a.c_struct[h] = red[0] * invb;
+}
+
+// p_v[J] = (1/b) sum_r (lo + hi)[r][J] 2^(m c - mcl_r);  p_s[J] = (1/b) sum_r (lo[r][J] +
+// hi[r][J - 1]) scaled alike.  Each wave takes kScaleRun consecutive blocks, lanes take
+// rows l and l + 64, and a block's row sum is a fixed-order butterfly.
+constexpr int kScaleRun = 2;
+__global__ __launch_bounds__(256) void est_scale(EstArgs a) {
+  const int h = blockIdx.x, l = threadIdx.x & 63;
+  const int Ja = (blockIdx.y * 4 + (threadIdx.x >> 6)) * kScaleRun;
+  if (Ja >= a.nb) return;
+  const int Jb = Ja + kScaleRun < a.nb ? Ja + kScaleRun : a.nb;
+  const bool ok0 = l < a.b, ok1 = l + 64 < a.b;
+  const float mcl0 = ok0 ? a.rowfinal[(size_t)h * 128 + l] : 0.f;
+  const float mcl1 = ok1 ? a.rowfinal[(size_t)h * 128 + l + 64] : 0.f;
+  const float4* P = a.parts + (size_t)h * a.nb * 128;
+  auto row = [&](int J, int rr, float mcl, bool ok, float& lo, float& hi) {
+    lo = hi = 0.f;
+    if (!ok) return;
+    const float4 e = P[(size_t)J * 128 + rr];
+    const float f = e.z == -__builtin_inff() ? 0.f : fast_exp2(e.z * a.c - mcl);
+    lo = e.x * f;
+    hi = e.y * f;
+  };
+  float prev_hi = 0.f;
+  if (Ja > 0) {
+    float lo0, hi0, lo1, hi1;
+    row(Ja - 1, l, mcl0, ok0, lo0, hi0);
+    row(Ja - 1, l + 64, mcl1, ok1, lo1, hi1);
+    prev_hi = wave_sum(hi0 + hi1);
+  }
+  const float invb = 1.f / (float)a.b;
+  for (int J = Ja; J < Jb; ++J) {
+    float lo0, hi0, lo1, hi1;
+    row(J, l, mcl0, ok0, lo0, hi0);
+    row(J, l + 64, mcl1, ok1, lo1, hi1);
+    const float slo = wave_sum(lo0 + lo1), shi = wave_sum(hi0 + hi1);
+    if (l == 0) {
+      a.p_v[(size_t)h * a.nb + J] = (slo + shi) * invb;
+      a.p_s[(size_t)h * a.nb + J] = (slo + prev_hi) * invb;
+    }
+    prev_hi = shi;
+  }
 }
 
 }  // namespace
 
 EstSplit est_split(const Dims& d) {
   EstSplit s;
-  const int64_t want = 2048;  // target workgroups for pass 1 / pass 2
+  const int64_t want = 2048;  // target workgroups of the pass
   int64_t bps = ((int64_t)d.nb * d.hq + want - 1) / want;
-  if (bps < 1) bps = 1;
+  if (bps < 4) bps = 4;  // short layers: fewer, longer ranges (each range loads Q_hat once)
   s.bps = (int)bps;
   s.splits = (d.nb + s.bps - 1) / s.bps;
   if (s.splits < 1) s.splits = 1;
@@ -287,15 +297,15 @@ hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, 
   a.bps = sp.bps; a.splits = sp.splits;
   a.c = scale * kLog2e;
   a.w_sink = w_sink; a.w_local = w_local;
-  a.rowstat = reinterpret_cast<float*>(ws + L.rowstat);
+  a.rowstat = reinterpret_cast<float4*>(ws + L.rowstat);
   a.rowfinal = reinterpret_cast<float*>(ws + L.rowfinal);
   a.parts = reinterpret_cast<float4*>(ws + L.parts);
   a.c_struct = c_struct; a.p_v = p_v; a.p_s = p_s;
   const int grid = d.hq * sp.splits;
-  hipLaunchKernelGGL(est_rowstats, dim3(grid), dim3(NT), 0, stream, a);
-  hipLaunchKernelGGL(est_combine, dim3(d.hq, 4), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(est_reduce, dim3(grid), dim3(NT), 0, stream, a);
-  hipLaunchKernelGGL(est_finalize, dim3(d.hq), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(est_pass, dim3(grid), dim3(NT), 0, stream, a);
+  hipLaunchKernelGGL(est_combine, dim3(d.hq), dim3(1024), 0, stream, a);
+  const int runs = (d.nb + kScaleRun - 1) / kScaleRun;
+  hipLaunchKernelGGL(est_scale, dim3(d.hq, (runs + 3) / 4), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

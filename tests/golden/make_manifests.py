@@ -49,6 +49,10 @@ def head_record(q, k, v, block, params, attend):
         "k_v": len(r.S_v),
         "k_s": len(r.S_s),
         "pe_k_star": None if r.pe_info is None else int(r.pe_info["kstar"]),
+        # VS residual r_d = 1 - p_d[0] - p_d[N_b - 1] per direction (Alg. 3); below float32
+        # resolution next to 1 the floor, and with it the VS selection, is degenerate
+        "residual_v": float(max(1.0 - r.p_v[0] - r.p_v[nb - 1], 0.0)),
+        "residual_s": float(max(1.0 - r.p_s[0] - r.p_s[nb - 1], 0.0)),
         "pairs": int(pairs),
         "density": pairs / (nb * (nb + 1) / 2),
     }

