@@ -463,10 +463,15 @@ __global__ __launch_bounds__(256) void jsd_score(JsdArgs a) {
   if (tid == 0) a.jsd[h] = (float)sqrt(fmax(0.5 * t, 0.0));
 }
 
-// Pooled logits (log2 domain), 64 x 64 tiles of the block-causal triangle.  grid (ntri, hq), 256 threads.
+// Pooled logits (log2 domain) on fp32 MFMA: 64 x 64 tiles of the block-causal
+// triangle, grid (ntri, hq), 256 threads; wave w computes the 32 x 32 sub-tile
+// (query blocks 32 (w >> 1) .., key blocks 32 (w & 1) ..) as 64 steps of
+// v_mfma_f32_32x32x2_f32.  The contraction over d is split between the half-waves:
+// at step t, lanes 0..31 contribute d = t and lanes 32..63 d = 64 + t, for A (Q_bar
+// rows) and B (K_bar rows) alike, so each lane streams 64 consecutive floats of its
+// row with 16-byte loads.  Output row m = 8 (i / 4) + 4 (lane / 32) + i % 4 of
+// register i, column = lane % 32.
 __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
-  __shared__ float Qs[128][64];
-  __shared__ float Ks[128][64];
   const int h = blockIdx.y, tid = threadIdx.x;
   if (a.route[h] != 1) return;
   const int t = blockIdx.x;
@@ -474,44 +479,37 @@ __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
   while ((qt + 1) * (qt + 2) / 2 <= t) ++qt;
   while (qt * (qt + 1) / 2 > t) --qt;
   const int kt = t - qt * (qt + 1) / 2;
-  const int qb0 = qt * 64, kb0 = kt * 64;
-  const float* Qb = a.qbar + (size_t)h * a.nb * kHeadDim;
-  const float* Kb = a.kbar + (size_t)(h / a.G) * a.nb * kHeadDim;
-  for (int idx = tid; idx < 64 * 32; idx += 256) {
-    const int row = idx >> 5, d4 = idx & 31;
-    float4 qv = make_float4(0.f, 0.f, 0.f, 0.f), kv = qv;
-    if (qb0 + row < a.nb) qv = *reinterpret_cast<const float4*>(Qb + (size_t)(qb0 + row) * kHeadDim + 4 * d4);
-    if (kb0 + row < a.nb) kv = *reinterpret_cast<const float4*>(Kb + (size_t)(kb0 + row) * kHeadDim + 4 * d4);
-    Qs[4 * d4 + 0][row] = qv.x; Qs[4 * d4 + 1][row] = qv.y; Qs[4 * d4 + 2][row] = qv.z; Qs[4 * d4 + 3][row] = qv.w;
-    Ks[4 * d4 + 0][row] = kv.x; Ks[4 * d4 + 1][row] = kv.y; Ks[4 * d4 + 2][row] = kv.z; Ks[4 * d4 + 3][row] = kv.w;
-  }
-  __syncthreads();
-  const int tx = tid & 15, ty = tid >> 4;
-  float acc[4][4];
+  const int w = tid >> 6, l = tid & 63;
+  const int qs0 = qt * 64 + 32 * (w >> 1), ks0 = kt * 64 + 32 * (w & 1);
+  if (ks0 > qs0 + 31 || qs0 >= a.nb) return;  // sub-tile wholly above the diagonal or past N_b
+  const int qrow = qs0 + (l & 31), krow = ks0 + (l & 31);
+  const int d0 = 64 * (l >> 5);
+  const float* Qr = a.qbar + ((size_t)h * a.nb + (qrow < a.nb ? qrow : 0)) * kHeadDim + d0;
+  const float* Kr = a.kbar + ((size_t)(h / a.G) * a.nb + (krow < a.nb ? krow : 0)) * kHeadDim + d0;
+  const bool qok = qrow < a.nb, kok = krow < a.nb;
+  f32x16 acc = zero16();
+#pragma unroll 2
+  for (int c = 0; c < 64; c += 16) {
+    float4 qa[4], ka[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int u = 0; u < 4; ++u) {
+      qa[u] = qok ? *reinterpret_cast<const float4*>(Qr + c + 4 * u) : make_float4(0.f, 0.f, 0.f, 0.f);
+      ka[u] = kok ? *reinterpret_cast<const float4*>(Kr + c + 4 * u) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
-  for (int d = 0; d < kHeadDim; ++d) {
-    const float4 qa = *reinterpret_cast<const float4*>(&Qs[d][4 * ty]);
-    const float4 ka = *reinterpret_cast<const float4*>(&Ks[d][4 * tx]);
-    const float qv[4] = {qa.x, qa.y, qa.z, qa.w};
-    const float kv[4] = {ka.x, ka.y, ka.z, ka.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = __builtin_fmaf(qv[i], kv[j], acc[i][j]);
+    for (int u = 0; u < 4; ++u) {
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].x, ka[u].x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].y, ka[u].y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].z, ka[u].z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].w, ka[u].w, acc, 0, 0, 0);
+    }
   }
   float* At = a.atil + (size_t)h * a.cap;
+  const int kb = ks0 + (l & 31);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int qb = qb0 + 4 * ty + i;
-    if (qb >= a.nb) continue;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int kb = kb0 + 4 * tx + j;
-      if (kb <= qb) At[(int64_t)qb * (qb + 1) / 2 + kb] = acc[i][j] * a.c2;
-    }
+  for (int i = 0; i < 16; ++i) {
+    const int qb = qs0 + 8 * (i >> 2) + 4 * (l >> 5) + (i & 3);
+    if (qb < a.nb && kb <= qb) At[(int64_t)qb * (qb + 1) / 2 + kb] = acc[i] * a.c2;
   }
 }
 
