@@ -311,10 +311,13 @@ def test_config0_full_path():
 
 @pytest.mark.parametrize("n,block,hq,hkv", [(1000, 128, 2, 1), (777, 64, 4, 2), (130, 64, 2, 1), (100, 128, 2, 2),
                                             (4096, 64, 4, 1), (1, 128, 1, 1), (200, 128, 2, 1), (256, 128, 2, 2),
-                                            (65, 64, 2, 2)])
+                                            (65, 64, 2, 2), (529, 128, 2, 1), (1553, 128, 2, 2)])
 def test_ragged_and_small_layers(n, block, hq, hkv):
     """Ragged tails, one block (n < B, b = n), one token, and exactly two blocks (N_b <= 2:
-    every causal pair is selected) through the whole path against the oracle."""
+    every causal pair is selected) through the whole path against the oracle.  The
+    estimator takes ranges of at least four blocks, so at n = 529 (N_b = 5) and n = 1553
+    (N_b = 13) the last range is the ragged last block alone, which most proxy rows
+    cannot see (their running max stays -inf there)."""
     C = _crisp()
     _say(f"ragged layer n={n} B={block} hq={hq} hkv={hkv}")
     cfg = custom_config(n, hq, hkv, block=block, config_id=100 + n % 97)
