@@ -702,6 +702,33 @@ def test_run_to_run_determinism():
         assert np.array_equal(x, y)
 
 
+def test_concurrent_streams():
+    """The library keeps no state between calls: two layers (different shapes, block sizes
+    and parameters) run at the same time on two streams with their own workspaces give
+    exactly their results run one after the other."""
+    C = _crisp()
+    _say("two layers on two streams")
+    cfg_a = custom_config(6000, 8, 2, block=128, config_id=151)
+    cfg_b = custom_config(5000, 6, 3, block=64, config_id=152)
+    pa, pb = C.make_params(), C.make_params(alpha=1.5, gamma=0.9)
+    qa, ka, va, _ = make_layer(cfg_a, device=DEV)
+    qb, kb, vb, _ = make_layer(cfg_b, device=DEV)
+    wa = C.workspace(C.shape_of(qa, ka, 128), DEV, prefill=True)
+    wb = C.workspace(C.shape_of(qb, kb, 64), DEV, prefill=True)
+    ref_a = C.crisp_prefill_attn(qa, ka, va, pa, 128, ws=wa).clone()
+    ref_b = C.crisp_prefill_attn(qb, kb, vb, pb, 64, ws=wb).clone()
+    oa, ob = torch.empty_like(qa), torch.empty_like(qb)
+    torch.cuda.synchronize()
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            C.crisp_prefill_attn(qa, ka, va, pa, 128, ws=wa, out=oa)
+        with torch.cuda.stream(s2):
+            C.crisp_prefill_attn(qb, kb, vb, pb, 64, ws=wb, out=ob)
+        torch.cuda.synchronize()
+        assert torch.equal(oa, ref_a) and torch.equal(ob, ref_b)
+
+
 def test_empty_layer_is_noop():
     C = _crisp()
     _say("empty layer")
