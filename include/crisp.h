@@ -40,6 +40,14 @@
  * already be queued.  crisp_last_error() returns a thread-local message for the
  * last failing call of the calling thread.  Non-finite inputs give undefined
  * (but memory-safe) results.  No C++ exception crosses this interface.
+ *
+ * Debug build: libcrisp_debug.so exports the same functions with the same host-side
+ * validation and, before each call's kernels, also checks on the device that Q, K and
+ * V hold no infinite or NaN value and, for crisp_sparse_attn, that every list row
+ * keeps row_ptr within [0, col_cap_per_head] and non-decreasing and its entries in
+ * [0, qb] and strictly increasing; a violation is CRISP_EINVAL with a message naming
+ * it.  These checks launch their own kernels and wait for the stream (the one place
+ * where the library synchronises), so the debug build is for testing, not timing.
  */
 #ifndef CRISP_H
 #define CRISP_H

@@ -1,4 +1,6 @@
-"""Builds libcrisp.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+"""Builds libcrisp.so (the HIP kernels and the C ABI) for gfx950 with hipcc, and
+libcrisp_debug.so, the same with the host layer built with CRISP_DEBUG (device-side
+checks of the inputs before each call's kernels).
 
     python -m paper_2609_01925_amd.build
 
@@ -19,6 +21,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libcrisp.so")
+LIB_DEBUG = os.path.join(PKG, "libcrisp_debug.so")  # CRISP_DEBUG: device-side input checks
 ARCH = "gfx950"
 
 # Packed fp32 VALU forms are kept out of every kernel: the compiler would
@@ -64,9 +67,12 @@ def build(verbose: bool = False) -> str:
     for f in cpp:
         obj = os.path.join(BUILD, f[:-4] + ".o")
         jobs.append([cc, f"--offload-arch={ARCH}", *COMMON, "-c", os.path.join(CSRC, f), "-o", obj])
-    workers = min(len(jobs), max(1, min(8, os.cpu_count() or 1)))
+    # the debug library differs only in the host layer
+    debug_jobs = [[cc, f"--offload-arch={ARCH}", *COMMON, "-DCRISP_DEBUG=1", "-c", os.path.join(CSRC, f),
+                   "-o", os.path.join(BUILD, f[:-4] + "_debug.o")] for f in cpp]
+    workers = min(len(jobs) + len(debug_jobs), max(1, min(8, os.cpu_count() or 1)))
     with cf.ThreadPoolExecutor(workers) as ex:
-        results = list(ex.map(_run, jobs))
+        results = list(ex.map(_run, jobs + debug_jobs))
     bad = [(cmd, out) for rc, cmd, out in results if rc != 0]
     if verbose or bad:
         for rc, cmd, out in results:
@@ -75,11 +81,13 @@ def build(verbose: bool = False) -> str:
     if bad:
         raise RuntimeError("libcrisp compile failed:\n" + "\n".join(f"$ {c}\n{o}" for c, o in bad))
     objs = [j[-1] for j in jobs]
-    tmp = LIB + ".tmp"
-    rc, cmd, out = _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
-    if rc != 0:
-        raise RuntimeError(f"libcrisp link failed:\n$ {cmd}\n{out}")
-    os.replace(tmp, LIB)
+    debug_objs = [o for o in objs if not any(o.endswith(f[:-4] + ".o") for f in cpp)] + [j[-1] for j in debug_jobs]
+    for target, members in ((LIB, objs), (LIB_DEBUG, debug_objs)):
+        tmp = target + ".tmp"
+        rc, cmd, out = _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *members, "-o", tmp])
+        if rc != 0:
+            raise RuntimeError(f"libcrisp link failed:\n$ {cmd}\n{out}")
+        os.replace(tmp, target)
     return LIB
 
 

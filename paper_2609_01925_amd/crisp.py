@@ -15,7 +15,11 @@ from typing import Optional, Tuple
 
 import torch
 
-_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcrisp.so")
+# CRISP_DEBUG=1 in the environment loads the debug build, which also checks the inputs on
+# the device (non-finite values, malformed caller lists) and waits for the stream to do so.
+_LIB_DIR = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_LIB_DIR, "libcrisp_debug.so" if os.environ.get("CRISP_DEBUG") == "1" else "libcrisp.so")
+DEBUG_LIB_PATH = os.path.join(_LIB_DIR, "libcrisp_debug.so")
 
 CRISP_OK, CRISP_EINVAL, CRISP_EUNSUPPORTED, CRISP_EHIP = 0, 1, 2, 3
 ROUTE_VS, ROUTE_PE = 0, 1

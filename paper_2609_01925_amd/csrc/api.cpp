@@ -1,6 +1,8 @@
 // libcrisp host layer: argument validation, workspace carving and the launch
 // sequence behind the C ABI declared in include/crisp.h.  Validation touches no
 // device state, so every argument error is reported before anything is queued.
+// Built with CRISP_DEBUG (libcrisp_debug.so) it also checks the inputs on the device
+// (non-finite values, malformed caller lists), waiting for the stream to do so.
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
@@ -97,6 +99,43 @@ crisp_status hip_status(hipError_t e, const char* what) {
 }
 
 bool empty(const Dims& d) { return d.n == 0 || d.hq == 0; }
+
+#ifdef CRISP_DEBUG
+// Debug build: non-finite inputs and malformed caller lists become CRISP_EINVAL.
+// These checks launch their own kernels and wait for the stream.
+crisp_status debug_inputs(const Dims& d, const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                          hipStream_t st) {
+  const struct {
+    const uint16_t* p;
+    size_t n;
+    const char* name;
+  } in[3] = {{q, (size_t)d.hq * d.n * kHeadDim, "q"},
+             {k, (size_t)d.hkv * d.n * kHeadDim, "k"},
+             {v, (size_t)d.hkv * d.n * kHeadDim, "v"}};
+  for (const auto& x : in) {
+    if (!x.p) continue;
+    int found = 0;
+    CHECK(hip_status(debug_nonfinite(x.p, x.n, st, &found), "debug input check"));
+    if (found) return fail(CRISP_EINVAL, "%s holds an infinite or NaN value (debug build)", x.name);
+  }
+  return CRISP_OK;
+}
+
+crisp_status debug_list_check(const Dims& d, const int32_t* row_ptr, const int32_t* col_idx, int64_t cap,
+                              hipStream_t st) {
+  int code = 0;
+  CHECK(hip_status(debug_lists(d, row_ptr, col_idx, cap, st, &code), "debug list check"));
+  static const char* const what[4] = {"", "a row_ptr value outside [0, col_cap] or decreasing",
+                                      "an entry outside [0, qb]", "entries not strictly increasing"};
+  if (code) return fail(CRISP_EINVAL, "block lists: %s (debug build)", what[code & 3]);
+  return CRISP_OK;
+}
+#define DEBUG_INPUTS(q, k, v, st) CHECK(debug_inputs(d, (q), (k), (v), (st)))
+#define DEBUG_LISTS(rp, ci, cap, st) CHECK(debug_list_check(d, (rp), (ci), (cap), (st)))
+#else
+#define DEBUG_INPUTS(q, k, v, st) ((void)0)
+#define DEBUG_LISTS(rp, ci, cap, st) ((void)0)
+#endif
 
 }  // namespace
 
@@ -217,6 +256,7 @@ crisp_status crisp_estimate(const crisp_shape* shape, const crisp_params* params
   CHECK(check_ptr(workspace, 256, "workspace"));
   if (workspace_bytes < ws_layout(d).total)
     return fail(CRISP_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, ws_layout(d).total);
+  DEBUG_INPUTS(q, k, nullptr, (hipStream_t)stream);
   return hip_status(launch_estimate(d, scale_of(params->softmax_scale), params->w_sink, params->w_local, q, k,
                                     c_struct, p_v, p_s, (char*)workspace, (hipStream_t)stream),
                     "crisp_estimate launch");
@@ -236,6 +276,7 @@ crisp_status crisp_jsd(const crisp_shape* shape, const crisp_params* params, con
   CHECK(check_ptr(workspace, 256, "workspace"));
   if (workspace_bytes < ws_layout(d).total)
     return fail(CRISP_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, ws_layout(d).total);
+  DEBUG_INPUTS(q, k, nullptr, (hipStream_t)stream);
   return hip_status(launch_jsd(d, scale_of(params->softmax_scale), q, k, p_v, jsd, (char*)workspace,
                                (hipStream_t)stream),
                     "crisp_jsd launch");
@@ -264,6 +305,7 @@ crisp_status crisp_route_select(const crisp_shape* shape, const crisp_params* pa
                 (long long)d.cap);
   if (workspace_bytes < ws_layout(d).total)
     return fail(CRISP_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, ws_layout(d).total);
+  DEBUG_INPUTS(q, k, nullptr, (hipStream_t)stream);
   return hip_status(launch_select(d, scale_of(params->softmax_scale), params->alpha, route_tau(params),
                                   params->gamma, kmin_of(params, d.B), params->vs_mode, params->floor_mode, false, q, k,
                                   c_struct, p_v,
@@ -301,6 +343,8 @@ crisp_status crisp_sparse_attn(const crisp_shape* shape, float softmax_scale, co
     if (workspace_bytes < attn_schedule_bytes(d))
       return fail(CRISP_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, attn_schedule_bytes(d));
   }
+  DEBUG_INPUTS(q, k, v, (hipStream_t)stream);
+  DEBUG_LISTS(row_ptr, col_idx, col_cap_per_head, (hipStream_t)stream);
   return hip_status(launch_attn(d, scale_of(softmax_scale), q, k, v, row_ptr, col_idx, col_cap_per_head, false, o,
                                 workspace_or_null, (hipStream_t)stream),
                     "crisp_sparse_attn launch");
@@ -317,6 +361,7 @@ crisp_status crisp_dense_attn(const crisp_shape* shape, float softmax_scale, con
   CHECK(check_ptr(k, 16, "k"));
   CHECK(check_ptr(v, 16, "v"));
   CHECK(check_ptr(o, 16, "o"));
+  DEBUG_INPUTS(q, k, v, (hipStream_t)stream);
   return hip_status(launch_attn(d, scale_of(softmax_scale), q, k, v, nullptr, nullptr, 0, true, o, nullptr,
                                 (hipStream_t)stream),
                     "crisp_dense_attn launch");
@@ -346,6 +391,7 @@ crisp_status crisp_prefill_attn(const crisp_shape* shape, const crisp_params* pa
   const PrefillExtra e = prefill_extra(d, L.total);
   const size_t need = given ? e.route : e.total;
   if (workspace_bytes < need) return fail(CRISP_EINVAL, "workspace too small: %zu < %zu", workspace_bytes, need);
+  DEBUG_INPUTS(q, k, v, (hipStream_t)stream);
   char* ws = (char*)workspace;
   if (d.n < params->dense_below_len) {  // context-length gate: the layer is dense attention
     if (given)

@@ -56,4 +56,12 @@ hipError_t launch_dense_lists(const Dims& d, int8_t* route, int32_t* row_ptr, in
 hipError_t launch_jsd(const Dims& d, float scale, const uint16_t* q, const uint16_t* k, const float* p_v,
                       float* jsd, char* ws, hipStream_t stream);
 
+// Debug build only (CRISP_DEBUG): these wait for the stream.  *found = 1 if any of
+// the n bf16 values is infinite or NaN; *code = 0 if every row of the lists keeps the
+// list invariants, else 1 (row_ptr out of range or decreasing), 2 (an entry outside
+// [0, qb]) or 3 (entries not strictly increasing).
+hipError_t debug_nonfinite(const uint16_t* p, size_t n, hipStream_t stream, int* found);
+hipError_t debug_lists(const Dims& d, const int32_t* row_ptr, const int32_t* col_idx, int64_t cap,
+                       hipStream_t stream, int* code);
+
 }  // namespace crisp

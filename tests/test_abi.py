@@ -37,6 +37,25 @@ def test_header_functions_are_exported():
     assert set(C.EXPORTED) == set(names)
 
 
+def test_debug_library_exports_the_same_functions_and_validates_alike():
+    """libcrisp_debug.so (host layer built with CRISP_DEBUG) exports the header's functions
+    and rejects bad arguments on the host exactly as the release library does."""
+    names = declared_functions()
+    out = subprocess.run(["nm", "-D", "--defined-only", C.DEBUG_LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(line.split()[-1] for line in out.splitlines() if line.strip())
+    assert not [n for n in names if n not in exported]
+    dbg = C._load(C.DEBUG_LIB_PATH)
+    p = C.make_params()
+    for sh, code in ((C.CrispShape(3, 2, 4096, 128, 128), C.CRISP_EINVAL),
+                     (C.CrispShape(4, 2, 4096, 64, 128), C.CRISP_EUNSUPPORTED)):
+        st = dbg.crisp_estimate(ctypes.byref(sh), ctypes.byref(p), P_ALIGNED, P_ALIGNED, P_ALIGNED, P_ALIGNED,
+                                P_ALIGNED, P_ALIGNED, 1 << 40, None)
+        assert st == code
+    sh = C.CrispShape(4, 2, 4096, 128, 128)
+    assert dbg.crisp_dense_attn(ctypes.byref(sh), 0.0, P_MISALIGNED, P_ALIGNED, P_ALIGNED, P_ALIGNED,
+                                None) == C.CRISP_EINVAL
+
+
 def test_params_default_matches_paper():
     p = C.crisp_params_default()
     assert (p.alpha, p.w_sink, p.w_local, p.k_min_blocks, p.softmax_scale) == (1.0, 128, 128, 0, 0.0)

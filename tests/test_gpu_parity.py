@@ -852,3 +852,62 @@ def test_golden_manifests_on_gpu():
                 assert abs(og.mean() - st["out_mean"]) <= 2e-3, f"{w}: output mean {og.mean()} vs {st['out_mean']}"
                 assert abs(np.abs(og).max() - st["out_max_abs"]) <= 2e-2, f"{w}: max |O| {np.abs(og).max()}"
         del q, k, v, o
+
+
+def test_debug_build_checks_inputs():
+    """libcrisp_debug.so: on valid inputs the same results as the release library, bit for
+    bit; infinite or NaN values in Q, K or V, and caller lists with an entry outside
+    [0, qb], entries out of order or a decreasing row_ptr, are CRISP_EINVAL with a
+    message naming them, before any of the call's kernels run."""
+    C = _crisp()
+    _say("debug build input checks")
+    release = C.lib
+    cfg = custom_config(1000, 2, 1, block=128, config_id=153)
+    q, k, v, _ = make_layer(cfg, device=DEV)
+    params = C.make_params()
+    o_rel, _, rp, ci = C.crisp_prefill_attn(q, k, v, params, 128, return_lists=True)
+    s_rel = C.crisp_sparse_attn(q, k, v, rp, ci, 128)
+    d_rel = C.crisp_dense_attn(q, k, v, 128)
+    torch.cuda.synchronize()
+    try:
+        C.lib = C._load(C.DEBUG_LIB_PATH)
+        assert torch.equal(C.crisp_prefill_attn(q, k, v, params, 128), o_rel)
+        assert torch.equal(C.crisp_sparse_attn(q, k, v, rp, ci, 128), s_rel)
+        assert torch.equal(C.crisp_dense_attn(q, k, v, 128), d_rel)
+
+        def rejects(fn, text):
+            with pytest.raises(C.CrispError) as err:
+                fn()
+            assert err.value.status == C.CRISP_EINVAL and text in str(err.value), str(err.value)
+
+        kn = k.clone()
+        kn[0, 517, 33] = float("nan")
+        rejects(lambda: C.crisp_prefill_attn(q, kn, v, params, 128), "k holds")
+        rejects(lambda: C.crisp_estimate(q, kn, params, 128), "k holds")
+        qi = q.clone()
+        qi[1, 999, 127] = float("inf")
+        rejects(lambda: C.crisp_dense_attn(qi, k, v, 128), "q holds")
+        vi = v.clone()
+        vi[0, 0, 0] = float("-inf")
+        rejects(lambda: C.crisp_sparse_attn(q, k, vi, rp, ci, 128), "v holds")
+        nb = O.n_blocks(1000, 128)
+        cap = ci.shape[1]
+        # head 0, last row: one entry past the diagonal
+        bad = ci.clone()
+        last = int(rp[0, nb - 1])
+        bad[0, last] = nb
+        rejects(lambda: C.crisp_sparse_attn(q, k, v, rp, bad, 128), "outside [0, qb]")
+        # head 1, row 3 holds {0, 3} and more: swap two entries
+        bad = ci.clone()
+        b3 = int(rp[1, 3])
+        bad[1, b3], bad[1, b3 + 1] = ci[1, b3 + 1], ci[1, b3]
+        rejects(lambda: C.crisp_sparse_attn(q, k, v, rp, bad, 128), "strictly increasing")
+        badp = rp.clone()
+        badp[0, 2] = badp[0, 1] - 1
+        rejects(lambda: C.crisp_sparse_attn(q, k, v, badp, ci, 128), "row_ptr")
+        badp = rp.clone()
+        badp[1, nb] = cap + 1
+        rejects(lambda: C.crisp_sparse_attn(q, k, v, badp, ci, 128), "row_ptr")
+        torch.cuda.synchronize()
+    finally:
+        C.lib = release
