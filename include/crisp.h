@@ -47,7 +47,9 @@
  * keeps row_ptr within [0, col_cap_per_head] and non-decreasing and its entries in
  * [0, qb] and strictly increasing; a violation is CRISP_EINVAL with a message naming
  * it.  These checks launch their own kernels and wait for the stream (the one place
- * where the library synchronises), so the debug build is for testing, not timing.
+ * where the library synchronises), and its attention kernels run their tile pipeline
+ * serialised (same arithmetic, same results as the release build, bit for bit), so
+ * the debug build is for testing, not timing.
  */
 #ifndef CRISP_H
 #define CRISP_H

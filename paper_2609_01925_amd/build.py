@@ -1,6 +1,6 @@
 """Builds libcrisp.so (the HIP kernels and the C ABI) for gfx950 with hipcc, and
-libcrisp_debug.so, the same with the host layer built with CRISP_DEBUG (device-side
-checks of the inputs before each call's kernels).
+libcrisp_debug.so, built with CRISP_DEBUG: device-side checks of the inputs before
+each call's kernels, and the attention's tile pipeline serialised (a race check).
 
     python -m paper_2609_01925_amd.build
 
@@ -67,9 +67,12 @@ def build(verbose: bool = False) -> str:
     for f in cpp:
         obj = os.path.join(BUILD, f[:-4] + ".o")
         jobs.append([cc, f"--offload-arch={ARCH}", *COMMON, "-c", os.path.join(CSRC, f), "-o", obj])
-    # the debug library differs only in the host layer
+    # the debug library: host layer with input checks, attention with its tile
+    # pipeline serialised (the other kernels are the release objects)
     debug_jobs = [[cc, f"--offload-arch={ARCH}", *COMMON, "-DCRISP_DEBUG=1", "-c", os.path.join(CSRC, f),
                    "-o", os.path.join(BUILD, f[:-4] + "_debug.o")] for f in cpp]
+    debug_jobs.append([cc, f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS, *EXTRA.get("attn.hip", []),
+                       "-DCRISP_DEBUG=1", "-c", os.path.join(CSRC, "attn.hip"), "-o", os.path.join(BUILD, "attn_debug.o")])
     workers = min(len(jobs) + len(debug_jobs), max(1, min(8, os.cpu_count() or 1)))
     with cf.ThreadPoolExecutor(workers) as ex:
         results = list(ex.map(_run, jobs + debug_jobs))
@@ -81,7 +84,8 @@ def build(verbose: bool = False) -> str:
     if bad:
         raise RuntimeError("libcrisp compile failed:\n" + "\n".join(f"$ {c}\n{o}" for c, o in bad))
     objs = [j[-1] for j in jobs]
-    debug_objs = [o for o in objs if not any(o.endswith(f[:-4] + ".o") for f in cpp)] + [j[-1] for j in debug_jobs]
+    replaced = {f[:-4] + ".o" for f in cpp} | {"attn.o"}
+    debug_objs = [o for o in objs if os.path.basename(o) not in replaced] + [j[-1] for j in debug_jobs]
     for target, members in ((LIB, objs), (LIB_DEBUG, debug_objs)):
         tmp = target + ".tmp"
         rc, cmd, out = _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *members, "-o", tmp])

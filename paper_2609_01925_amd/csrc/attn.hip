@@ -253,6 +253,19 @@ __device__ __forceinline__ bf16x4 lds_ld_tr(int addr) {
 // Waits until every LDS-DMA load of this wave has landed (s_waitcnt vmcnt(0)).
 __device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
 
+// Debug build: the tile pipeline serialised -- every tile load waited for and a
+// barrier after each LDS phase -- so that its results, compared bit for bit with the
+// pipelined kernel's, show that the rings' overlap of loads and reads never races.
+// The arithmetic and its order are unchanged.
+#ifdef CRISP_DEBUG
+__device__ __forceinline__ void race_sync() {
+  wait_dma();
+  __syncthreads();
+}
+#else
+__device__ __forceinline__ void race_sync() {}
+#endif
+
 // S^T for one tile: s[h][mb] holds keys 32 mb + (C-layout row) against the 32
 // queries of half h (lane column).  Rows 32..63 have the same swizzle as rows
 // 0..31, so sub-block mb is +32 mb rows, and each K operand read serves every
@@ -463,6 +476,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
 
       if (j + 2 < T) fetch_tile<NW, BK>(fe, rk, kst(P), key0_of(j + 2), w);
       fetch_tile<NW, BK>(fe, rv, vst(P), key0_of(j), w);
+      race_sync();
       {
         bool vj, mj;
         const int kj = tile_key0(j, vj, mj);
@@ -482,6 +496,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
         grow = grow || !(ts[h] <= kSumLimit) || m_run[h] == -__builtin_inff();
       }
       if (!decltype(first)::value) pv_tile<QH, NMB>(vst(1 - P), off, pp, o);
+      race_sync();
       // Keeps the probabilities formed here, beside the PV product, rather than
       // letting the compiler sink them into the no-rescale path.
 #pragma unroll
@@ -518,6 +533,7 @@ __device__ __forceinline__ void attn_unit(const AttnArgs& a, int head, int qb, i
       // K operand reads with the MFMAs in its LDS/MFMA pipelining mode.
       __builtin_amdgcn_iglp_opt(0);
       qk_tile<QH, NMB>(kst(1 - P), qf, off, s);
+      race_sync();
       if (!DENSE && (((j + 1) / TPB) >> 6) != chunk0) {  // tile j+1 starts the next chunk
         ++chunk0;
         if ((chunk0 + 1) & 1)

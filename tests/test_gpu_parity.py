@@ -854,6 +854,33 @@ def test_golden_manifests_on_gpu():
         del q, k, v, o
 
 
+@pytest.mark.parametrize("layer", ["config0", "ragged-b64", "pe-8k-split-rows"])
+def test_debug_build_race_check(layer):
+    """The debug build's attention runs the same arithmetic with its tile pipeline
+    serialised (each tile load waited for, a barrier after every LDS phase): its outputs
+    equal the pipelined kernel's bit for bit, so the overlapped loads and reads of the
+    LDS rings never race.  Layers: the 4k tiny layer, a ragged B = 64 layer, and an 8k
+    layer whose long rows are split (persistent grid, partial results merged)."""
+    C = _crisp()
+    _say(f"debug race check {layer}")
+    cfg, block = {"config0": (CONFIGS[0], 128), "ragged-b64": (custom_config(3001, 4, 2, block=64, config_id=154), 64),
+                  "pe-8k-split-rows": (structured_pe_config(8192), 128)}[layer]
+    q, k, v, _ = make_layer(cfg, device=DEV)
+    params = C.make_params(alpha=cfg.alpha)
+    release = C.lib
+    o_rel, _, rp, ci = C.crisp_prefill_attn(q, k, v, params, block, return_lists=True)
+    d_rel = C.crisp_dense_attn(q, k, v, block)
+    torch.cuda.synchronize()
+    try:
+        C.lib = C._load(C.DEBUG_LIB_PATH)
+        o_dbg = C.crisp_prefill_attn(q, k, v, params, block)
+        d_dbg = C.crisp_dense_attn(q, k, v, block)
+        torch.cuda.synchronize()
+    finally:
+        C.lib = release
+    assert torch.equal(o_dbg, o_rel) and torch.equal(d_dbg, d_rel)
+
+
 def test_debug_build_checks_inputs():
     """libcrisp_debug.so: on valid inputs the same results as the release library, bit for
     bit; infinite or NaN values in Q, K or V, and caller lists with an entry outside
