@@ -76,7 +76,9 @@ def time_events(fn, steps, warmup):
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) * 1e3 / steps
     ms = sorted(a.elapsed_time(b) for a, b in evs)
-    return {"median": ms[len(ms) // 2], "mean": sum(ms) / len(ms), "min": ms[0], "max": ms[-1], "wall_per_step": wall}
+    pct = lambda f: ms[min(len(ms) - 1, int(round(f * (len(ms) - 1))))]
+    return {"median": ms[len(ms) // 2], "mean": sum(ms) / len(ms), "min": ms[0], "max": ms[-1],
+            "p10": pct(0.1), "p90": pct(0.9), "wall_per_step": wall}
 
 
 def layer_measure(cfg, steps, warmup, label):
@@ -108,7 +110,7 @@ def layer_measure(cfg, steps, warmup, label):
     del o_
 
     crisp = time_events(lambda: C.crisp_prefill_attn(q, k, v, params, block, ws=ws, out=o), steps, warmup)
-    log(f"{label}: CRISP {crisp['median']:.3f} ms/layer")
+    log(f"{label}: CRISP {crisp['wall_per_step']:.3f} ms/layer")
 
     # per-stage timing (same stream, same buffers)
     cs, pv, ps = C.crisp_estimate(q, k, params, block)
@@ -118,20 +120,20 @@ def layer_measure(cfg, steps, warmup, label):
                       steps, warmup)
     att = time_events(lambda: C.crisp_sparse_attn(q, k, v, rp, ci, block, out=o), steps, warmup)
     dense = time_events(lambda: C.crisp_dense_attn(q, k, v, block, out=o), steps, warmup)
-    log(f"{label}: stages est {est['median']:.3f} sel {sel['median']:.3f} attn {att['median']:.3f}; "
-        f"dense {dense['median']:.3f} ms")
+    log(f"{label}: stages est {est['mean']:.3f} sel {sel['mean']:.3f} attn {att['mean']:.3f}; "
+        f"dense {dense['wall_per_step']:.3f} ms")
 
     d = 128
     # algorithmic HBM bytes: the estimator reads each KV head's K once (one pass); the
     # selection pools Q of the PE heads and K of their groups, writes the pooled scores
     # A~ once, then reads/writes them in the softmax, reads them in the three radix passes
     # and the two CSR passes (32 bytes per causal pair per PE head), and writes the lists
-    est_gbs = cfg.n_kv_heads * cfg.seq_len * d * 2.0 / (est["median"] * 1e-3) / 1e9
+    est_gbs = cfg.n_kv_heads * cfg.seq_len * d * 2.0 / (est["mean"] * 1e-3) / 1e9
     pe_heads = [h for h in range(cfg.n_q_heads) if int(route_c[h]) == 1]
     pe_groups = len({h // cfg.group for h in pe_heads})
     sel_bytes = ((len(pe_heads) + pe_groups) * cfg.seq_len * d * 2.0 + 32.0 * nb * (nb + 1) / 2 * len(pe_heads)
                  + 4.0 * executed_pairs)
-    sel_gbs = sel_bytes / (sel["median"] * 1e-3) / 1e9
+    sel_gbs = sel_bytes / (sel["mean"] * 1e-3) / 1e9
     pair_flop = 4.0 * block * block * d
     attn_flop = executed_pairs * pair_flop
     dense_flop_exec = dense_pairs * pair_flop
@@ -139,25 +141,30 @@ def layer_measure(cfg, steps, warmup, label):
     res = {
         "workload": cfg.name, "seq_len": cfg.seq_len, "n_q_heads": cfg.n_q_heads, "n_kv_heads": cfg.n_kv_heads,
         "block": block, "alpha": cfg.alpha,
-        "ms_per_layer": crisp["median"], "ms_p_min": crisp["min"], "ms_p_max": crisp["max"],
-        "dense_ms_per_layer": dense["median"],
-        "speedup_vs_dense": dense["median"] / crisp["median"],
-        "stage_ms": {"estimate": est["median"], "route_select": sel["median"], "sparse_attn": att["median"]},
+        # exactly `steps` prefills between two synchronisations, per step; the per-step
+        # event times give the median and spread
+        "ms_per_layer": crisp["wall_per_step"], "ms_median": crisp["median"], "ms_p10": crisp["p10"],
+        "ms_p90": crisp["p90"], "ms_p_min": crisp["min"], "ms_p_max": crisp["max"],
+        "dense_ms_per_layer": dense["wall_per_step"],
+        "speedup_vs_dense": dense["wall_per_step"] / crisp["wall_per_step"],
+        "stage_ms": {"estimate": est["mean"], "route_select": sel["mean"], "sparse_attn": att["mean"]},
         "routes": {"vs": n_vs, "pe": cfg.n_q_heads - n_vs},
         "executed_pairs": executed_pairs, "density": executed_pairs / dense_pairs,
-        "sparse_attn_tflops_executed": attn_flop / (att["median"] * 1e-3) / 1e12,
-        "sparse_attn_mfma_frac": attn_flop / (att["median"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
-        "dense_tflops_executed": dense_flop_exec / (dense["median"] * 1e-3) / 1e12,
-        "dense_mfma_frac": dense_flop_exec / (dense["median"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
-        "effective_tflops_dense_equiv": dense_useful / (crisp["median"] * 1e-3) / 1e12,
+        "density_by_route": {name: float(pairs_per_head[route_c == rt].sum()) / max(1, int((route_c == rt).sum()))
+                             / (nb * (nb + 1) / 2) for name, rt in (("vs", 0), ("pe", 1))},
+        "sparse_attn_tflops_executed": attn_flop / (att["mean"] * 1e-3) / 1e12,
+        "sparse_attn_mfma_frac": attn_flop / (att["mean"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+        "dense_tflops_executed": dense_flop_exec / (dense["mean"] * 1e-3) / 1e12,
+        "dense_mfma_frac": dense_flop_exec / (dense["mean"] * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS,
+        "effective_tflops_dense_equiv": dense_useful / (crisp["wall_per_step"] * 1e-3) / 1e12,
         "estimate_hbm_gbs": est_gbs, "estimate_hbm_frac": est_gbs / HBM_PEAK_GBS,
         # the estimator's proxy scores on MFMA: 2 b n d FLOP per query head (b = block)
-        "estimate_tflops": 2.0 * cfg.n_q_heads * block * cfg.seq_len * d / (est["median"] * 1e-3) / 1e12,
-        "estimate_mfma_frac": 2.0 * cfg.n_q_heads * block * cfg.seq_len * d / (est["median"] * 1e-3) / 1e12
+        "estimate_tflops": 2.0 * cfg.n_q_heads * block * cfg.seq_len * d / (est["mean"] * 1e-3) / 1e12,
+        "estimate_mfma_frac": 2.0 * cfg.n_q_heads * block * cfg.seq_len * d / (est["mean"] * 1e-3) / 1e12
         / MFMA_BF16_PEAK_TFLOPS,
         "select_hbm_gbs": sel_gbs, "select_hbm_frac": sel_gbs / HBM_PEAK_GBS,
     }
-    res["_attn_launch_ms"] = att["median"]
+    res["_attn_launch_ms"] = att["mean"]
     res["_attn_flop"] = attn_flop
     res["_tensors"] = (q, k, v, specs, route_c, rp.cpu(), ci.cpu(), pairs_per_head)
     return res
@@ -189,8 +196,8 @@ def comparator_measure(cfg, res, steps, warmup, label, mixes=True):
         t = time_events(lambda: C.crisp_prefill_attn(q, k, v, params, block, ws=ws, out=o), steps, warmup)
         rc = route.cpu()
         n_vs = int((rc == 0).sum())
-        rec = {"ms_per_layer": t["median"], "speedup_vs_dense": res["dense_ms_per_layer"] / t["median"],
-               "crisp_speedup_vs_this": t["median"] / res["ms_per_layer"],
+        rec = {"ms_per_layer": t["wall_per_step"], "speedup_vs_dense": res["dense_ms_per_layer"] / t["wall_per_step"],
+               "crisp_speedup_vs_this": t["wall_per_step"] / res["ms_per_layer"],
                "routes": {"vs": n_vs, "pe": cfg.n_q_heads - n_vs}, "executed_pairs": pairs,
                "density": pairs / dense_pairs,
                "route_agreement_with_cstruct": float((rc == route_cs).double().mean())}
@@ -198,9 +205,9 @@ def comparator_measure(cfg, res, steps, warmup, label, mixes=True):
             cs, pv, ps = C.crisp_estimate(q, k, params, block)
             wsj = C.workspace(sh, q.device)
             rec["pattern_search_ms"] = time_events(lambda: C.crisp_jsd(q, k, pv, params, block, ws=wsj),
-                                                   steps, warmup)["median"]
+                                                   steps, warmup)["mean"]
         out[name] = rec
-        log(f"{label}: {name} {t['median']:.3f} ms/layer, density {rec['density']:.3f}, "
+        log(f"{label}: {name} {t['wall_per_step']:.3f} ms/layer, density {rec['density']:.3f}, "
             f"routes VS {n_vs}, agreement {rec['route_agreement_with_cstruct']:.2f}")
     return out
 
@@ -226,8 +233,8 @@ def floor_variants_measure(cfg, res, steps, warmup, label):
         torch.cuda.synchronize()
         pairs = float(rp[:, nb].double().sum())
         t = time_events(lambda: C.crisp_prefill_attn(q, k, v, params, block, ws=ws, out=o), steps, warmup)
-        out[name] = {"ms_per_layer": t["median"], "density": pairs / dense_pairs, "executed_pairs": pairs}
-        log(f"{label}: floor {name} {t['median']:.3f} ms/layer, density {pairs / dense_pairs:.4f}")
+        out[name] = {"ms_per_layer": t["wall_per_step"], "density": pairs / dense_pairs, "executed_pairs": pairs}
+        log(f"{label}: floor {name} {t['wall_per_step']:.3f} ms/layer, density {pairs / dense_pairs:.4f}")
     return out
 
 
