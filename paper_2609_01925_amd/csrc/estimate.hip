@@ -85,12 +85,13 @@ __device__ __forceinline__ int key_of(int key0, int mb, int i, int l) {
 }
 
 // One pass over K: scores, causal mask, per-row running max, and under that running
-// max the row's sums of exp2((s - max) c): over all its keys (l), over the anchor
-// keys (anchor mass), and per key block J split by slash block (lo: keys whose
-// diagonal through the last proxy row stays in J, hi: those moving to J + 1).  When
-// the running max rises, the sums still open are scaled down to the new max; a
-// block's (lo, hi) is written with the max it was summed under when the block ends,
-// and the range's (max, l, anchor) when the range ends.
+// max the row's sums of exp2((s - max) c): per key block J split by slash block (lo:
+// keys whose diagonal through the last proxy row stays in J, hi: those moving to
+// J + 1), over the anchor keys (anchor mass), and over all its keys (l, the blocks'
+// lo + hi added as each block ends).  When the running max rises, the sums still open
+// are scaled down to the new max; a block's (lo, hi) is written with the max it was
+// summed under when the block ends, and the range's (max, l, anchor) when the range
+// ends.
 __global__ __launch_bounds__(NT) void est_pass(EstArgs a) {
   __shared__ __attribute__((aligned(16))) char smem[2 * kTileBytes];
   const int h = blockIdx.x / a.splits, sp = blockIdx.x % a.splits;
@@ -149,14 +150,22 @@ __global__ __launch_bounds__(NT) void est_pass(EstArgs a) {
         m_run = mx;
       }
       const float mc = m_run == -__builtin_inff() ? 0.f : m_run * a.c;
-      float ps = 0.f;
-      if (plain) {
+      // In most tiles a whole wave's entries fall on one side of its rows' slash split
+      // (the split sits at key offset r + 1 of the block): one sum, no per-entry test.
+      const bool all_lo = __all(key0 + BK - 1 < ksplit), all_hi = __all(key0 >= ksplit);
+      if (plain && (all_lo || all_hi)) {
+        float t = 0.f;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) t += fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc));
+        if (all_lo) lo += t; else hi += t;
+      } else if (plain) {
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
             const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc));
-            ps += p;
             if (key_of(key0, mb, i, l) < ksplit) lo += p; else hi += p;
           }
       } else {
@@ -166,13 +175,12 @@ __global__ __launch_bounds__(NT) void est_pass(EstArgs a) {
           for (int i = 0; i < 16; ++i) {
             const int key = key_of(key0, mb, i, l);
             const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc));  // masked: exp2(-inf) = 0
-            ps += p;
             if (key < ksplit) lo += p; else hi += p;
             if (key < a.w_sink || key >= a.n - a.w_local) anc += p;
           }
       }
-      l_run += ps;
     }
+    l_run += lo + hi;  // the block's sum joins the row's, under the same running max
     lo += swap_halves(lo);
     hi += swap_halves(hi);
     if (l < 32 && row_ok) a.parts[((size_t)h * a.nb + J) * 128 + r] = make_float4(lo, hi, m_run, 0.f);
