@@ -324,6 +324,41 @@ def test_ragged_and_small_layers(n, block, hq, hkv):
     _check_layer(C, cfg, C.make_params(), where=f"n{n}")
 
 
+def _random_cases(count=24, seed=20260901):
+    """Seeded random small layers and parameter sets (the same list every run)."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(count):
+        block = int(rng.choice([64, 128]))
+        hq, hkv = [(2, 1), (4, 2), (6, 3), (8, 2), (4, 4), (5, 1)][int(rng.integers(6))]
+        n = int(rng.integers(65, 3001))
+        route_mode, vs_mode = [(0, 0), (1, 1), (0, 1), (1, 0)][int(rng.integers(4))]
+        cases.append(dict(
+            n=n, block=block, hq=hq, hkv=hkv, config_id=200 + i,
+            diffuse_frac=float(rng.choice([0.25, 0.5, 0.75])), structured_pe=bool(n >= 1024 and rng.random() < 0.5),
+            params=dict(alpha=float(rng.choice([0.5, 0.75, 1.0, 1.5, 2.0])),
+                        gamma=float(rng.choice([0.8, 0.9, 0.95, 1.0])),
+                        tau_proxy=float(rng.choice([0.1, 0.2, 0.3])),
+                        w_sink=int(rng.choice([0, 64, 128, 300])), w_local=int(rng.choice([0, 128, 500])),
+                        k_min_blocks=int(rng.choice([0, 1, 3, 8])),
+                        softmax_scale=float(rng.choice([0.0, 0.05, 0.1])),
+                        route_mode=route_mode, vs_mode=vs_mode,
+                        floor_mode=int(rng.integers(2)) if vs_mode == 0 else 0)))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_cases(), ids=lambda c: f"n{c['n']}-b{c['block']}-{c['hq']}x{c['hkv']}")
+def test_random_layers_and_parameters(case):
+    """Seeded random small layers (length, block, GQA grouping, head mixture) under random
+    parameters (alpha, gamma, tau, anchor windows, k_min, scale, route and VS modes, floor)
+    through the whole path against the oracle, every head and query block."""
+    C = _crisp()
+    _say(f"random layer {case}")
+    cfg = custom_config(case["n"], case["hq"], case["hkv"], block=case["block"], config_id=case["config_id"],
+                        diffuse_frac=case["diffuse_frac"], structured_pe=case["structured_pe"])
+    _check_layer(C, cfg, C.make_params(**case["params"]), where=f"random{case['config_id']}")
+
+
 @pytest.mark.parametrize("n,hq,hkv,block", [(4000, 12, 3, 128), (3000, 10, 5, 64), (2500, 32, 16, 128)])
 def test_unusual_gqa_groupings(n, hq, hkv, block):
     """KV-group counts that do not divide 8 (the sparse kernel's queues then leave some XCDs
