@@ -201,6 +201,9 @@ crisp_status crisp_sparse_workspace_size(const crisp_shape* shape, size_t* bytes
  * J(i) = {j <= i : j / B in row (i / B) of head h's list}.  Accepts caller-built
  * lists; entries outside [0, qb] are ignored and row_ptr values are clamped to
  * [0, col_cap_per_head], so a malformed list cannot cause an out-of-bounds access.
+ * Rows are read as given: the order of a row's entries only changes floating-point
+ * rounding, and an entry listed twice counts its block twice (crisp_route_select
+ * writes every row ascending and unique; the debug build rejects other rows).
  * A row with no visible key gets o = 0.  softmax_scale 0 means 1/sqrt(d).
  * workspace_or_null (crisp_sparse_workspace_size bytes) holds a longest-first
  * work list that balances rows of very different lengths over the GPU and, for
