@@ -215,6 +215,46 @@ def test_split_rows(case):
         PR.compare_attention(to_f64(o1[h]), to_f64(o_fixed[h]), rows=rows, where=f"{case} h{h} vs fixed")
 
 
+def test_caller_lists_unordered_and_repeated_entries():
+    """crisp_sparse_attn reads rows as given: a row in another order gives the same output
+    up to rounding, and an entry listed twice counts its block twice (its keys' softmax
+    weights doubled), checked against a float64 statement of exactly that."""
+    C = _crisp()
+    _say("caller lists: unordered and repeated entries")
+    n, block, nb = 1024, 128, 8
+    q, k, v = _rand(1, n, seed=31), _rand(1, n, seed=32), _rand(1, n, seed=33)
+    rows = [sorted({0, qb, qb // 2, max(qb - 3, 0)}) for qb in range(nb)]
+    cap = nb * (nb + 1) // 2
+    def csr(rs):
+        rp = np.zeros((1, nb + 1), np.int32)
+        ci = np.zeros((1, cap), np.int32)
+        for qb, r in enumerate(rs):
+            rp[0, qb + 1] = rp[0, qb] + len(r)
+            ci[0, rp[0, qb]:rp[0, qb + 1]] = r
+        return torch.from_numpy(rp).to(DEV), torch.from_numpy(ci).to(DEV)
+    qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
+    o_sorted = to_f64(C.crisp_sparse_attn(qd, kd, vd, *csr(rows), block))[0]
+    rng = np.random.default_rng(7)
+    shuffled = [list(rng.permutation(r)) for r in rows]
+    o_shuf = to_f64(C.crisp_sparse_attn(qd, kd, vd, *csr(shuffled), block))[0]
+    assert np.abs(o_shuf - o_sorted).max() <= 1e-2 and np.abs(o_shuf - o_sorted).mean() <= 1e-3
+    doubled = [r + [r[0]] for r in rows]  # block 0 listed twice in every row
+    o_dup = to_f64(C.crisp_sparse_attn(qd, kd, vd, *csr(doubled), block))[0]
+    torch.cuda.synchronize()
+    Q, K, V = to_f64(q)[0], to_f64(k)[0], to_f64(v)[0]
+    ref = np.zeros((n, 128))
+    for i in range(n):
+        qb = i // block
+        mult = np.zeros(n)
+        for kb in doubled[qb]:
+            mult[kb * block:(kb + 1) * block] += 1.0
+        mult[i + 1:] = 0.0
+        sc = (K @ Q[i]) / math.sqrt(128)
+        w = mult * np.exp(sc - sc[mult > 0].max())
+        ref[i] = w @ V / w.sum()
+    PR.compare_attention(o_dup, ref, rows=np.arange(n), where="repeated entries")
+
+
 def test_attention_custom_scale_and_empty_rows():
     C = _crisp()
     _say("custom scale, empty rows")
