@@ -672,7 +672,11 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
     __syncthreads();
     const int item = *s_unit;
     if (item < 0) break;
-    const int unit = item & ((1 << kItemUnitBits) - 1), chunk = item >> kItemUnitBits;
+    // items carry a chunk index only when rows may be split (fewer than 2^21 units);
+    // otherwise an item is the unit itself, which may exceed 2^21
+    const bool split = a.split_slots > 0;
+    const int unit = split ? item & ((1 << kItemUnitBits) - 1) : item;
+    const int chunk = split ? item >> kItemUnitBits : 0;
     float* part = nullptr;
     if (a.split_slots > 0) {
       const int sb = a.slot_base[unit];

@@ -215,6 +215,41 @@ def test_split_rows(case):
         PR.compare_attention(to_f64(o1[h]), to_f64(o_fixed[h]), rows=rows, where=f"{case} h{h} vs fixed")
 
 
+def test_more_than_2p21_units():
+    """A layer with more (head, query block) units than a split work item can name
+    (2^21): 65 query heads over one KV head at the longest length with B = 64 (2,129,920
+    units, one unit per workgroup), each row listing only its diagonal block.  Sampled
+    rows of the first and the last head (whose units all lie past 2^21) against float64
+    attention over the visible keys of the diagonal block."""
+    C = _crisp()
+    _say("2^21+ units: 65 heads x 2^21 tokens, B = 64, diagonal lists")
+    n, block, hq = 1 << 21, 64, 65
+    nb = n // block
+    g = torch.Generator(device=DEV).manual_seed(5)
+    q = torch.randn(hq, n, 128, generator=g, device=DEV, dtype=torch.bfloat16)
+    k = torch.randn(1, n, 128, generator=g, device=DEV, dtype=torch.bfloat16)
+    v = torch.randn(1, n, 128, generator=g, device=DEV, dtype=torch.bfloat16)
+    rp = torch.arange(nb + 1, dtype=torch.int32, device=DEV).repeat(hq, 1)
+    ci = torch.arange(nb, dtype=torch.int32, device=DEV).repeat(hq, 1)
+    o = C.crisp_sparse_attn(q, k, v, rp, ci, block)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(11)
+    rows = [(h, int(i)) for h in (0, 64) for i in rng.integers(0, n, 40)] + [(64, n - 1), (64, 0), (0, n - 1)]
+    K, V = k[0], v[0]
+    for h, i in rows:
+        lo = (i // block) * block
+        qi = to_f64(q[h, i:i + 1])[0]
+        kk = to_f64(K[lo:i + 1])
+        vv = to_f64(V[lo:i + 1])
+        sc = kk @ qi / math.sqrt(128)
+        w = np.exp(sc - sc.max())
+        ref = w @ vv / w.sum()
+        got = to_f64(o[h, i:i + 1])[0]
+        assert np.abs(got - ref).max() <= PR.ATTN_MAX_ABS, f"head {h} row {i}: {np.abs(got - ref).max():.3e}"
+    del q, k, v, o
+    torch.cuda.empty_cache()
+
+
 def test_caller_lists_unordered_and_repeated_entries():
     """crisp_sparse_attn reads rows as given: a row in another order gives the same output
     up to rounding, and an entry listed twice counts its block twice (its keys' softmax
