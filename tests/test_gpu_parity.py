@@ -964,17 +964,19 @@ def test_golden_manifests_on_gpu():
         del q, k, v, o
 
 
-@pytest.mark.parametrize("layer", ["config0", "ragged-b64", "pe-8k-split-rows"])
+@pytest.mark.parametrize("layer", ["config0", "ragged-b64", "pe-8k-split-rows", "one-shot-512k"])
 def test_debug_build_race_check(layer):
     """The debug build's attention runs the same arithmetic with its tile pipeline
     serialised (each tile load waited for, a barrier after every LDS phase): its outputs
     equal the pipelined kernel's bit for bit, so the overlapped loads and reads of the
-    LDS rings never race.  Layers: the 4k tiny layer, a ragged B = 64 layer, and an 8k
-    layer whose long rows are split (persistent grid, partial results merged)."""
+    LDS rings never race.  Layers: the 4k tiny layer, a ragged B = 64 layer, an 8k
+    layer whose long rows are split (persistent grid, partial results merged), and a
+    512k layer (one unit per workgroup)."""
     C = _crisp()
     _say(f"debug race check {layer}")
     cfg, block = {"config0": (CONFIGS[0], 128), "ragged-b64": (custom_config(3001, 4, 2, block=64, config_id=154), 64),
-                  "pe-8k-split-rows": (structured_pe_config(8192), 128)}[layer]
+                  "pe-8k-split-rows": (structured_pe_config(8192), 128),
+                  "one-shot-512k": (custom_config(1 << 19, 2, 1, block=128, config_id=155), 128)}[layer]
     q, k, v, _ = make_layer(cfg, device=DEV)
     params = C.make_params(alpha=cfg.alpha)
     release = C.lib
