@@ -40,6 +40,7 @@
 // workgroup takes the next unit of the group lists in order (one KV group after
 // the other, longest first within a group), so units that start together
 // advance together over the same group's K/V.
+#include <atomic>
 #include <type_traits>
 
 #include "crisp_device.h"
@@ -904,19 +905,21 @@ hipError_t launch_t(const AttnArgs& a, int grid, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// Workgroups that fit on the device at once (persistent grid size).
+// Workgroups that fit on the device at once (persistent grid size), cached per
+// device; threads that race on the first call compute and store the same value.
 template <int BQ>
 int persistent_grid() {
-  static int cached[64] = {0};
+  static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
-  if (cached[dev] > 0) return cached[dev];
+  const int c = cached[dev].load(std::memory_order_relaxed);
+  if (c > 0) return c;
   int cus = 0, per = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) cus = 256;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, attn_kernel<BQ, false>, Geo<BQ>::kThreads, 0) != hipSuccess || per <= 0)
     per = 1;
-  cached[dev] = cus * per;
-  return cached[dev];
+  cached[dev].store(cus * per, std::memory_order_relaxed);
+  return cus * per;
 }
 
 }  // namespace

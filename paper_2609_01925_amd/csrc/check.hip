@@ -6,6 +6,8 @@
 // Each check clears a result word, runs one kernel that stores a nonzero code there
 // when it finds a violation, copies the word to the host and waits for the stream:
 // the debug build trades the library's asynchrony for a status it can return.
+#include <atomic>
+
 #include "crisp_device.h"
 #include "crisp_internal.h"
 
@@ -53,20 +55,21 @@ __global__ __launch_bounds__(256) void chk_lists(const int32_t* row_ptr, const i
 
 __device__ int g_found;
 
-// The result word's address on the current device (each device holds its own copy).
+// The result word's address on the current device (each device holds its own copy),
+// cached per device; threads that race on the first call store the same address.
 hipError_t result_word(int** p) {
   constexpr int kMaxDevices = 64;
-  static int* addr[kMaxDevices] = {};
+  static std::atomic<int*> addr[kMaxDevices];
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
-  if (!addr[dev]) {
-    int* a = nullptr;
+  int* a = addr[dev].load(std::memory_order_relaxed);
+  if (a == nullptr) {
     if ((e = hipGetSymbolAddress(reinterpret_cast<void**>(&a), HIP_SYMBOL(g_found))) != hipSuccess) return e;
-    addr[dev] = a;
+    addr[dev].store(a, std::memory_order_relaxed);
   }
-  *p = addr[dev];
+  *p = a;
   return hipSuccess;
 }
 
