@@ -37,19 +37,25 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--skip-512k", action="store_true")
     ap.add_argument("--skip-cpu", action="store_true")
-    ap.add_argument("--steps-512k", type=int, default=2)
-    ap.add_argument("--sweep", action="store_true",
-                    help="also run the length sweep 8k..512k on the paper-like structured-PE workload "
-                         "(CRISP, dense and FlexPrefill) and report the crossover with dense")
+    ap.add_argument("--steps-512k", type=int, default=7)
+    ap.add_argument("--skip-sweep", action="store_true",
+                    help="skip the length sweep 2k..512k on the paper-like structured-PE workload "
+                         "(CRISP, dense and FlexPrefill; locates the crossover with dense)")
+    ap.add_argument("--skip-configs", action="store_true",
+                    help="skip the per-config records of the 4k tiny layer, the 32k Llama layer and the six "
+                         "alpha x B cells of the 64k selection-stress layer")
+    ap.add_argument("--skip-peaks", action="store_true", help="skip the MFMA and copy peak microbenchmarks")
     ap.add_argument("--skip-comparators", action="store_true",
                     help="skip the FlexPrefill comparator, ablation and noise-floor variant timings")
     ap.add_argument("--config", type=int, default=2, help="headline config id (2 = 128k Llama GQA layer)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy, the reference for rocprofv3 byte counters")
     ap.add_argument("--summarize", metavar="ROCPROF_DIR",
-                    help="summarize rocprofv3 output under ROCPROF_DIR into profiles/ and exit (no GPU)")
-    ap.add_argument("--label", default="attn_128k", help="file stem for --summarize")
-    ap.add_argument("--command", default="", help="the profiling command, recorded by --summarize")
+                    help="summarize rocprofv3 output under ROCPROF_DIR (one sub-folder per rocprofv3 run) "
+                         "into profiles/ and exit (no GPU)")
+    ap.add_argument("--label", default="crisp_kernels_llama3_8b_128k", help="file stem for --summarize")
+    ap.add_argument("--command", action="append", default=[],
+                    help="a profiling command, recorded by --summarize (repeatable)")
     return ap.parse_args()
 
 
@@ -145,7 +151,7 @@ def layer_measure(cfg, steps, warmup, label):
         # event times give the median and spread
         "ms_per_layer": crisp["wall_per_step"], "ms_median": crisp["median"], "ms_p10": crisp["p10"],
         "ms_p90": crisp["p90"], "ms_p_min": crisp["min"], "ms_p_max": crisp["max"],
-        "dense_ms_per_layer": dense["wall_per_step"],
+        "dense_ms_per_layer": dense["wall_per_step"], "dense_ms_median": dense["median"],
         "speedup_vs_dense": dense["wall_per_step"] / crisp["wall_per_step"],
         "stage_ms": {"estimate": est["mean"], "route_select": sel["mean"], "sparse_attn": att["mean"]},
         "routes": {"vs": n_vs, "pe": cfg.n_q_heads - n_vs},
@@ -168,6 +174,19 @@ def layer_measure(cfg, steps, warmup, label):
     res["_attn_flop"] = attn_flop
     res["_tensors"] = (q, k, v, specs, route_c, rp.cpu(), ci.cpu(), pairs_per_head)
     return res
+
+
+def add_measured_fracs(res, peaks):
+    """Adds each roofline fraction against the rates measured on this GPU beside the one
+    against the published peak."""
+    if not peaks:
+        return
+    m, c = peaks["mfma_bf16_tflops"], peaks["copy_gbs"]
+    res["sparse_attn_frac_of_measured_mfma"] = res["sparse_attn_tflops_executed"] / m
+    res["dense_frac_of_measured_mfma"] = res["dense_tflops_executed"] / m
+    res["estimate_frac_of_measured_mfma"] = res["estimate_tflops"] / m
+    res["estimate_frac_of_measured_copy"] = res["estimate_hbm_gbs"] / c
+    res["select_frac_of_measured_copy"] = res["select_hbm_gbs"] / c
 
 
 def comparator_measure(cfg, res, steps, warmup, label, mixes=True):
@@ -238,7 +257,7 @@ def floor_variants_measure(cfg, res, steps, warmup, label):
     return out
 
 
-def pe_sweep_measure():
+def pe_sweep_measure(peaks=None):
     """Length sweep on the structured-PE workload (the regime of the paper's latency table):
     CRISP, the dense baseline and the FlexPrefill comparator at each length, and the shortest
     length at which CRISP beats dense (the context-length gate's threshold)."""
@@ -248,24 +267,32 @@ def pe_sweep_measure():
     rows = []
     for n in sorted(PE_SWEEP_LENGTHS):
         cfg = structured_pe_config(n)
-        steps = 5 if n <= 131072 else 2
-        res = layer_measure(cfg, steps, 1, f"sweep {n // 1024}k")
-        fp = comparator_measure(cfg, res, steps, 1, f"sweep {n // 1024}k", mixes=False)["flexprefill"]
+        steps, warmup = (10, 3) if n <= 131072 else (3, 1)
+        res = layer_measure(cfg, steps, warmup, f"sweep {n // 1024}k")
+        fp = comparator_measure(cfg, res, steps, warmup, f"sweep {n // 1024}k", mixes=False)["flexprefill"]
         rows.append({"seq_len": n, "workload": cfg.name, "crisp_ms": res["ms_per_layer"],
                      "dense_ms": res["dense_ms_per_layer"], "speedup_vs_dense": res["speedup_vs_dense"],
+                     "crisp_ms_event_median": res["ms_median"], "dense_ms_event_median": res["dense_ms_median"],
                      "density": res["density"], "routes": res["routes"], "stage_ms": res["stage_ms"],
                      "flexprefill_ms": fp["ms_per_layer"], "flexprefill_density": fp["density"],
                      "crisp_speedup_vs_flexprefill": fp["crisp_speedup_vs_this"],
-                     "sparse_attn_mfma_frac": res["sparse_attn_mfma_frac"]})
+                     "sparse_attn_mfma_frac": res["sparse_attn_mfma_frac"],
+                     "sparse_attn_frac_of_measured_mfma": (res["sparse_attn_tflops_executed"] / peaks["mfma_bf16_tflops"]
+                                                           if peaks else None)})
         del res
         torch.cuda.empty_cache()
     faster = [r["seq_len"] for r in rows if r["crisp_ms"] < r["dense_ms"]]
-    return {"rows": rows, "crisp_beats_dense_from": min(faster) if faster else None}
+    faster_ev = [r["seq_len"] for r in rows if r["crisp_ms_event_median"] < r["dense_ms_event_median"]]
+    return {"rows": rows, "crisp_beats_dense_from": min(faster) if faster else None,
+            "crisp_beats_dense_from_event_median": min(faster_ev) if faster_ev else None}
 
 
-def cpu_baseline(cfg, res, budget_s=25.0):
-    """The oracle, as it stands, on the host cores: estimate + route/select for every head,
-    attention on a sample of (head, query block) units, extrapolated to ms per layer."""
+def cpu_baseline(cfg, res, budget_s=25.0, full=False):
+    """The oracle, as it stands, on the host cores: estimate + route/select for every head
+    (or as many as fit 60% of the budget, scaled to all heads), attention on a sample of
+    (head, query block) units, extrapolated to ms per layer by the oracle's own executed
+    block pairs.  full=True runs and times the oracle on every head and query block (no
+    extrapolation; for layers the oracle finishes in seconds)."""
     import numpy as np
     import torch
     from oracle import crisp_oracle as O
@@ -296,7 +323,7 @@ def cpu_baseline(cfg, res, budget_s=25.0):
         pairs_total_h = sum(len(s) for s in r.sets)
         pairs_total += pairs_total_h
         heads_done += 1
-        if time.perf_counter() - t0 > budget_s * 0.6 and heads_done >= 2:
+        if not full and time.perf_counter() - t0 > budget_s * 0.6 and heads_done >= 2:
             break
     # extrapolate selection to all heads by the measured mean
     sel_ms_layer = sel_time / heads_done * cfg.n_q_heads * 1e3
@@ -305,6 +332,20 @@ def cpu_baseline(cfg, res, budget_s=25.0):
     att_time, att_pairs, units = 0.0, 0, 0
     rng = np.random.default_rng(0)
     hs = list(sets.keys())
+    if full:
+        for h in hs:
+            Qh, s = sets[h]
+            t = time.perf_counter()
+            O.sparse_attention(Qh, Kc[h // G], Vc[h // G], s, block, op.scale(128))
+            att_time += time.perf_counter() - t
+            att_pairs += sum(len(x) for x in s)
+            units += nb
+        total = (sel_time + att_time) * 1e3
+        return {"value": total, "unit": "ms/layer", "cores": cores, "kind": "oracle",
+                "sample": (f"{cfg.name}: the whole oracle (estimate, route, select and attention) on every head "
+                           f"and query block ({cfg.n_q_heads} heads, {units} units, {att_pairs} block pairs); "
+                           f"float64 numpy, {cores} BLAS threads of {len(os.sched_getaffinity(0))} host cores"),
+                "measured_s": time.perf_counter() - t0}
     while time.perf_counter() - t0 < budget_s and units < 512:
         h = hs[units % len(hs)]
         Qh, s = sets[h]
@@ -326,10 +367,86 @@ def cpu_baseline(cfg, res, budget_s=25.0):
     }
 
 
-def attn_traffic(kernel_src_hash, label="sparse_attn_128k_pmc"):
-    """HBM bytes (fetch + write) per launch of the sparse attention kernel from the committed
-    rocprofv3 counter summary, if it was taken on the current attention kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", label + ".md")
+def measured_peaks():
+    """The rates this GPU sustains, beside the published peaks: bf16 MFMA from a register-only
+    loop of independent v_mfma_f32_32x32x16_bf16 (2048 workgroups, the chip's clock under
+    MFMA load) and HBM bandwidth from a plain 1 GiB device copy (16-byte loads and stores;
+    read plus written bytes).  Both kernels are in libcrisp_peaks.so."""
+    import ctypes
+    import torch
+    path = os.path.join(ROOT, "paper_2609_01925_amd", "libcrisp_peaks.so")
+    lib = ctypes.CDLL(path)
+    lib.crisp_peak_mfma_flop.restype = ctypes.c_double
+    lib.crisp_peak_mfma_flop.argtypes = [ctypes.c_int, ctypes.c_int]
+    lib.crisp_peak_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    lib.crisp_peak_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p]
+    dev = "cuda:0"
+    stream = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    wg, iters = 2048, 20000
+    out = torch.empty(wg * 256, dtype=torch.float32, device=dev)
+
+    def mfma():
+        assert lib.crisp_peak_mfma_bf16(wg, iters, ctypes.c_void_p(out.data_ptr()), stream) == 0
+
+    t_mfma = time_events(mfma, 10, 3)
+    mfma_tflops = lib.crisp_peak_mfma_flop(wg, iters) / (t_mfma["median"] * 1e-3) / 1e12
+    nbytes = 1 << 30
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+
+    def copy():
+        assert lib.crisp_peak_copy(ctypes.c_void_p(src.data_ptr()), ctypes.c_void_p(dst.data_ptr()), nbytes,
+                                   8192, stream) == 0
+
+    t_copy = time_events(copy, 10, 3)
+    torch.cuda.synchronize()
+    assert bool(torch.equal(src, dst))
+    copy_gbs = 2.0 * nbytes / (t_copy["median"] * 1e-3) / 1e9
+    del src, dst, out
+    torch.cuda.empty_cache()
+    log(f"peaks: bf16 MFMA {mfma_tflops:.0f} TFLOP/s, copy {copy_gbs:.0f} GB/s")
+    return {"mfma_bf16_tflops": mfma_tflops, "mfma_bf16_published_tflops": MFMA_BF16_PEAK_TFLOPS,
+            "copy_gbs": copy_gbs, "hbm_published_gbs": HBM_PEAK_GBS,
+            "method": ("MFMA: 2048 workgroups x 4 waves, 4 independent v_mfma_f32_32x32x16_bf16 chains per wave, "
+                       f"{iters} rounds, median of 10 launches; copy: 1 GiB device to device, 16-byte "
+                       "loads and stores, read + written bytes, median of 10 launches")}
+
+
+def config_records(steps, warmup, skip_cpu, peaks):
+    """Per-config records of the smaller layers: the 4k tiny layer, the 32k Llama-3-8B layer and
+    the six alpha x B cells of the 64k selection-stress layer, each timed like the headline
+    (CRISP end to end, stages, dense), with the oracle beside it: the whole oracle on the 4k
+    layer, a bounded sample elsewhere."""
+    import torch
+    from workloads import CONFIGS, STRESS_ALPHAS, STRESS_BLOCKS, stress_config
+    layers = [("c0", CONFIGS[0], 0.0, True), ("c1", CONFIGS[1], 12.0, False)]
+    layers += [(f"c4_a{a:g}_b{b}", stress_config(a, b), 4.0, False) for a in STRESS_ALPHAS for b in STRESS_BLOCKS]
+    out = {}
+    for key, cfg, budget, full in layers:
+        r = layer_measure(cfg, steps, warmup, key)
+        rec = {k_: v_ for k_, v_ in r.items() if not k_.startswith("_")}
+        if peaks:
+            rec["sparse_attn_frac_of_measured_mfma"] = (r["_attn_flop"] / (r["_attn_launch_ms"] * 1e-3) / 1e12
+                                                        / peaks["mfma_bf16_tflops"])
+        if not skip_cpu:
+            rec["cpu_baseline"] = cpu_baseline(cfg, r, budget_s=budget, full=full)
+            log(f"{key}: oracle {rec['cpu_baseline']['value']:.0f} ms/layer "
+                f"({rec['cpu_baseline']['measured_s']:.1f}s)")
+        out[key] = rec
+        del r
+        torch.cuda.empty_cache()
+    return out
+
+
+def profile_path(workload):
+    return os.path.join(ROOT, "profiles", f"crisp_kernels_{workload}.md")
+
+
+def attn_traffic(kernel_src_hash, workload):
+    """HBM bytes (fetch + write) per launch of the sparse attention kernel on `workload`, from the
+    committed rocprofv3 counter summary, if it was taken on the current attention kernel source;
+    else None."""
+    path = profile_path(workload)
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -338,9 +455,9 @@ def attn_traffic(kernel_src_hash, label="sparse_attn_128k_pmc"):
     for line in text.splitlines():
         if "PMC_RECORD " in line:
             rec = json.loads(line.split("PMC_RECORD ", 1)[1].rstrip("`"))
-            f_, w_ = rec.get("sparse_attn_FETCH_SIZE_bytes"), rec.get("sparse_attn_WRITE_SIZE_bytes")
-            if f_ is not None and w_ is not None:
-                return f_ + w_
+            k = rec.get("kernels", {}).get("attn_kernel<128, false>", {})
+            if k.get("FETCH_bytes") is not None and k.get("WRITE_bytes") is not None:
+                return k["FETCH_bytes"] + k["WRITE_bytes"]
     return None
 
 
@@ -348,69 +465,134 @@ COPY_BYTES = 1 << 30
 
 
 def copy_calibration():
-    """A plain device-to-device copy of COPY_BYTES: its FETCH_SIZE / WRITE_SIZE give the
-    scale from counter units to bytes."""
+    """A plain device copy of COPY_BYTES (libcrisp_peaks.so's peak_copy): its FETCH_SIZE /
+    WRITE_SIZE give the scale from counter units to bytes."""
+    import ctypes
     import torch
-    x = torch.empty(COPY_BYTES // 4, dtype=torch.float32, device="cuda:0").fill_(1.0)
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_01925_amd", "libcrisp_peaks.so"))
+    lib.crisp_peak_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p]
+    x = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda:0")
     y = torch.empty_like(x)
     torch.cuda.synchronize()
-    torch.mul(x, 2.0, out=y)   # one elementwise kernel: reads and writes COPY_BYTES
+    assert lib.crisp_peak_copy(ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(y.data_ptr()), COPY_BYTES, 8192,
+                               ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)) == 0
     torch.cuda.synchronize()
     del x, y
 
 
+def _short_kernel(name):
+    """'void crisp::(anonymous namespace)::attn_kernel<128, false>(crisp::...)' -> 'attn_kernel<128, false>'."""
+    import re
+    for pre in ("void ", "crisp::(anonymous namespace)::", "(anonymous namespace)::", "crisp::"):
+        name = name.replace(pre, "")
+    depth = 0
+    for i, ch in enumerate(name):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            name = name[:i]
+            break
+    return re.sub(r"\s+", " ", name).strip()
+
+
 def summarize(args):
-    """Turns rocprofv3 csv output (kernel trace stats or counter collection) into a short
-    markdown summary under profiles/."""
+    """Turns rocprofv3 csv output into a short markdown summary under profiles/: the kernel
+    trace statistics, and per kernel the median per dispatch of every counter collected
+    (one rocprofv3 run per counter set), with the derived figures: HBM bytes read and
+    written (FETCH_SIZE / WRITE_SIZE scaled by what they read for a plain copy of known
+    size), bf16 and fp32 MFMA work (MOPS x 512 FLOP), MFMA and LDS utilisation
+    (rocprofv3's MfmaUtil, LdsUtil), the L2 hit rate, the counter-run dispatch duration and
+    the clock (GRBM_GUI_ACTIVE per XCD over that duration)."""
     import csv
     import glob
     import statistics
     root = args.summarize
-    out = []
-    out.append(f"# {args.label}\n")
-    out.append(f"Command: `{args.command}`\n")
-    out.append(f"attn.hip sha256[:16]: {src_hash(os.path.join(ROOT, 'paper_2609_01925_amd', 'csrc', 'attn.hip'))}\n")
+    out = [f"# {args.label}\n\n"]
+    out.append("Commands (rocprofv3 runs of committed files; `<out>` is the output folder):\n\n")
+    for c in args.command:
+        out.append(f"* `{c}`\n")
+    out.append("\nSource hashes:\n\n")
+    csrc = os.path.join(ROOT, "paper_2609_01925_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith(".hip"):
+            out.append(f"* {f} sha256[:16]: {src_hash(os.path.join(csrc, f))}\n")
     stats = sorted(glob.glob(os.path.join(root, "**", "*kernel_stats.csv"), recursive=True))
     if stats:
-        out.append("\n## Kernel time (rocprofv3 --kernel-trace --stats)\n")
+        out.append("\n## Kernel time (rocprofv3 --kernel-trace --stats)\n\n")
         out.append("| kernel | calls | avg us | min us | max us | total ms |\n|---|---|---|---|---|---|\n")
         for r in csv.DictReader(open(stats[0])):
-            name = r["Name"]
-            if "crisp" not in name:
+            if "crisp" not in r["Name"]:
                 continue
-            short = name.replace("crisp::(anonymous namespace)::", "").replace("void ", "").split("(")[0]
-            out.append(f"| {short} | {r['Calls']} | {float(r['AverageNs'])/1e3:.1f} | {float(r['MinNs'])/1e3:.1f} | "
-                       f"{float(r['MaxNs'])/1e3:.1f} | {float(r['TotalDurationNs'])/1e6:.2f} |\n")
-    pmc = sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True))
-    if pmc:
-        per = {}
-        for path in pmc:
-            for r in csv.DictReader(open(path)):
-                name = r["Kernel_Name"]
-                key = ("sparse_attn" if "attn_kernel<128, false>" in name else
-                       "dense_attn" if "attn_kernel<128, true>" in name else
-                       "copy" if "MulFunctor" in name and int(r["Grid_Size"]) >= (COPY_BYTES // 64) else None)
-                if key is None:
-                    continue
-                per.setdefault((key, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
-        out.append("\n## Counters per dispatch (rocprofv3 --pmc), median over dispatches\n")
-        out.append("| kernel | counter | value (KiB) | dispatches |\n|---|---|---|---|\n")
-        med = {}
-        for (k, c), vals in sorted(per.items()):
-            med[(k, c)] = statistics.median(vals)
-            out.append(f"| {k} | {c} | {med[(k, c)]:.1f} | {len(vals)} |\n")
-        rec = {}
+            out.append(f"| {_short_kernel(r['Name'])} | {r['Calls']} | {float(r['AverageNs'])/1e3:.1f} | "
+                       f"{float(r['MinNs'])/1e3:.1f} | {float(r['MaxNs'])/1e3:.1f} | "
+                       f"{float(r['TotalDurationNs'])/1e6:.2f} |\n")
+    per, dur = {}, {}
+    for path in sorted(glob.glob(os.path.join(root, "**", "*counter_collection.csv"), recursive=True)):
+        for r in csv.DictReader(open(path)):
+            name = r["Kernel_Name"]
+            if "crisp" in name:
+                key = _short_kernel(name)
+            elif "peak_copy" in name:
+                key = "copy (1 GiB calibration)"
+            else:
+                continue
+            per.setdefault((key, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
+            d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9
+            dur.setdefault((key, r["Counter_Name"]), []).append(d)
+    rec = {"kernels": {}}
+    if per:
+        med = {k: statistics.median(v) for k, v in per.items()}
+        kernels = sorted({k for k, _ in per})
+        counters = sorted({c for _, c in per})
+        scale = {}
         for c, known in (("FETCH_SIZE", COPY_BYTES), ("WRITE_SIZE", COPY_BYTES)):
-            if ("copy", c) in med and med[("copy", c)] > 0:
-                scale = known / med[("copy", c)]
-                rec[c + "_bytes_per_unit"] = scale
-                for k in ("sparse_attn", "dense_attn"):
-                    if (k, c) in med:
-                        rec[f"{k}_{c}_bytes"] = med[(k, c)] * scale
-        if rec:
-            out.append("\nScale: a plain copy of %d bytes reads/writes that many bytes; counter units -> bytes:\n" % COPY_BYTES)
-            out.append("\n```\n" + json.dumps(rec, indent=1) + "\n```\n")
-            out.append("\nMachine-readable: `PMC_RECORD " + json.dumps(rec) + "`\n")
+            cal = med.get(("copy (1 GiB calibration)", c))
+            if cal:
+                scale[c] = known / cal
+                rec[c + "_bytes_per_unit"] = scale[c]
+        out.append("\n## Counters per dispatch (rocprofv3 --pmc), median over dispatches\n\n")
+        out.append("| kernel | " + " | ".join(counters) + " | dispatches |\n")
+        out.append("|---" * (len(counters) + 2) + "|\n")
+        for k in kernels:
+            n_disp = max(len(per.get((k, c), [])) for c in counters)
+            cells = [f"{med[(k, c)]:.6g}" if (k, c) in med else "" for c in counters]
+            out.append(f"| {k} | " + " | ".join(cells) + f" | {n_disp} |\n")
+        out.append("\n## Derived per dispatch\n\n")
+        out.append("| kernel | counter-run ms | HBM read GB | HBM written GB | bf16 MFMA TFLOP | fp32 MFMA TFLOP "
+                   "| MfmaUtil % | LdsUtil % | L2 hit % | clock GHz |\n|---|---|---|---|---|---|---|---|---|---|\n")
+        for k in kernels:
+            d = {}
+            dms = [statistics.median(v) for (kk, c), v in dur.items() if kk == k]
+            if dms:
+                d["counter_run_ms"] = statistics.median(dms) * 1e3
+            if ("FETCH_SIZE" in scale) and (k, "FETCH_SIZE") in med:
+                d["FETCH_bytes"] = med[(k, "FETCH_SIZE")] * scale["FETCH_SIZE"]
+            if ("WRITE_SIZE" in scale) and (k, "WRITE_SIZE") in med:
+                d["WRITE_bytes"] = med[(k, "WRITE_SIZE")] * scale["WRITE_SIZE"]
+            for c, key in (("SQ_INSTS_VALU_MFMA_MOPS_BF16", "bf16_mfma_flop"), ("SQ_INSTS_VALU_MFMA_MOPS_F32",
+                                                                                  "f32_mfma_flop")):
+                if (k, c) in med:
+                    d[key] = med[(k, c)] * 512.0
+            for c in ("MfmaUtil", "LdsUtil"):
+                if (k, c) in med:
+                    d[c] = med[(k, c)]
+            if (k, "TCC_HIT_sum") in med and (k, "TCC_MISS_sum") in med:
+                tot = med[(k, "TCC_HIT_sum")] + med[(k, "TCC_MISS_sum")]
+                d["L2_hit"] = med[(k, "TCC_HIT_sum")] / tot if tot else None
+            if (k, "GRBM_GUI_ACTIVE") in med and (k, "GRBM_GUI_ACTIVE") in dur:
+                d["clock_ghz"] = med[(k, "GRBM_GUI_ACTIVE")] / 8.0 / statistics.median(dur[(k, "GRBM_GUI_ACTIVE")]) / 1e9
+            rec["kernels"][k] = d
+            f = lambda key, sc=1.0, fmt="{:.3g}": fmt.format(d[key] / sc) if d.get(key) is not None else ""
+            out.append(f"| {k} | {f('counter_run_ms')} | {f('FETCH_bytes', 1e9)} | {f('WRITE_bytes', 1e9)} | "
+                       f"{f('bf16_mfma_flop', 1e12)} | {f('f32_mfma_flop', 1e12)} | {f('MfmaUtil')} | {f('LdsUtil')} | "
+                       f"{f('L2_hit', 0.01)} | {f('clock_ghz')} |\n")
+        out.append("\nMfmaUtil = 100 * (sum of SQ_VALU_MFMA_BUSY_CYCLES) / (GRBM_GUI_ACTIVE * SIMD count), "
+                   "rocprofv3's own derived metric; clock = GRBM_GUI_ACTIVE / 8 XCDs / dispatch duration "
+                   "in the counter run (counter runs serialise dispatches, so their durations are close to, "
+                   "not equal to, the trace's).\n")
+    out.append("\nMachine-readable: `PMC_RECORD " + json.dumps(rec) + "`\n")
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
     dst = os.path.join(ROOT, "profiles", args.label + ".md")
     with open(dst, "w") as f:
@@ -434,6 +616,7 @@ def main():
     cfg = CONFIGS[args.config]
     if args.copy_calibration:
         copy_calibration()
+    peaks = None if args.skip_peaks else measured_peaks()
     res = layer_measure(cfg, args.steps, args.warmup, "headline")
     if not args.skip_comparators:
         res["comparators"] = comparator_measure(cfg, res, args.steps, args.warmup, "headline")
@@ -443,22 +626,40 @@ def main():
     roofline = {
         "bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
         "frac": achieved / MFMA_BF16_PEAK_TFLOPS,
-        "traffic": attn_traffic(attn_src) if cfg.config_id == 2 else None,
+        "traffic": attn_traffic(attn_src, cfg.name) if cfg.config_id in (2, 3) else None,
         "kernel": "attn_kernel<128,false> (crisp_sparse_attn)",
         "flop_per_launch": res["_attn_flop"], "launch_ms": res["_attn_launch_ms"],
     }
+    if peaks:
+        roofline["measured_peak"] = peaks["mfma_bf16_tflops"]
+        roofline["frac_of_measured_peak"] = achieved / peaks["mfma_bf16_tflops"]
+    for r_ in (res,):
+        add_measured_fracs(r_, peaks)
     extra = {}
     if not args.skip_512k and args.config != 3:
         try:
             r3 = layer_measure(CONFIGS[3], args.steps_512k, 1, "512k")
             if not args.skip_comparators:
                 r3["comparators"] = comparator_measure(CONFIGS[3], r3, args.steps_512k, 1, "512k", mixes=False)
+            add_measured_fracs(r3, peaks)
             extra = {k_: v_ for k_, v_ in r3.items() if not k_.startswith("_")}
+            extra["sparse_attn_traffic_bytes"] = attn_traffic(attn_src, CONFIGS[3].name)
             del r3
             torch.cuda.empty_cache()
         except Exception as e:  # noqa: BLE001 -- the headline line must still be printed
             extra = {"error": repr(e)}
-    sweep = pe_sweep_measure() if args.sweep else None
+    configs = None
+    if not args.skip_configs:
+        try:
+            configs = config_records(args.steps, args.warmup, args.skip_cpu, peaks)
+        except Exception as e:  # noqa: BLE001
+            configs = {"error": repr(e)}
+    sweep = None
+    if not args.skip_sweep:
+        try:
+            sweep = pe_sweep_measure(peaks)
+        except Exception as e:  # noqa: BLE001
+            sweep = {"error": repr(e)}
     cpu = None
     if not args.skip_cpu:
         cpu = cpu_baseline(cfg, res)
@@ -483,8 +684,13 @@ def main():
         "dense_ms_per_layer": res["dense_ms_per_layer"],
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "measured_peaks": peaks,
         "headline_detail": headline,
         "at_512k": extra,
+        "per_config": configs,
+        "src_sha": {f: src_hash(os.path.join(ROOT, "paper_2609_01925_amd", "csrc", f))
+                    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2609_01925_amd", "csrc")))
+                    if f.endswith((".hip", ".cpp", ".h"))},
         "attn_src_sha": attn_src,
     }
     if sweep is not None:

@@ -4,11 +4,14 @@ TEST INFRASTRUCTURE ONLY.  Only tests/, __graft_entry__.smoke() and bench.py's
 cpu_baseline leg may import this module.  The HIP path never calls it, shares no
 code with it, and nothing here reads anything the HIP path produced.
 
-Arithmetic is float64 on the exact float values of the bf16 inputs.  Every
-floating-point comparison that decides an integer result (route, VS block
-membership, PE order and cutoff) is taken in float32, the precision of the GPU
-kernels, on the float64 results rounded once to float32; the GPU side takes the
-same decisions in float32 on its own values.  Where the paper is silent or
+Arithmetic is float64 on the exact float values of the bf16 inputs; every
+long reduction (softmax denominators, C_struct, the directional scores, the
+noise-floor residual and mean, the pooled-score normalisation and the
+gamma cumulative sum) is a float64 sum.  Every floating-point comparison that
+decides an integer result (route, VS block membership, PE order and cutoff) is
+taken in float32, the precision of the GPU kernels, on the float64 results
+rounded once to float32; the GPU side takes the same decisions in float32 on
+its own values.  Where the paper is silent or
 ambiguous, the reading taken is named in the function's docstring (the readings
 are listed with their reasons in the design notes).
 
@@ -135,29 +138,34 @@ def vs_scores(ahat: np.ndarray, n: int, block: int):
 
 def vs_floor(p: np.ndarray, alpha: float, floor: str = "mean"):
     """r_d = max(1 - p_d[0] - p_d[N_b-1], 0), mu_d = r_d / (N_b - 2), threshold alpha * mu_d
-    (Alg. 3; noise-floor equation, Sec. 4.3).  Evaluated in float32 as
-    ((1 - p[0]) - p[N_b-1]), then / (N_b - 2), then * alpha.  Needs N_b > 2.
+    (Alg. 3; noise-floor equation, Sec. 4.3).  r_d, mu_d and alpha * mu_d are float64,
+    r_d evaluated as printed, ((1 - p[0]) - p[N_b-1]).  For the score vectors of
+    vs_scores, which sum to 1, r_d is the mass of the inner blocks p[1 .. N_b-2] up to
+    float64 rounding (reading R20; crisp_head checks it).  Needs N_b > 2.
 
     floor="median" is App. H's robust variant: mu_d is the median of the N_b - 2
     non-anchor block scores p_d[1 .. N_b-2] (reading R29: for an even count the
-    mean of the two middle values, in float32)."""
+    mean of the two middle values, in float32).
+    Returns (r_d, mu_d, threshold); the median variant returns float32 mu and threshold."""
     nb = len(p)
-    p32 = np.asarray(p, dtype=np.float32)
-    r = np.maximum((np.float32(1.0) - p32[0]) - p32[nb - 1], np.float32(0.0))
+    p64 = np.asarray(p, dtype=np.float64)
+    r = max((1.0 - p64[0]) - p64[nb - 1], 0.0)
     if floor == "median":
+        p32 = np.asarray(p, dtype=np.float32)
         mid = np.sort(p32[1:nb - 1])
         m = len(mid)
         mu = mid[m // 2] if m % 2 else (mid[m // 2 - 1] + mid[m // 2]) * np.float32(0.5)
-    else:
-        mu = r / np.float32(nb - 2)
-    return r, mu, np.float32(alpha) * mu
+        return r, mu, np.float32(alpha) * mu
+    mu = r / (nb - 2)
+    return r, mu, float(alpha) * mu
 
 
 def vs_select(p: np.ndarray, alpha: float, k_min: int, floor: str = "mean") -> List[int]:
     """S_d = top-k_d(p_d) with k_d = clip(|{J : p_d[J] > alpha mu_d}|, k_min, N_b) (Alg. 3).
 
-    Readings: the floor test is strict (>); k_min is in blocks; top-k orders
-    by (p desc, block index asc).  With N_b <= 2 the forced blocks already
+    Readings: the floor test is strict (>), taken in float32 between the block
+    score and the float64 threshold, each rounded once; k_min is in blocks;
+    top-k orders by (float32 p desc, block index asc).  With N_b <= 2 the forced blocks already
     cover every causal pair, so the direction selects nothing extra.
     Returns the selected block indices, ascending.
     """
@@ -166,7 +174,7 @@ def vs_select(p: np.ndarray, alpha: float, k_min: int, floor: str = "mean") -> L
         return []
     p32 = np.asarray(p, dtype=np.float32)
     _, _, thr = vs_floor(p, alpha, floor)
-    c = int(np.count_nonzero(p32 > thr))
+    c = int(np.count_nonzero(p32 > np.float32(thr)))
     kd = min(max(c, k_min), nb)
     order = sorted(range(nb), key=lambda J: (-float(p32[J]), J))
     return sorted(order[:kd])
@@ -397,6 +405,9 @@ def crisp_head(q: np.ndarray, k: np.ndarray, v: Optional[np.ndarray], block: int
             res.S_v = vs_select_gamma(p_v, params.gamma, km)
             res.S_s = vs_select_gamma(p_s, params.gamma, km)
         else:
+            for p in (p_v, p_s):   # R20: the residual is the inner-block mass
+                if nb > 2:
+                    assert abs(vs_floor(p, params.alpha)[0] - p[1:nb - 1].sum()) <= 1e-6
             res.S_v = vs_select(p_v, params.alpha, km, params.floor_mode)
             res.S_s = vs_select(p_s, params.alpha, km, params.floor_mode)
         res.sets = vs_block_sets(res.S_v, res.S_s, nb)

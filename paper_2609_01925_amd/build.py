@@ -22,6 +22,10 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libcrisp.so")
 LIB_DEBUG = os.path.join(PKG, "libcrisp_debug.so")  # CRISP_DEBUG: device-side input checks
+# measurement only: MFMA and copy peak-rate microbenchmarks that the benchmark reports
+# beside the published peaks (not part of the CRISP path)
+PEAKS_SRC = os.path.join(PKG, "peaks", "peaks.hip")
+LIB_PEAKS = os.path.join(PKG, "libcrisp_peaks.so")
 ARCH = "gfx950"
 
 # Packed fp32 VALU forms are kept out of every kernel: the compiler would
@@ -73,9 +77,11 @@ def build(verbose: bool = False) -> str:
                    "-o", os.path.join(BUILD, f[:-4] + "_debug.o")] for f in cpp]
     debug_jobs.append([cc, f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS, *EXTRA.get("attn.hip", []),
                        "-DCRISP_DEBUG=1", "-c", os.path.join(CSRC, "attn.hip"), "-o", os.path.join(BUILD, "attn_debug.o")])
-    workers = min(len(jobs) + len(debug_jobs), max(1, min(8, os.cpu_count() or 1)))
+    peaks_job = [cc, f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS, "-c", PEAKS_SRC,
+                 "-o", os.path.join(BUILD, "peaks.o")]
+    workers = min(len(jobs) + len(debug_jobs) + 1, max(1, min(8, os.cpu_count() or 1)))
     with cf.ThreadPoolExecutor(workers) as ex:
-        results = list(ex.map(_run, jobs + debug_jobs))
+        results = list(ex.map(_run, jobs + debug_jobs + [peaks_job]))
     bad = [(cmd, out) for rc, cmd, out in results if rc != 0]
     if verbose or bad:
         for rc, cmd, out in results:
@@ -86,7 +92,7 @@ def build(verbose: bool = False) -> str:
     objs = [j[-1] for j in jobs]
     replaced = {f[:-4] + ".o" for f in cpp} | {"attn.o"}
     debug_objs = [o for o in objs if os.path.basename(o) not in replaced] + [j[-1] for j in debug_jobs]
-    for target, members in ((LIB, objs), (LIB_DEBUG, debug_objs)):
+    for target, members in ((LIB, objs), (LIB_DEBUG, debug_objs), (LIB_PEAKS, [peaks_job[-1]])):
         tmp = target + ".tmp"
         rc, cmd, out = _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *members, "-o", tmp])
         if rc != 0:

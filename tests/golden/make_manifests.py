@@ -4,9 +4,11 @@ layers, computed by the oracle alone (this script imports only oracle/ and workl
 Each record names the generator version and the layer, and per head gives the quantities
 that decide the path: C_struct (the structural mass of Sec. 3.2), the proxy's sink mass
 (keys 0..3, the planted sink tag), the route (Alg. 2), the VS selections' sizes k_v and
-k_s (Alg. 3), the PE cutoff K* (Alg. 4), the executed block pairs and their density over
-the causal pairs, and, where the attention is run, the mean and the largest magnitude of
-the head's output (Eq. of Sec. 3.1 over the selected blocks).  Inputs are drawn by the
+k_s and, for VS heads, the block scores p_v, p_s and the selected blocks S_v, S_s of
+each direction (Alg. 3 with the noise floor of Sec. 4.3), the PE cutoff K* (Alg. 4), the
+executed block pairs and their density over the causal pairs, and, where the attention
+is run, the mean and the largest magnitude of the head's output (Eq. 1 over the
+selected blocks).  Inputs are drawn by the
 generator on the CPU (the generator's stream depends on the device), only the listed
 heads being filled.  A later change of the generator or of the oracle's arithmetic shows
 up as a difference against this file.
@@ -56,6 +58,11 @@ def head_record(q, k, v, block, params, attend):
         "pairs": int(pairs),
         "density": pairs / (nb * (nb + 1) / 2),
     }
+    if r.route == O.ROUTE_VS:
+        rec["p_v"] = [float(x) for x in r.p_v]
+        rec["p_s"] = [float(x) for x in r.p_s]
+        rec["S_v"] = [int(J) for J in r.S_v]
+        rec["S_s"] = [int(J) for J in r.S_s]
     if attend:
         rec["out_mean"] = float(r.out.mean())
         rec["out_max_abs"] = float(np.abs(r.out).max())

@@ -1,13 +1,19 @@
 """Generator and oracle drift: the realised per-head statistics of small seeded layers
 (written by tests/golden/make_manifests.py, which calls only the oracle and the
-generator) must come out the same when recomputed.  Routes, selection sizes, PE
-cutoffs and pair counts are compared exactly; the float64 masses and output
-statistics to 1e-9 relative (BLAS summation order may differ between machines)."""
+generator) must come out the same when recomputed.  Routes, PE cutoffs, VS block
+lists, selection sizes and pair counts are compared exactly; the float64 masses,
+block scores and output statistics to 1e-9 relative (BLAS summation order may differ
+between machines).  A VS direction whose residual is below float32 resolution (E3) or
+whose blocks sit within the floor band (E1/E2) may select differently under another
+summation order: there the lists are compared outside those blocks, and the sizes and
+pair counts that follow from them are not compared."""
 import importlib.util
 import json
 import os
 
 import pytest
+
+from tests import parity as PR
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 GOLDEN = os.path.join(HERE, "golden")
@@ -34,11 +40,22 @@ def test_manifests_are_reproduced():
         for key in ("generator", "layer", "seq_len", "block", "alpha"):
             assert rec[key] == new[key], (name, key)
         assert sorted(rec["heads"]) == sorted(new["heads"]), name
+        k_min = -(-1024 // rec["block"])
         for h, st in rec["heads"].items():
             nw = new["heads"][h]
             assert sorted(st) == sorted(nw), (name, h)
+            exact_lists = True
+            for d in ("v", "s") if st["route"] == "VS" else ():
+                degenerate, ex = PR.vs_direction_exempt(st["p_" + d], rec["alpha"], k_min)
+                diff = set(st["S_" + d]) ^ set(nw["S_" + d])
+                assert degenerate or not (diff - ex), (name, h, d, sorted(diff - ex))
+                exact_lists &= not diff
             for key, val in st.items():
-                if isinstance(val, float):
+                if key in ("S_v", "S_s") or (not exact_lists and key in ("k_v", "k_s", "pairs", "density")):
+                    continue
+                if isinstance(val, list):
+                    assert len(nw[key]) == len(val) and all(_close(a, b) for a, b in zip(nw[key], val)), (name, h, key)
+                elif isinstance(val, float):
                     assert _close(nw[key], val), (name, h, key, nw[key], val)
                 else:
                     assert nw[key] == val, (name, h, key, nw[key], val)
@@ -49,9 +66,9 @@ def test_manifests_show_the_planted_structure():
     with most of their proxy mass on the sink tag, i.i.d. diffuse heads route PE with a
     near-uniform proxy (C_struct about (w_sink + w_local) / n plus the proxy's own block)
     and select about 90% of the causal pairs, and the three adversarial heads behave as
-    designed (under sink collapse the float32 residual is zero, so the floor is zero and
-    every vertical block with any mass is kept; the flat head selects like a diffuse one;
-    the head at the floor routes VS with about half of its mass in the sinks)."""
+    designed (under sink collapse the vertical residual lies below float32 resolution, a
+    degenerate direction; the flat head selects like a diffuse one; the head at the floor
+    routes VS with about half of its mass in the sinks and keeps k_min vertical blocks)."""
     with open(os.path.join(GOLDEN, "manifests.json")) as f:
         m = json.load(f)
     tiny = m["tiny-4k"]["heads"]
@@ -64,6 +81,6 @@ def test_manifests_show_the_planted_structure():
         else:
             assert r["c_struct"] <= 0.15 and 0.85 < r["density"] < 0.95, h
     adv = m["stress-64k-a1-b128-adversarial"]["heads"]
-    assert adv["0"]["route"] == "VS" and adv["0"]["sink_mass"] > 1 - 1e-9 and adv["0"]["k_v"] == 512
+    assert adv["0"]["route"] == "VS" and adv["0"]["sink_mass"] > 1 - 1e-9 and adv["0"]["residual_v"] < 2 ** -20
     assert adv["1"]["route"] == "PE" and 0.85 < adv["1"]["density"] < 0.95
     assert adv["2"]["route"] == "VS" and 0.45 < adv["2"]["sink_mass"] < 0.55

@@ -455,13 +455,14 @@ def test_forced_routes_and_params(tau):
     assert (route == (0 if tau == 0.0 else 1)).all()
 
 
-def test_config1_sampled():
+def test_config1_every_head():
+    """The 32k Llama-3-8B layer: every head's scores, route and block sets against the
+    oracle, and the attention rows of six query blocks per head."""
     C = _crisp()
-    _say("config 1 (32k Llama shape), 8 heads, sampled query blocks")
+    _say("config 1 (32k Llama shape), every head, sampled query blocks")
     cfg = CONFIGS[1]
-    heads = [0, 1, 3, 8, 11, 17, 21, 31]
     qsel = lambda h, nb: sorted({0, 1, nb // 3, nb // 2, nb - 2, nb - 1})
-    _check_layer(C, cfg, C.make_params(), heads=heads, qbs_per_head=qsel, where="c1")
+    _check_layer(C, cfg, C.make_params(), qbs_per_head=qsel, where="c1")
 
 
 def _check_head_lists(res, gsets, nb, op, block, where):
@@ -485,8 +486,10 @@ def _check_head_lists(res, gsets, nb, op, block, where):
 def test_full_size_layer_in_bench_launch(cid):
     """The headline layers at full size (128k Llama, 512k Qwen-like), run as bench.py runs them
     (crisp_prefill_attn over the whole layer with the prefill workspace): every head's scores,
-    route and block lists against the oracle (list invariants checked on the device too), and
-    the attention rows of sampled query blocks of a VS and a PE head."""
+    route and block lists against the oracle (list invariants checked on the device too), the
+    attention rows of sampled query blocks of a VS and a PE head, the PE head's longest row
+    among them, and the dense baseline's first and last query blocks (the last attends to
+    every key of the layer) on the first and last head."""
     C = _crisp()
     cfg = CONFIGS[cid]
     block, G = cfg.block, cfg.group
@@ -534,13 +537,30 @@ def test_full_size_layer_in_bench_launch(cid):
             gsets = [cih[rp[h, qb]:rp[h, qb + 1]].tolist() for qb in range(nb)]
             _check_head_lists(res, gsets, nb, op, block, w)
             if h in (hv, hp):
-                qbs = [0, nb // 2, nb - 1] if h == hv else [1, nb // 8]
-                _say(f"  attention rows for {w}")
+                # the PE head also at its longest row (the lazy rescale and the float32
+                # running sums over the most tiles any unit of the layer takes)
+                longest = int(np.argmax(np.diff(rp[h])))
+                qbs = [0, nb // 2, nb - 1] if h == hv else sorted({1, nb // 8, longest})
+                _say(f"  attention rows for {w} (query blocks {qbs}; longest row {longest}: "
+                     f"{int(rp[h, longest + 1] - rp[h, longest])} blocks)")
                 ref = O.sparse_attention(Qh, Kc[g], Vc[g], gsets, block, op.scale(128), qbs=qbs)
                 PR.compare_attention(to_f64(o[h]), ref, rows=PR.qb_rows(qbs, block, cfg.seq_len), where=w + " attn")
                 del ref
             del gsets
         del Qh, res
+    # the dense baseline's last query block (every key of the layer) and its first
+    _say(f"  dense baseline rows of {cfg.name}")
+    od = C.crisp_dense_attn(q, k, v, block)
+    torch.cuda.synchronize()
+    for h in (0, cfg.n_q_heads - 1):
+        g = h // G
+        Kh, Vh, Qh = to_f64(k[g]), to_f64(v[g]), to_f64(q[h])
+        sets = [[] for _ in range(nb)]
+        sets[0], sets[nb - 1] = [0], list(range(nb))
+        ref = O.sparse_attention(Qh, Kh, Vh, sets, block, op.scale(128), qbs=[0, nb - 1])
+        PR.compare_attention(to_f64(od[h]), ref, rows=PR.qb_rows([0, nb - 1], block, cfg.seq_len),
+                             where=f"{cfg.name} h{h} dense")
+        del Kh, Vh, Qh, ref
 
 
 @pytest.mark.parametrize("block", [64, 128])
@@ -652,13 +672,17 @@ def test_max_length_layer():
         del Qh, ref
 
 
-@pytest.mark.parametrize("alpha,block", [(0.5, 64), (1.0, 128), (2.0, 128), (1.0, 64)])
+@pytest.mark.parametrize("alpha,block", [(a, b) for a in (0.5, 1.0, 2.0) for b in (64, 128)])
 def test_stress_config4(alpha, block):
+    """The 64k selection-stress layer in every cell of alpha x B (Alg. 3 with the noise
+    floor of Sec. 4.3): every head's scores, route and block sets against the oracle (the
+    three adversarial heads included), and the attention rows of three query blocks per
+    head."""
     C = _crisp()
     _say(f"config 4 stress alpha={alpha} B={block}")
     cfg = stress_config(alpha, block)
     qsel = lambda h, nb: sorted({0, nb // 2, nb - 1})
-    _check_layer(C, cfg, C.make_params(alpha=alpha), heads=[0, 1, 2, 5, 13], qbs_per_head=qsel, where=cfg.name)
+    _check_layer(C, cfg, C.make_params(alpha=alpha), qbs_per_head=qsel, where=cfg.name)
 
 
 # ------------------------------------------------------------------ FlexPrefill comparator (App. A)
@@ -920,12 +944,14 @@ def test_prefill_in_a_hip_graph(n, block):
 
 def test_golden_manifests_on_gpu():
     """The GPU path against values stored in tests/golden/manifests.json (written by the
-    oracle-only script beside it): routes exact, C_struct to the stage tolerance, a PE
-    head's pair count to 0.1% of the causal pairs (ties at the gamma cutoff may fall either
-    way; the VS selections of these layers include heads whose blocks sit exactly at the
-    floor or whose residual is below float32 resolution, E1 and E3, and are checked block
-    by block against the oracle elsewhere), and for the layer whose attention is stored, the output's mean and
-    largest magnitude to the attention tolerances.  The stored values come from inputs
+    oracle-only script beside it): routes exact, C_struct to the stage tolerance; on VS
+    heads the block scores p_v, p_s to the stage tolerances and each direction's selected
+    blocks against the stored S_v, S_s, exactly outside the E1/E2 bands of the stored
+    scores (a direction whose stored residual is below float32 resolution, E3, is checked
+    for its forced blocks and k_min only), and the lists against the expansion of the GPU's
+    own direction sets; a PE head's pair count to 0.1% of the causal pairs (ties at the
+    gamma cutoff may fall either way); and for the layer whose attention is stored, the
+    output's mean and largest magnitude to the attention tolerances.  The stored values come from inputs
     drawn by the generator on the CPU (its stream differs by device), so the same heads are
     drawn on the CPU here and copied to the GPU; the other heads of each layer stay zero."""
     import json
@@ -954,9 +980,24 @@ def test_golden_manifests_on_gpu():
             w = f"{name} h{h}"
             assert (route[h] == O.ROUTE_VS) == (st["route"] == "VS"), f"{w}: route {route[h]} vs {st['route']}"
             assert abs(float(cs[h]) - st["c_struct"]) <= PR.CS_ABS, f"{w}: C_struct {float(cs[h])} vs {st['c_struct']}"
-            pairs = sum(len(s) for s in PR.csr_to_sets(rp, ci, h, nb))
+            gsets = PR.csr_to_sets(rp, ci, h, nb)
+            pairs = sum(len(s) for s in gsets)
             if st["route"] == "PE":
                 assert abs(pairs - st["pairs"]) <= 1e-3 * nb * (nb + 1) / 2, f"{w}: pairs {pairs} vs {st['pairs']}"
+                assert not dm[h].any()
+            else:
+                k_min = -(-1024 // cfg.block)
+                stored = O.HeadResult(route=O.ROUTE_VS, c_struct=st["c_struct"], p_v=np.asarray(st["p_v"]),
+                                      p_s=np.asarray(st["p_s"]), S_v=st["S_v"], S_s=st["S_s"])
+                PR.compare_scores(cs[h], pv[h], ps[h], stored, where=w)
+                PR.compare_vs(dm[h], stored, cfg.alpha, k_min, where=w)
+                for d in (0, 1):   # also for a degenerate direction (E3)
+                    assert int(dm[h, d].sum()) >= min(k_min, nb), f"{w}: direction {d} below k_min"
+                PR.check_structure(gsets, nb, where=w)
+                S_v, S_s = (np.nonzero(dm[h, d])[0].tolist() for d in (0, 1))
+                assert gsets == O.vs_block_sets(S_v, S_s, nb), f"{w}: lists differ from the direction sets"
+                if st["S_v"] == S_v and st["S_s"] == S_s:
+                    assert pairs == st["pairs"], f"{w}: pairs {pairs} vs {st['pairs']}"
             if attend:
                 og = to_f64(o[h])
                 assert abs(og.mean() - st["out_mean"]) <= 2e-3, f"{w}: output mean {og.mean()} vs {st['out_mean']}"

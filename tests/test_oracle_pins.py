@@ -29,6 +29,7 @@ import pytest
 import torch
 
 from oracle import crisp_oracle as O
+from tests import parity as PR
 from tests.helpers import bf16_round, random_head, sink_head
 
 S128 = 1.0 / math.sqrt(128)
@@ -60,6 +61,36 @@ def test_p1_all_blocks_is_dense(n, block, kind):
     assert r.sets == O.dense_causal_sets(nb)
     ref = _sdpa_causal(q, k, v, S128)
     assert np.max(np.abs(r.out - ref)) < 1e-12
+
+
+def test_layer_gqa_mapping_matches_sdpa():
+    """crisp_layer over a GQA layer (6 query heads on 3 KV heads, so h // G and h % H_kv
+    differ for heads 1, 3 and 4): with every block selected, each head's output is torch's
+    grouped-query causal SDPA (enable_gqa, whose grouping is its own), and with the default
+    parameters each head's result is the same as the single-head path run on the KV head of
+    that grouping."""
+    n, block, hq, hkv = 384, 128, 6, 3
+    rng = np.random.default_rng(7)
+    Q = bf16_round(rng.standard_normal((hq, n, 128)) * 0.3)
+    K = bf16_round(rng.standard_normal((hkv, n, 128)))
+    V = bf16_round(rng.standard_normal((hkv, n, 128)))
+    Q[1, :, 0] += 3.0                 # heads differ in structure so a wrong grouping shows
+    K[:, :4, 0] = 8.0
+    nb = O.n_blocks(n, block)
+    dense = O.crisp_layer(Q, K, V, block, O.Params(k_min_blocks=nb, gamma=1.0))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(Q)[None], torch.from_numpy(K)[None], torch.from_numpy(V)[None],
+        is_causal=True, scale=S128, enable_gqa=True)[0].numpy()
+    assert sorted(dense) == list(range(hq))
+    for h in range(hq):
+        assert np.max(np.abs(dense[h].out - ref[h])) < 1e-12, h
+    sparse = O.crisp_layer(Q, K, V, block, O.Params(), heads=[1, 4], qbs={4: [0, 2]})
+    assert sorted(sparse) == [1, 4]
+    for h in (1, 4):
+        g = torch.arange(hq).reshape(hkv, hq // hkv).tolist()
+        g = next(i for i, hs in enumerate(g) if h in hs)
+        one = O.crisp_head(Q[h], K[g], V[g], block, O.Params(), qbs=[0, 2] if h == 4 else None)
+        assert sparse[h].sets == one.sets and np.array_equal(sparse[h].out, one.out)
 
 
 def test_p2_masked_softmax_identity():
@@ -324,12 +355,33 @@ def test_p6_noise_at_floor():
 
 
 def test_degenerate_residual_sink_collapse():
-    n = 8192
+    """Sink collapse (E3): logits beta on keys 0..3 and exactly 0 elsewhere, so proxy row r
+    (query i) has Z = 4 e^beta + (i + 1 - 4) and every inner block the same mass
+    (1/b) sum_r B / Z -- about 1.4e-16, far below float32 resolution next to 1.  The
+    block scores match that closed form; the residual, evaluated as printed in float64
+    ((1 - p_0) - p_last), equals the inner-block mass up to the cancellation's rounding
+    (a few dozen ulps of 1; reading R20) and lies below 2^-20, so the direction is
+    degenerate and its floor decisions are rounding noise.  Whatever the floor, the
+    k_min top-up takes the sink block and then the tied inner blocks in index order."""
+    n, block = 8192, 128
+    nb, b = n // block, block
     q, k, _ = sink_head(n, beta=40.0)
-    r = O.crisp_head(q, k, None, 128, O.Params(), attend=False)
+    r = O.crisp_head(q, k, None, block, O.Params(), attend=False)
+    assert r.route == O.ROUTE_VS
+    beta = q[0, 0] * k[0, 0] / math.sqrt(128)           # the exact logit of the bf16 tag values
+    rows = np.arange(n - b, n)
+    Z = 4.0 * np.exp(beta) + (rows + 1 - 4)
+    p_inner = np.mean(block / Z)
+    p_last = np.mean((rows - (nb - 1) * block + 1) / Z)
+    assert np.allclose(r.p_v[1:nb - 1], p_inner, rtol=1e-12, atol=0)
+    assert abs(r.p_v[nb - 1] - p_last) <= 1e-12 * p_last
     rr, mu, thr = O.vs_floor(r.p_v, 1.0)
-    assert r.route == O.ROUTE_VS and rr == 0.0 and thr == 0.0
-    assert sum(r.p_v[1:-1]) < 2 ** -20
+    assert abs(rr - (nb - 2) * p_inner) <= 1e-14 and rr < 2 ** -20
+    assert mu == rr / (nb - 2) and thr == mu
+    degenerate, _ = PR.vs_direction_exempt(r.p_v, 1.0, 8)
+    assert degenerate
+    for alpha in (0.5, 1.0, 2.0, 4.0):
+        assert O.vs_select(r.p_v, alpha, 8)[:8] == list(range(8))
 
 
 # ---------------------------------------------------------------- P7 (metamorphic)

@@ -112,7 +112,7 @@ STRESS_ALPHAS = (0.5, 1.0, 2.0)
 STRESS_BLOCKS = (64, 128)
 
 
-PE_SWEEP_LENGTHS = (8192, 65536, 131072, 262144, 524288, 16384, 32768)   # variant = position here
+PE_SWEEP_LENGTHS = (8192, 65536, 131072, 262144, 524288, 16384, 32768, 2048, 4096)   # variant = position here
 
 
 def structured_pe_config(seq_len: int = 131072) -> LayerConfig:
