@@ -218,6 +218,25 @@ crisp_status crisp_sparse_attn(const crisp_shape* shape, float softmax_scale,
                                int64_t col_cap_per_head, crisp_bf16* o,
                                void* workspace_or_null, size_t workspace_bytes, crisp_stream stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): crisp_sparse_attn with its balanced
+ * work list kept in the library's own static schedule area instead of a caller's
+ * workspace.  Same arguments, list semantics, output and error behaviour as
+ * crisp_sparse_attn; it allocates and frees nothing.  The area is a file-scope device
+ * array of 16 MiB, one per GPU the library runs on, held until the process ends; it
+ * holds the work list of any layer of up to 1.5 million (head, query block) units
+ * (about 4 million from 2^19 tokens on, where rows are never split; a larger layer is
+ * CRISP_EINVAL before anything is enqueued) and at most 64 partial-result slots, so
+ * fewer long rows are split than with a workspace (results then differ from
+ * crisp_sparse_attn's by floating-point rounding only).  Every call on one GPU uses that
+ * GPU's area, which is rewritten before each use: calls that overlap in time on one
+ * GPU (on different streams, or from different threads) race and must be serialised
+ * by the caller. */
+crisp_status crisp_sparse_attn_noalloc(const crisp_shape* shape, float softmax_scale,
+                                       const crisp_bf16* q, const crisp_bf16* k, const crisp_bf16* v,
+                                       const int32_t* row_ptr, const int32_t* col_idx,
+                                       int64_t col_cap_per_head, crisp_bf16* o, crisp_stream stream);
+
 /* Alg. 1: all stages on `stream`: estimate, route and select, sparse attention
  * (with route_mode CRISP_ROUTE_BY_JSD, crisp_jsd's pattern search before the route).
  * route_or_null, row_ptr_or_null and col_idx_or_null, if all three are given,

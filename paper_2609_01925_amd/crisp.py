@@ -59,6 +59,7 @@ def _load(path: str = _LIB_PATH):
         "crisp_route_select": (ctypes.c_int, [sh, pa, P, P, P, P, P, P, P, P, I64, P, P, SZ, P]),
         "crisp_sparse_workspace_size": (ctypes.c_int, [sh, ctypes.POINTER(SZ)]),
         "crisp_sparse_attn": (ctypes.c_int, [sh, F, P, P, P, P, P, I64, P, P, SZ, P]),
+        "crisp_sparse_attn_noalloc": (ctypes.c_int, [sh, F, P, P, P, P, P, I64, P, P]),
         "crisp_prefill_attn": (ctypes.c_int, [sh, pa, P, P, P, P, P, P, P, P, SZ, P]),
         "crisp_dense_attn": (ctypes.c_int, [sh, F, P, P, P, P, P]),
         "crisp_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -74,7 +75,7 @@ def _load(path: str = _LIB_PATH):
 lib = _load()
 EXPORTED = ("crisp_params_default", "crisp_col_capacity", "crisp_workspace_size", "crisp_prefill_workspace_size",
             "crisp_sparse_workspace_size", "crisp_estimate", "crisp_jsd", "crisp_route_select", "crisp_sparse_attn",
-            "crisp_prefill_attn", "crisp_dense_attn", "crisp_status_string", "crisp_last_error")
+            "crisp_sparse_attn_noalloc", "crisp_prefill_attn", "crisp_dense_attn", "crisp_status_string", "crisp_last_error")
 
 # route_mode / vs_mode values (include/crisp.h)
 ROUTE_BY_CSTRUCT, ROUTE_BY_JSD = 0, 1
@@ -259,6 +260,22 @@ def crisp_sparse_attn(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, row_ptr
     _check(lib.crisp_sparse_attn(ctypes.byref(sh), softmax_scale, _ptr(q), _ptr(k), _ptr(v), _ptr(row_ptr),
                                  _ptr(col_idx), col_idx.shape[1], _ptr(o), _ptr(ws), 0 if ws is None else ws.numel(),
                                  _stream(q.device)), "crisp_sparse_attn")
+    return o
+
+
+def crisp_sparse_attn_noalloc(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, row_ptr: torch.Tensor,
+                              col_idx: torch.Tensor, block: int = 128, softmax_scale: float = 0.0,
+                              out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Stage 4 over caller-given CSR lists with the library's own static schedule area (the
+    C entry point allocates nothing; calls that overlap on one GPU race) -> o bf16 [H_q, n, d]."""
+    _inputs(q, k, v)
+    sh = shape_of(q, k, block)
+    _tensor(row_ptr, "row_ptr", torch.int32, (q.shape[0], n_blocks(q.shape[1], block) + 1), q.device)
+    _tensor(col_idx, "col_idx", torch.int32, (q.shape[0], None), q.device)
+    o = torch.empty_like(q) if out is None else _tensor_out(out, q)
+    _check(lib.crisp_sparse_attn_noalloc(ctypes.byref(sh), softmax_scale, _ptr(q), _ptr(k), _ptr(v), _ptr(row_ptr),
+                                         _ptr(col_idx), col_idx.shape[1], _ptr(o), _stream(q.device)),
+           "crisp_sparse_attn_noalloc")
     return o
 
 

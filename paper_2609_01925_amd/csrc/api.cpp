@@ -350,6 +350,35 @@ crisp_status crisp_sparse_attn(const crisp_shape* shape, float softmax_scale, co
                     "crisp_sparse_attn launch");
 }
 
+crisp_status crisp_sparse_attn_noalloc(const crisp_shape* shape, float softmax_scale, const crisp_bf16* q,
+                                       const crisp_bf16* k, const crisp_bf16* v, const int32_t* row_ptr,
+                                       const int32_t* col_idx, int64_t col_cap_per_head, crisp_bf16* o,
+                                       crisp_stream stream) {
+  Dims d;
+  CHECK(check_shape(shape, &d));
+  if (!(softmax_scale >= 0.f) || !isfinite(softmax_scale))
+    return fail(CRISP_EINVAL, "softmax_scale must be finite and >= 0");
+  if (empty(d)) return CRISP_OK;
+  CHECK(check_ptr(q, 16, "q"));
+  CHECK(check_ptr(k, 16, "k"));
+  CHECK(check_ptr(v, 16, "v"));
+  CHECK(check_ptr(o, 16, "o"));
+  CHECK(check_ptr(row_ptr, 4, "row_ptr"));
+  CHECK(check_ptr(col_idx, 4, "col_idx"));
+  if (col_cap_per_head < 0) return fail(CRISP_EINVAL, "col_cap_per_head must be >= 0");
+  const size_t need = attn_schedule_bytes(d, kStaticSlots);
+  if (need > kStaticSchedBytes)
+    return fail(CRISP_EINVAL, "layer needs %zu bytes of schedule area (%lld query blocks over all heads); the "
+                "static area holds %zu", need, (long long)d.hq * d.nb, kStaticSchedBytes);
+  void* area = nullptr;
+  CHECK(hip_status(static_schedule_area(&area), "crisp_sparse_attn_noalloc static area"));
+  DEBUG_INPUTS(q, k, v, (hipStream_t)stream);
+  DEBUG_LISTS(row_ptr, col_idx, col_cap_per_head, (hipStream_t)stream);
+  return hip_status(launch_attn(d, scale_of(softmax_scale), q, k, v, row_ptr, col_idx, col_cap_per_head, false, o,
+                                area, (hipStream_t)stream, kStaticSlots),
+                    "crisp_sparse_attn_noalloc launch");
+}
+
 crisp_status crisp_dense_attn(const crisp_shape* shape, float softmax_scale, const crisp_bf16* q,
                               const crisp_bf16* k, const crisp_bf16* v, crisp_bf16* o, crisp_stream stream) {
   Dims d;

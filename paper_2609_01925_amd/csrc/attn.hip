@@ -63,7 +63,6 @@ struct Tile {
 constexpr float kSumLimit = 256.0f;          // a lane's tile sum of P above this forces a rescale
 constexpr int kCostBuckets = 8192;
 constexpr int kOneShotMinLen = 1 << 19;  // from this length on, sparse lists run one unit per workgroup
-constexpr int kSplitSlots = 1024;        // most partial-result slots of one launch
 constexpr int kMinChunk = 8;             // shortest chunk of a split row, in list entries
 constexpr int kItemUnitBits = 21;        // work item = unit | chunk << 21
 
@@ -947,17 +946,17 @@ int persistent_grid() {
 
 // Schedule area of the sparse kernel: header and items, then (when rows may be
 // split: persistent mode, fewer than 2^21 units) slot_base, split_rows and the
-// partial slots.  Slots: min(1024, 2 x units).
+// partial slots.  Slots: min(max_slots, 2 x units).
 struct SchedLayout {
   int slots;
   size_t slot_base, split_rows, parts, total;
 };
 
-SchedLayout sched_layout(const Dims& d) {
+SchedLayout sched_layout(const Dims& d, int max_slots) {
   SchedLayout s;
   const size_t units = (size_t)d.hq * d.nb;
   const bool split = d.n < kOneShotMinLen && units < ((size_t)1 << kItemUnitBits);
-  s.slots = split ? (int)(2 * units < (size_t)kSplitSlots ? 2 * units : (size_t)kSplitSlots) : 0;
+  s.slots = split ? (int)(2 * units < (size_t)max_slots ? 2 * units : (size_t)max_slots) : 0;
   size_t off = (64 + units + (size_t)s.slots) * sizeof(int32_t);
   s.slot_base = off;
   if (s.slots > 0) off += units * sizeof(int32_t);
@@ -970,11 +969,35 @@ SchedLayout sched_layout(const Dims& d) {
   return s;
 }
 
-size_t attn_schedule_bytes(const Dims& d) { return sched_layout(d).total; }
+size_t attn_schedule_bytes(const Dims& d, int max_slots) { return sched_layout(d, max_slots).total; }
+
+namespace {
+// The library's static schedule area for callers that cannot allocate: a file-scope
+// device array, one copy per device.  In host code its name is not a device address;
+// kernels get the address hipGetSymbolAddress returns for the current device.
+__device__ __align__(256) char scratch[kStaticSchedBytes];
+}  // namespace
+
+hipError_t static_schedule_area(void** p) {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<void*> addr[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void* a = addr[dev].load(std::memory_order_relaxed);
+  if (a == nullptr) {  // first call on this device (threads that race store the same address)
+    if ((e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+    if (a == nullptr) return hipErrorInvalidSymbol;
+    addr[dev].store(a, std::memory_order_relaxed);
+  }
+  *p = a;
+  return hipSuccess;
+}
 
 hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                        const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, bool dense,
-                       uint16_t* o, void* sched, hipStream_t stream) {
+                       uint16_t* o, void* sched, hipStream_t stream, int max_slots) {
   if (d.n == 0 || d.hq == 0) return hipSuccess;
   if (dense && d.B == 64) {
     // Dense causal attention does not depend on the query block size: 128-row
@@ -983,7 +1006,7 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
     Dims d2 = d;
     d2.B = 128;
     d2.nb = (d.n + 127) / 128;
-    return launch_attn(d2, scale, q, k, v, row_ptr, col_idx, col_cap, dense, o, sched, stream);
+    return launch_attn(d2, scale, q, k, v, row_ptr, col_idx, col_cap, dense, o, sched, stream, max_slots);
   }
   AttnArgs a;
   a.q = q; a.k = k; a.v = v; a.o = o;
@@ -1005,7 +1028,7 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
   }
   if (!dense && sched != nullptr) {
     char* sc = reinterpret_cast<char*>(sched);
-    const SchedLayout sl = sched_layout(d);
+    const SchedLayout sl = sched_layout(d, max_slots);
     a.counter = reinterpret_cast<int*>(sc);
     a.order = reinterpret_cast<const int32_t*>(sc) + 64;
     a.one_shot = d.n >= kOneShotMinLen ? 1 : 0;

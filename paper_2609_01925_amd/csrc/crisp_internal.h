@@ -28,13 +28,26 @@ struct WsLayout {
 };
 WsLayout ws_layout(const Dims& d);
 
-// Bytes of the longest-first work list used by the persistent sparse kernel.
-size_t attn_schedule_bytes(const Dims& d);
+// Partial-result slots of the sparse kernel's schedule area (split rows): a caller's
+// workspace provides up to kWorkspaceSlots; the library's own static area, used by the
+// entry point that allocates nothing, up to kStaticSlots within kStaticSchedBytes.
+constexpr int kWorkspaceSlots = 1024;
+constexpr int kStaticSlots = 64;
+constexpr size_t kStaticSchedBytes = (size_t)16 << 20;
 
-// sched == nullptr: static grid (dense, or sparse without a work list).
+// Bytes of the longest-first work list used by the persistent sparse kernel, with at
+// most max_slots partial-result slots.
+size_t attn_schedule_bytes(const Dims& d, int max_slots = kWorkspaceSlots);
+
+// Device address of the library's static schedule area on the current device (its
+// kStaticSchedBytes are a file-scope device array; each device holds its own copy).
+hipError_t static_schedule_area(void** p);
+
+// sched == nullptr: static grid (dense, or sparse without a work list); otherwise sched
+// holds attn_schedule_bytes(d, max_slots) bytes.
 hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint16_t* k, const uint16_t* v,
                        const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, bool dense,
-                       uint16_t* o, void* sched, hipStream_t stream);
+                       uint16_t* o, void* sched, hipStream_t stream, int max_slots = kWorkspaceSlots);
 
 hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, const uint16_t* q,
                            const uint16_t* k, float* c_struct, float* p_v, float* p_s, char* ws,

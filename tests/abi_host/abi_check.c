@@ -197,6 +197,21 @@ static void check_pointers(void) {
          "small sparse workspace");
   EXPECT(crisp_sparse_attn(&s, 0.f, P256, P256, P256, P256, P256, cap, P256, P16, sws, NULL) == CRISP_EINVAL,
          "sparse workspace not 256-aligned");
+  EXPECT(crisp_sparse_attn_noalloc(&s, 0.f, P256, P256, P8, P256, P256, cap, P256, NULL) == CRISP_EINVAL,
+         "misaligned v (no-alloc)");
+  EXPECT(crisp_sparse_attn_noalloc(&s, 0.f, P256, P256, P256, NULL, P256, cap, P256, NULL) == CRISP_EINVAL,
+         "null row_ptr (no-alloc)");
+  EXPECT(crisp_sparse_attn_noalloc(&s, 0.f, P256, P256, P256, P256, P256, -1, P256, NULL) == CRISP_EINVAL,
+         "negative capacity (no-alloc)");
+  EXPECT(crisp_sparse_attn_noalloc(&s, NAN, P256, P256, P256, P256, P256, cap, P256, NULL) == CRISP_EINVAL,
+         "NaN scale (no-alloc)");
+  {
+    /* 128 heads x 32768 blocks: the work list alone is one int past the static area */
+    crisp_shape big = shape(128, 1, 1 << 21, 128, 64);
+    EXPECT(crisp_sparse_attn_noalloc(&big, 0.f, P256, P256, P256, P256, P256, (int64_t)1 << 40, P256, NULL) ==
+               CRISP_EINVAL && strstr(crisp_last_error(), "static area") != NULL,
+           "layer too large for the static schedule area");
+  }
   EXPECT(crisp_dense_attn(&s, 0.f, P256, P256, P256, NULL, NULL) == CRISP_EINVAL, "null o (dense)");
   EXPECT(crisp_prefill_attn(&s, &p, P256, P256, P256, P256, P256, NULL, P256, P256, pws, NULL) == CRISP_EINVAL,
          "lists partly given");
@@ -224,6 +239,8 @@ static void check_empty(void) {
     EXPECT(crisp_prefill_attn(s, &p, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL, 0, NULL) == CRISP_OK,
            "empty prefill %d", i);
     EXPECT(crisp_dense_attn(s, 0.f, NULL, NULL, NULL, NULL, NULL) == CRISP_OK, "empty dense %d", i);
+    EXPECT(crisp_sparse_attn_noalloc(s, 0.f, NULL, NULL, NULL, NULL, NULL, 0, NULL, NULL) == CRISP_OK,
+           "empty no-alloc sparse %d", i);
   }
 }
 
@@ -264,6 +281,9 @@ static void check_launch_failure(void) {
   crisp_status st = crisp_dense_attn(&s, 0.f, P256, P256, P256, P256, NULL);
   EXPECT(st == CRISP_EHIP && strstr(crisp_last_error(), "crisp_dense_attn") != NULL, "dense launch failure: %s",
          crisp_status_string(st));
+  st = crisp_sparse_attn_noalloc(&s, 0.f, P256, P256, P256, P256, P256, crisp_col_capacity(&s), P256, NULL);
+  EXPECT(st == CRISP_EHIP && strstr(crisp_last_error(), "crisp_sparse_attn_noalloc") != NULL,
+         "no-alloc sparse launch failure: %s", crisp_status_string(st));
   size_t ws = 0;
   crisp_workspace_size(&s, &ws);
   st = crisp_estimate(&s, &p, P256, P256, P256, P256, P256, P256, ws, NULL);
