@@ -390,6 +390,21 @@ def measured_peaks():
 
     t_mfma = time_events(mfma, 10, 3)
     mfma_tflops = lib.crisp_peak_mfma_flop(wg, iters) / (t_mfma["median"] * 1e-3) / 1e12
+    # the same MFMAs on operands that change every instruction (random normal bf16 values),
+    # each launch about as long as the 128k attention launch, so the clock settles where
+    # it does under that kernel
+    lib.crisp_peak_mfma_bf16_toggling.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                                  ctypes.c_void_p]
+    g = torch.Generator(device="cpu").manual_seed(20261202)
+    ops = torch.randn(64 * 16 * 8, generator=g).to(torch.bfloat16).to(dev)
+    iters_t = 80000
+
+    def mfma_t():
+        assert lib.crisp_peak_mfma_bf16_toggling(wg, iters_t, ctypes.c_void_p(ops.data_ptr()),
+                                                 ctypes.c_void_p(out.data_ptr()), stream) == 0
+
+    t_tog = time_events(mfma_t, 10, 3)
+    tog_tflops = lib.crisp_peak_mfma_flop(wg, iters_t) / (t_tog["median"] * 1e-3) / 1e12
     nbytes = 1 << 30
     src = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)
@@ -402,14 +417,18 @@ def measured_peaks():
     torch.cuda.synchronize()
     assert bool(torch.equal(src, dst))
     copy_gbs = 2.0 * nbytes / (t_copy["median"] * 1e-3) / 1e9
-    del src, dst, out
+    del src, dst, out, ops
     torch.cuda.empty_cache()
-    log(f"peaks: bf16 MFMA {mfma_tflops:.0f} TFLOP/s, copy {copy_gbs:.0f} GB/s")
-    return {"mfma_bf16_tflops": mfma_tflops, "mfma_bf16_published_tflops": MFMA_BF16_PEAK_TFLOPS,
+    log(f"peaks: bf16 MFMA {mfma_tflops:.0f} TFLOP/s (constant operands), {tog_tflops:.0f} TFLOP/s "
+        f"(toggling operands), copy {copy_gbs:.0f} GB/s")
+    return {"mfma_bf16_tflops": tog_tflops, "mfma_bf16_constant_operand_tflops": mfma_tflops,
+            "mfma_bf16_published_tflops": MFMA_BF16_PEAK_TFLOPS,
             "copy_gbs": copy_gbs, "hbm_published_gbs": HBM_PEAK_GBS,
             "method": ("MFMA: 2048 workgroups x 4 waves, 4 independent v_mfma_f32_32x32x16_bf16 chains per wave, "
-                       f"{iters} rounds, median of 10 launches; copy: 1 GiB device to device, 16-byte "
-                       "loads and stores, read + written bytes, median of 10 launches")}
+                       f"median of 10 launches; mfma_bf16_tflops: operands cycling through 16 random normal "
+                       f"bf16 registers per lane ({iters_t} rounds, launches about as long as the 128k attention's); "
+                       f"constant_operand: the same registers every MFMA ({iters} rounds); copy: 1 GiB device to "
+                       "device, 16-byte loads and stores, read + written bytes, median of 10 launches")}
 
 
 def config_records(steps, warmup, skip_cpu, peaks):

@@ -256,8 +256,12 @@ crisp_status crisp_prefill_attn(const crisp_shape* shape, const crisp_params* pa
  * block lists itself (crisp_workspace_size plus the route, row_ptr and col_idx). */
 crisp_status crisp_prefill_workspace_size(const crisp_shape* shape, size_t* bytes);
 
-/* Dense causal softmax attention with the same kernel as crisp_sparse_attn and
- * every causal block listed implicitly (the dense baseline). */
+/* The dense baseline of the paper's latency comparison (Sec. 5 setup: full causal
+ * attention with FlashAttention, against which the sparse speedups are quoted): Eq. 1
+ * with every causal key block selected, o[h][i] = sum_{j <= i} softmax_j(scale *
+ * q_i . k_j) v_j, run by the same kernel as crisp_sparse_attn with every causal block
+ * listed implicitly.  Same tensor layouts, ownership and error behaviour as
+ * crisp_sparse_attn; no workspace.  softmax_scale 0 means 1/sqrt(d). */
 crisp_status crisp_dense_attn(const crisp_shape* shape, float softmax_scale,
                               const crisp_bf16* q, const crisp_bf16* k, const crisp_bf16* v,
                               crisp_bf16* o, crisp_stream stream);

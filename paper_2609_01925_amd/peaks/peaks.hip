@@ -45,13 +45,59 @@ __global__ __launch_bounds__(256) void peak_mfma_bf16(int iters, float* out) {
   out[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = s;
 }
 
-// dst[i] = src[i] over n16 16-byte words, grid-stride, one 16-byte load and store per
-// lane and step (reads n16 * 16 bytes and writes as many).
+// The same MFMA work on operands that change from one MFMA to the next: each lane holds
+// 8 A and 8 B operands loaded from `ops` (any bits that are finite bf16 values, e.g.
+// random normal values), and MFMA u of round-group g uses A[(u + c) % 8] and
+// B[(3 u + c) % 8], so the multipliers' inputs toggle as they do on real data (the
+// constant-operand loop above does not switch them and runs at a higher clock).
+// ops: 64 lanes x 16 operands x 16 bytes, read by every wave.  iters is a multiple of 8.
+__global__ __launch_bounds__(256) void peak_mfma_bf16_toggling(int iters, const bf16x8* __restrict__ ops,
+                                                             float* out) {
+  const int lane = threadIdx.x & 63;
+  bf16x8 av[8], bv[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    av[i] = ops[lane * 16 + i];
+    bv[i] = ops[lane * 16 + 8 + i];
+  }
+  f32x16 acc[kChains];
+#pragma unroll
+  for (int c = 0; c < kChains; ++c)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[c][i] = 0.f;
+  for (int it = 0; it < iters; it += 8) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int c = 0; c < kChains; ++c)
+        acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[(u + c) & 7], bv[(3 * u + c) & 7], acc[c], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < kChains; ++c)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s += acc[c][i];
+  out[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = s;
+}
+
+// dst[i] = src[i] over n16 16-byte words (reads n16 * 16 bytes and writes as many).  Each
+// lane moves four words per step, loads first, so every lane keeps 64 bytes in flight;
+// a grid-stride loop covers any size.
+constexpr int kCopyUnroll = 4;
+
 __global__ __launch_bounds__(256) void peak_copy(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
                                                  size_t n16) {
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
-    dst[i] = src[i];
+  const size_t lanes = (size_t)gridDim.x * blockDim.x;
+  const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  size_t i = t;
+  for (; i + (kCopyUnroll - 1) * lanes < n16; i += kCopyUnroll * lanes) {
+    u32x4 r[kCopyUnroll];
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u) r[u] = src[i + u * lanes];
+#pragma unroll
+    for (int u = 0; u < kCopyUnroll; ++u) dst[i + u * lanes] = r[u];
+  }
+  for (; i < n16; i += lanes) dst[i] = src[i];
 }
 
 }  // namespace
@@ -67,6 +113,16 @@ double crisp_peak_mfma_flop(int workgroups, int iters) {
 int crisp_peak_mfma_bf16(int workgroups, int iters, float* out, void* stream) {
   if (workgroups <= 0 || iters <= 0 || !out) return (int)hipErrorInvalidValue;
   hipLaunchKernelGGL(peak_mfma_bf16, dim3(workgroups), dim3(256), 0, (hipStream_t)stream, iters, out);
+  return (int)hipGetLastError();
+}
+
+// As crisp_peak_mfma_bf16 with toggling operands; ops: 16 KiB (64 x 16 x 8 bf16, 16-byte
+// aligned) of finite bf16 values; iters a multiple of 8.  Same FLOP count.
+int crisp_peak_mfma_bf16_toggling(int workgroups, int iters, const void* ops, float* out, void* stream) {
+  if (workgroups <= 0 || iters <= 0 || iters % 8 || !ops || !out || (uintptr_t)ops % 16)
+    return (int)hipErrorInvalidValue;
+  hipLaunchKernelGGL(peak_mfma_bf16_toggling, dim3(workgroups), dim3(256), 0, (hipStream_t)stream, iters,
+                     (const bf16x8*)ops, out);
   return (int)hipGetLastError();
 }
 

@@ -33,6 +33,10 @@ def test_peaks_library_exports_and_validates():
     lib.crisp_peak_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p]
     assert lib.crisp_peak_mfma_bf16(0, 10, ctypes.c_void_p(16), None) != 0      # no workgroups
     assert lib.crisp_peak_mfma_bf16(8, 10, None, None) != 0                     # no output
+    lib.crisp_peak_mfma_bf16_toggling.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                                  ctypes.c_void_p]
+    assert lib.crisp_peak_mfma_bf16_toggling(8, 12, ctypes.c_void_p(16), ctypes.c_void_p(16), None) != 0  # 12 % 8
+    assert lib.crisp_peak_mfma_bf16_toggling(8, 16, ctypes.c_void_p(8), ctypes.c_void_p(16), None) != 0   # misaligned
     assert lib.crisp_peak_copy(ctypes.c_void_p(16), ctypes.c_void_p(32), 15, 1, None) != 0   # not 16-byte words
     assert lib.crisp_peak_copy(ctypes.c_void_p(8), ctypes.c_void_p(32), 16, 1, None) != 0    # misaligned
 
