@@ -32,10 +32,11 @@ ARCH = "gfx950"
 # otherwise form them from ordinary float code.
 DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"-I{INCLUDE}", f"-I{CSRC}", "-Wall", "-Wno-unused-function"]
-# Per-source device flags.  The attention kernel keeps its MFMA results (scores,
-# read by the softmax every tile, and the output accumulators) in VGPRs; left to
-# itself the compiler places them in AGPRs and copies every score out again.
-EXTRA = {"attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+# Per-source device flags.  The attention and estimator kernels keep their MFMA
+# results (scores, read by the softmax every tile, and the output accumulators) in
+# VGPRs; left to itself the compiler places them in AGPRs and copies every score out
+# again.
+EXTRA = {"attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"], "estimate.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def hipcc() -> str:

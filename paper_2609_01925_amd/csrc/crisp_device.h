@@ -129,4 +129,69 @@ __device__ __forceinline__ int wave_sum_i(int x) {
   return x;
 }
 
+#if defined(__HIP_DEVICE_COMPILE__)
+
+// Tile fetch: a 64-key x 128-dim tile goes straight from global memory into an
+// LDS stage (buffer_load ... lds, 16 bytes per lane, lane t writing LDS base +
+// 16 t).  Instruction (i, w') fills rows 16 i + 4 w' .. +3; lane t supplies row
+// 16 i + 4 w' + t / 16, physical chunk t % 16, so it loads logical chunk
+// (t % 16) ^ swz(row) -- the swizzle only depends on row % 16, so the per-lane
+// source offset is the same for every i (i moves the scalar offset).  Keys at or
+// past n lie outside the buffer range and read as 0.
+template <int NW>
+struct Fetch {
+  static constexpr int kPerWave = 4 / NW;  // w' values per wave
+  int voff[kPerWave];
+};
+
+template <int NW>
+__device__ __forceinline__ void make_fetch(Fetch<NW>& f, int w, int t) {
+#pragma unroll
+  for (int x = 0; x < Fetch<NW>::kPerWave; ++x) {
+    const int wp = w + NW * x;
+    const int row = 4 * wp + (t >> 4);
+    f.voff[x] = row * 256 + (((t & 15) ^ swz(row)) << 4);
+  }
+}
+
+typedef __attribute__((__vector_size__(4 * sizeof(int)))) int i32x4;
+
+// Buffer descriptor (V#) over one KV head's [n, 128] bf16 tensor; num_records
+// bounds the byte range, so reads at or past key n return 0.
+__device__ __forceinline__ i32x4 tensor_rsrc(const uint16_t* base, int n) {
+  const unsigned long long p = (unsigned long long)base;
+  return i32x4{(int)(unsigned)p, (int)(unsigned)(p >> 32), n * 256, 0x00020000};
+}
+
+// One LDS-DMA load: 16 bytes per lane from rsrc + voff + soff into LDS address
+// lds_addr + 16 * lane.  Issued as inline assembly so that the compiler's
+// wait-count pass does not treat every later LDS read as dependent on it; the
+// kernel waits explicitly (wait_dma) and publishes the tile with a workgroup
+// barrier before any wave reads it.
+__device__ __forceinline__ void dma16(i32x4 rsrc, int voff, int soff, int lds_addr) {
+  const int m0 = __builtin_amdgcn_readfirstlane(lds_addr);
+  const int so = __builtin_amdgcn_readfirstlane(soff);
+  // The scalar offset may come from v_readfirstlane (a VALU write to an SGPR),
+  // which a VMEM instruction may only read after 5 wait states, and M0 is written
+  // just before; the compiler cannot see these reads inside the assembly, so the
+  // wait states are part of it.
+  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds" ::"v"(voff), "s"(rsrc), "s"(so), "{m0}"(m0));
+}
+
+// One tensor's tile of BK keys into the LDS stage at address stage.
+template <int NW, int BK>
+__device__ __forceinline__ void fetch_tile(const Fetch<NW>& f, i32x4 rsrc, int stage, int key0, int w) {
+#pragma unroll
+  for (int x = 0; x < Fetch<NW>::kPerWave; ++x) {
+    const int wp = w + NW * x;
+#pragma unroll
+    for (int i = 0; i < BK / 16; ++i) dma16(rsrc, f.voff[x], (key0 + 16 * i) * 256, stage + (16 * i + 4 * wp) * 256);
+  }
+}
+
+// Waits until every LDS-DMA load of this wave has landed (s_waitcnt vmcnt(0)).
+__device__ __forceinline__ void wait_dma() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
+
+#endif  // __HIP_DEVICE_COMPILE__
+
 }  // namespace crisp

@@ -24,6 +24,7 @@ namespace {
 constexpr int BK = 64;
 constexpr int kTileBytes = BK * 256;
 constexpr int NT = 256;  // 4 waves; wave w owns proxy rows 32w .. 32w + 31
+constexpr float kSumLimit = 256.0f;  // a lane's tile sum above this raises the running max
 
 struct EstArgs {
   const uint16_t* q;
@@ -51,97 +52,146 @@ __device__ __forceinline__ void load_q_hat(const EstArgs& a, int h, int r, int l
   }
 }
 
-// K tile of 64 keys (keys at or past n read as 0): 16 bytes x 4 per thread into
-// registers, then into an LDS buffer.  The next tile is loaded into registers
-// before the current one's MFMAs, so its latency overlaps them.
-__device__ __forceinline__ void load_k_regs(u32x4 (&t)[4], const uint16_t* Kg, int key0, int n, int tid) {
-  const int c = tid & 15;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int key = key0 + (tid >> 4) + 16 * i;
-    t[i] = key < n ? *reinterpret_cast<const u32x4*>(Kg + (size_t)key * kHeadDim + 8 * c) : u32x4{0, 0, 0, 0};
-  }
-}
+#if defined(__HIP_DEVICE_COMPILE__)
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
-__device__ __forceinline__ void store_k_regs(char* buf, const u32x4 (&t)[4], int tid) {
-  const int c = tid & 15;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) *reinterpret_cast<u32x4*>(buf + lds_off((tid >> 4) + 16 * i, 8 * c)) = t[i];
-}
-
-__device__ __forceinline__ void scores(const char* kbuf, const bf16x8 (&qf)[8], int l, f32x16 (&s)[2]) {
+// S^T of one 64-key tile (keys on M, the wave's 32 proxy rows on N) from the
+// swizzled K stage at LDS address kbuf.
+__device__ __forceinline__ void scores(int kbuf, const bf16x8 (&qf)[8], int l, f32x16 (&s)[2]) {
   s[0] = zero16();
   s[1] = zero16();
 #pragma unroll
   for (int kk = 0; kk < 8; ++kk) {
     const int d = 16 * kk + 8 * (l >> 5);
-    s[0] = mfma32(lds_read16(kbuf, lds_off(l & 31, d)), qf[kk], s[0]);
-    s[1] = mfma32(lds_read16(kbuf, lds_off(32 + (l & 31), d)), qf[kk], s[1]);
+    const bf16x8 k0 = *(const lds_bf16x8*)(uint32_t)(kbuf + lds_off(l & 31, d));
+    const bf16x8 k1 = *(const lds_bf16x8*)(uint32_t)(kbuf + lds_off(32 + (l & 31), d));
+    s[0] = mfma32(k0, qf[kk], s[0]);
+    s[1] = mfma32(k1, qf[kk], s[1]);
   }
 }
+#endif
 
 __device__ __forceinline__ int key_of(int key0, int mb, int i, int l) {
   return key0 + 32 * mb + 8 * (i >> 2) + 4 * (l >> 5) + (i & 3);
 }
 
-// One pass over K: scores, causal mask, per-row running max, and under that running
-// max the row's sums of exp2((s - max) c): per key block J split by slash block (lo:
-// keys whose diagonal through the last proxy row stays in J, hi: those moving to
-// J + 1), over the anchor keys (anchor mass), and over all its keys (l, the blocks'
-// lo + hi added as each block ends).  When the running max rises, the sums still open
-// are scaled down to the new max; a block's (lo, hi) is written with the max it was
-// summed under when the block ends, and the range's (max, l, anchor) when the range
-// ends.
-__global__ __launch_bounds__(NT) void est_pass(EstArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * kTileBytes];
-  const int h = blockIdx.x / a.splits, sp = blockIdx.x % a.splits;
+// One pass over K: scores, causal mask, and per proxy row, under a running max, the
+// sums of exp2((s - max) c): per key block J split by slash block (lo: keys whose
+// diagonal through the last proxy row stays in J, hi: those moving to J + 1), over the
+// anchor keys (anchor mass), and over all its keys (l, the blocks' lo + hi added as each
+// block ends).  K tiles go straight from global memory into a two-stage LDS ring
+// (LDS-DMA; keys at or past n read as 0), the next tile's load issued as the current
+// one is scored.  The running max is raised lazily: a tile's terms are formed against
+// the current max, and only when some lane's tile sum exceeds 2^8 (or is not finite,
+// or the row has no max yet) is the tile's true row max taken, the open sums scaled
+// down to it and the terms formed again -- until then every term is at most 2^8, which
+// float32 holds as exactly as terms below 1.  A block's (lo, hi) is written with the
+// max it was summed under when the block ends, and the range's (max, l, anchor) when
+// the range ends.
+__global__ __launch_bounds__(NT, 4) void est_pass(EstArgs a) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __shared__ __attribute__((aligned(1024))) char smem[2 * kTileBytes];
+  const int lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
+  // Workgroup i runs on XCD i % 8.  The G query heads of one (KV group, key range) take
+  // consecutive workgroups of one XCD, so they stream the same K tiles through that
+  // XCD's L2 at about the same time (K is read from HBM about once, not once per head).
+  const int xcd = blockIdx.x % kNumXcd, slot = blockIdx.x / kNumXcd;
+  const int pair = (slot / a.G) * kNumXcd + xcd;  // (KV group, range) pair, range fastest
+  if (pair >= (a.hq / a.G) * a.splits) return;
+  const int h = (pair / a.splits) * a.G + slot % a.G, sp = pair % a.splits;
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
   const int r = 32 * w + (l & 31);
   const int qi = a.n - a.b + r;
   const bool row_ok = r < a.b;
   bf16x8 qf[8];
   load_q_hat(a, h, r, l, qf);
-  const uint16_t* Kg = a.k + (size_t)(h / a.G) * a.n * kHeadDim;
+  Fetch<4> fe;
+  make_fetch<4>(fe, w, l);
+  const i32x4 rk = tensor_rsrc(a.k + (size_t)(h / a.G) * a.n * kHeadDim, a.n);
   const int J0 = sp * a.bps;
   const int J1 = (J0 + a.bps < a.nb) ? J0 + a.bps : a.nb;
   const int diag_off = a.b - 1 - r;  // key k of row r lies on the diagonal through (last row, k + diag_off)
   float m_run = -__builtin_inff(), l_run = 0.f, anc = 0.f;
-  int buf = 0;
-  u32x4 pre[4];
-  if (J0 < J1) load_k_regs(pre, Kg, J0 * a.B, a.n, tid);
-  for (int J = J0; J < J1; ++J) {
-    float lo = 0.f, hi = 0.f;
+  // tiles of the range in order: block J holds ceil(len / 64) tiles starting at J * B
+  const int tpb = a.B / BK;
+  const int key_end = J1 * a.B < a.n ? J1 * a.B : a.n;
+  const int T = J0 < J1 ? (key_end - J0 * a.B + BK - 1) / BK : 0;
+  if (T > 0) fetch_tile<4, BK>(fe, rk, lds0, J0 * a.B, w);
+  float lo = 0.f, hi = 0.f;
+  for (int t = 0; t < T; ++t) {
+    const int J = J0 + t / tpb;
+    const int key0 = J * a.B + (t % tpb) * BK;
     const int blo = J * a.B;
     const int bhi = blo + a.B < a.n ? blo + a.B : a.n;
     const int ksplit = (J + 1) * a.B - diag_off;  // keys >= this lie on diagonals of slash block J + 1
-    for (int key0 = blo; key0 < bhi; key0 += BK, buf ^= 1) {
-      char* kb = smem + buf * kTileBytes;
-      store_k_regs(kb, pre, tid);
-      const int next = key0 + BK < bhi ? key0 + BK : (J + 1 < J1 ? (J + 1) * a.B : a.n);
-      if (next < a.n) load_k_regs(pre, Kg, next, a.n, tid);
-      __syncthreads();
-      f32x16 s[2];
-      scores(kb, qf, l, s);
-      // Tiles wholly before the first proxy row, inside the block and outside both anchor
-      // windows (all but a few) need no per-entry masks and no anchor sum.
-      const bool plain = key0 + BK - 1 <= a.n - a.b && key0 + BK <= bhi && key0 >= a.w_sink &&
-                         key0 + BK <= a.n - a.w_local;
-      if (!plain) {
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int key = key_of(key0, mb, i, l);
-            if (!row_ok || key > qi || key >= bhi) s[mb][i] = -__builtin_inff();
-          }
-      }
-      float mx = -__builtin_inff();
+    wait_dma();
+    __syncthreads();  // tile t has landed for every wave; every wave is done with tile t - 1's stage
+    if (t + 1 < T) {
+      const int Jn = J0 + (t + 1) / tpb;
+      fetch_tile<4, BK>(fe, rk, lds0 + ((t + 1) & 1) * kTileBytes, Jn * a.B + ((t + 1) % tpb) * BK, w);
+    }
+    f32x16 s[2];
+    scores(lds0 + (t & 1) * kTileBytes, qf, l, s);
+    // Tiles wholly before the first proxy row, inside the block and outside both anchor
+    // windows (all but a few) need no per-entry masks and no anchor sum.
+    const bool plain = key0 + BK - 1 <= a.n - a.b && key0 + BK <= bhi && key0 >= a.w_sink &&
+                       key0 + BK <= a.n - a.w_local;
+    if (!plain) {
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[mb][i]);
-      mx = fmaxf(mx, swap_halves(mx));
-      if (mx > m_run) {  // the same in both lanes of a row
+        for (int i = 0; i < 16; ++i) {
+          const int key = key_of(key0, mb, i, l);
+          if (!row_ok || key > qi || key >= bhi) s[mb][i] = -__builtin_inff();
+        }
+    }
+    // In most tiles a whole wave's entries fall on one side of its rows' slash split
+    // (the split sits at key offset r + 1 of the block): one sum, no per-entry test.
+    const bool all_lo = __all(key0 + BK - 1 < ksplit), all_hi = __all(key0 >= ksplit);
+    float tlo = 0.f, thi = 0.f, tanc = 0.f;
+    // every entry tested against the slash split and the anchor windows (masked entries
+    // give exp2(-inf) = 0): the tiles that need it, and the rare tile that raises the max
+    auto general = [&](float mc) {
+      tlo = 0.f;
+      thi = 0.f;
+      tanc = 0.f;
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = key_of(key0, mb, i, l);
+          const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc));
+          if (key < ksplit) tlo += p; else thi += p;
+          if (key < a.w_sink || key >= a.n - a.w_local) tanc += p;
+        }
+    };
+    const float mc0 = m_run == -__builtin_inff() ? 0.f : m_run * a.c;
+    if (plain && (all_lo || all_hi)) {
+      float t0 = 0.f, t1 = 0.f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        t0 += fast_exp2(__builtin_fmaf(s[0][i], a.c, -mc0));
+        t1 += fast_exp2(__builtin_fmaf(s[1][i], a.c, -mc0));
+      }
+      if (all_lo) tlo = t0 + t1; else thi = t0 + t1;
+    } else if (plain) {
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc0));
+          if (key_of(key0, mb, i, l) < ksplit) tlo += p; else thi += p;
+        }
+    } else {
+      general(mc0);
+    }
+    const float tsum = tlo + thi;
+    if (__ballot(row_ok && (!(tsum <= kSumLimit) || m_run == -__builtin_inff()))) {
+      float mx = vmax(s[0][0], s[1][0]);
+#pragma unroll
+      for (int i = 1; i < 16; ++i) mx = vmax(mx, vmax(s[0][i], s[1][i]));
+      mx = vmax(mx, swap_halves(mx));  // the same in both lanes of a row
+      if (mx > m_run) {
         const float alpha = m_run == -__builtin_inff() ? 0.f : fast_exp2((m_run - mx) * a.c);
         l_run *= alpha;
         anc *= alpha;
@@ -149,45 +199,23 @@ __global__ __launch_bounds__(NT) void est_pass(EstArgs a) {
         hi *= alpha;
         m_run = mx;
       }
-      const float mc = m_run == -__builtin_inff() ? 0.f : m_run * a.c;
-      // In most tiles a whole wave's entries fall on one side of its rows' slash split
-      // (the split sits at key offset r + 1 of the block): one sum, no per-entry test.
-      const bool all_lo = __all(key0 + BK - 1 < ksplit), all_hi = __all(key0 >= ksplit);
-      if (plain && (all_lo || all_hi)) {
-        float t = 0.f;
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) t += fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc));
-        if (all_lo) lo += t; else hi += t;
-      } else if (plain) {
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc));
-            if (key_of(key0, mb, i, l) < ksplit) lo += p; else hi += p;
-          }
-      } else {
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int key = key_of(key0, mb, i, l);
-            const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc));  // masked: exp2(-inf) = 0
-            if (key < ksplit) lo += p; else hi += p;
-            if (key < a.w_sink || key >= a.n - a.w_local) anc += p;
-          }
-      }
+      general(m_run == -__builtin_inff() ? 0.f : m_run * a.c);
     }
-    l_run += lo + hi;  // the block's sum joins the row's, under the same running max
-    lo += swap_halves(lo);
-    hi += swap_halves(hi);
-    if (l < 32 && row_ok) a.parts[((size_t)h * a.nb + J) * 128 + r] = make_float4(lo, hi, m_run, 0.f);
+    lo += tlo;
+    hi += thi;
+    anc += tanc;
+    if ((t + 1) % tpb == 0 || t + 1 == T) {  // block J ends
+      l_run += lo + hi;  // the block's sum joins the row's, under the same running max
+      const float slo = lo + swap_halves(lo), shi = hi + swap_halves(hi);
+      if (l < 32 && row_ok) a.parts[((size_t)h * a.nb + J) * 128 + r] = make_float4(slo, shi, m_run, 0.f);
+      lo = 0.f;
+      hi = 0.f;
+    }
   }
   l_run += swap_halves(l_run);
   anc += swap_halves(anc);
   if (l < 32 && row_ok) a.rowstat[((size_t)h * a.splits + sp) * 128 + r] = make_float4(m_run, l_run, anc, 0.f);
+#endif
 }
 
 // Merges a range's (max m, sums l and anchor under m) into a running (M, L, A).
@@ -309,7 +337,8 @@ hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, 
   a.rowfinal = reinterpret_cast<float*>(ws + L.rowfinal);
   a.parts = reinterpret_cast<float4*>(ws + L.parts);
   a.c_struct = c_struct; a.p_v = p_v; a.p_s = p_s;
-  const int grid = d.hq * sp.splits;
+  const int pairs = d.hkv * sp.splits;  // (KV group, key range) pairs, spread over the XCDs
+  const int grid = kNumXcd * d.G * ((pairs + kNumXcd - 1) / kNumXcd);
   hipLaunchKernelGGL(est_pass, dim3(grid), dim3(NT), 0, stream, a);
   hipLaunchKernelGGL(est_combine, dim3(d.hq), dim3(1024), 0, stream, a);
   const int runs = (d.nb + kScaleRun - 1) / kScaleRun;

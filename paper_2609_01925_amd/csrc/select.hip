@@ -463,15 +463,20 @@ __global__ __launch_bounds__(256) void jsd_score(JsdArgs a) {
   if (tid == 0) a.jsd[h] = (float)sqrt(fmax(0.5 * t, 0.0));
 }
 
-// Pooled logits (log2 domain) on fp32 MFMA: 64 x 64 tiles of the block-causal
-// triangle, grid (ntri, hq), 256 threads; wave w computes the 32 x 32 sub-tile
-// (query blocks 32 (w >> 1) .., key blocks 32 (w & 1) ..) as 64 steps of
-// v_mfma_f32_32x32x2_f32.  The contraction over d is split between the half-waves:
-// at step t, lanes 0..31 contribute d = t and lanes 32..63 d = 64 + t, for A (Q_bar
-// rows) and B (K_bar rows) alike, so each lane streams 64 consecutive floats of its
-// row with 16-byte loads.  Output row m = 8 (i / 4) + 4 (lane / 32) + i % 4 of
-// register i, column = lane % 32.
+// Pooled logits (log2 domain) on fp32 MFMA (v_mfma_f32_32x32x2_f32): 128 x 128 tiles
+// of the block-causal triangle, grid (ntri, hq), 256 threads.  The contraction over d
+// runs in chunks of 16: each chunk of the tile's 128 Q_bar rows and 128 K_bar rows is
+// staged in LDS (two stages; the next chunk is loaded into registers while the current
+// one is multiplied), and wave w computes the 64 x 64 quarter (query blocks
+// 64 (w >> 1) .., key blocks 64 (w & 1) ..) as 2 x 2 accumulators of 32 x 32, so each
+// operand read from LDS serves two MFMAs.  Within a chunk lanes 0..31 take d = 0..7
+// and lanes 32..63 d = 8..15 (the same for Q_bar and K_bar, so the sum covers every d).
+// Output row m = 8 (i / 4) + 4 (lane / 32) + i % 4 of register i, column = lane % 32.
+constexpr int kLogitTile = 128, kLogitChunk = 16, kLogitPitch = kLogitChunk + 4;  // floats per LDS row
+
 __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
+  __shared__ __attribute__((aligned(16))) float lq[2][kLogitTile * kLogitPitch];
+  __shared__ __attribute__((aligned(16))) float lk[2][kLogitTile * kLogitPitch];
   const int h = blockIdx.y, tid = threadIdx.x;
   if (a.route[h] != 1) return;
   const int t = blockIdx.x;
@@ -480,36 +485,81 @@ __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
   while (qt * (qt + 1) / 2 > t) --qt;
   const int kt = t - qt * (qt + 1) / 2;
   const int w = tid >> 6, l = tid & 63;
-  const int qs0 = qt * 64 + 32 * (w >> 1), ks0 = kt * 64 + 32 * (w & 1);
-  if (ks0 > qs0 + 31 || qs0 >= a.nb) return;  // sub-tile wholly above the diagonal or past N_b
-  const int qrow = qs0 + (l & 31), krow = ks0 + (l & 31);
-  const int d0 = 64 * (l >> 5);
-  const float* Qr = a.qbar + ((size_t)h * a.nb + (qrow < a.nb ? qrow : 0)) * kHeadDim + d0;
-  const float* Kr = a.kbar + ((size_t)(h / a.G) * a.nb + (krow < a.nb ? krow : 0)) * kHeadDim + d0;
-  const bool qok = qrow < a.nb, kok = krow < a.nb;
-  f32x16 acc = zero16();
-#pragma unroll 2
-  for (int c = 0; c < 64; c += 16) {
-    float4 qa[4], ka[4];
+  const int q0 = qt * kLogitTile, k0 = kt * kLogitTile;
+  const int qs0 = q0 + 64 * (w >> 1), ks0 = k0 + 64 * (w & 1);
+  const bool work = ks0 <= qs0 + 63 && qs0 < a.nb;  // some pair of the quarter is causal
+  const float* Qb = a.qbar + (size_t)h * a.nb * kHeadDim;
+  const float* Kb = a.kbar + (size_t)(h / a.G) * a.nb * kHeadDim;
+  // staging: thread tid moves float4 number tid + 256 u of the chunk, u = 0, 1 for Q_bar
+  // (rows (tid + 256 u) / 4, columns 4 ((tid + 256 u) % 4)) and likewise for K_bar
+  float4 rq[2], rk[2];
+  auto load = [&](int c) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      qa[u] = qok ? *reinterpret_cast<const float4*>(Qr + c + 4 * u) : make_float4(0.f, 0.f, 0.f, 0.f);
-      ka[u] = kok ? *reinterpret_cast<const float4*>(Kr + c + 4 * u) : make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int u = 0; u < 2; ++u) {
+      const int f = tid + 256 * u, row = f >> 2, col = c * kLogitChunk + 4 * (f & 3);
+      rq[u] = q0 + row < a.nb ? *reinterpret_cast<const float4*>(Qb + (size_t)(q0 + row) * kHeadDim + col)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
+      rk[u] = k0 + row < a.nb ? *reinterpret_cast<const float4*>(Kb + (size_t)(k0 + row) * kHeadDim + col)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
     }
+  };
+  auto store = [&](int st) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].x, ka[u].x, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].y, ka[u].y, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].z, ka[u].z, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].w, ka[u].w, acc, 0, 0, 0);
+    for (int u = 0; u < 2; ++u) {
+      const int f = tid + 256 * u, row = f >> 2, col = 4 * (f & 3);
+      *reinterpret_cast<float4*>(&lq[st][row * kLogitPitch + col]) = rq[u];
+      *reinterpret_cast<float4*>(&lk[st][row * kLogitPitch + col]) = rk[u];
+    }
+  };
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = zero16();
+  constexpr int kChunks = kHeadDim / kLogitChunk;
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int c = 0; c < kChunks; ++c) {
+    if (c + 1 < kChunks) load(c + 1);
+    if (work) {
+      const int st = c & 1, dl = 8 * (l >> 5);
+      float av[2][8], bv[2][8];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const float* qa = &lq[st][(64 * (w >> 1) + 32 * i + (l & 31)) * kLogitPitch + dl];
+        const float* kbp = &lk[st][(64 * (w & 1) + 32 * i + (l & 31)) * kLogitPitch + dl];
+        const float4 x0 = *reinterpret_cast<const float4*>(qa), x1 = *reinterpret_cast<const float4*>(qa + 4);
+        const float4 y0 = *reinterpret_cast<const float4*>(kbp), y1 = *reinterpret_cast<const float4*>(kbp + 4);
+        av[i][0] = x0.x; av[i][1] = x0.y; av[i][2] = x0.z; av[i][3] = x0.w;
+        av[i][4] = x1.x; av[i][5] = x1.y; av[i][6] = x1.z; av[i][7] = x1.w;
+        bv[i][0] = y0.x; bv[i][1] = y0.y; bv[i][2] = y0.z; bv[i][3] = y0.w;
+        bv[i][4] = y1.x; bv[i][5] = y1.y; bv[i][6] = y1.z; bv[i][7] = y1.w;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][u], bv[j][u], acc[i][j], 0, 0, 0);
+    }
+    if (c + 1 < kChunks) {
+      store((c + 1) & 1);  // that stage was last read in chunk c - 1, before the barrier below it
+      __syncthreads();
     }
   }
+  if (!work) return;
   float* At = a.atil + (size_t)h * a.cap;
-  const int kb = ks0 + (l & 31);
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int qb = qs0 + 8 * (i >> 2) + 4 * (l >> 5) + (i & 3);
-    if (qb < a.nb && kb <= qb) At[(int64_t)qb * (qb + 1) / 2 + kb] = acc[i] * a.c2;
+  for (int j = 0; j < 2; ++j) {
+    const int kb = ks0 + 32 * j + (l & 31);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int qb = qs0 + 32 * i + 8 * (r >> 2) + 4 * (l >> 5) + (r & 3);
+        if (qb < a.nb && kb <= qb) At[(int64_t)qb * (qb + 1) / 2 + kb] = acc[i][j][r] * a.c2;
+      }
   }
 }
 
@@ -893,7 +943,7 @@ hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, flo
   const int nb = d.nb;
   hipLaunchKernelGGL(sel_route_vs, dim3(d.hq, 2), dim3(1024), 0, stream, a);
   hipLaunchKernelGGL(sel_pool, dim3(nb, d.hq + d.hkv), dim3(256), 0, stream, a);
-  const int nt = (nb + 63) / 64;
+  const int nt = (nb + kLogitTile - 1) / kLogitTile;
   hipLaunchKernelGGL(sel_pe_logits, dim3(nt * (nt + 1) / 2, d.hq), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(sel_pe_softmax, dim3(nb, d.hq), dim3(256), 0, stream, a);
   if (d.cap <= kSmallCap) {
