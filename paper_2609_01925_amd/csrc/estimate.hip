@@ -238,9 +238,8 @@ __device__ __forceinline__ void merge_stats(float& M, float& L, float& A, float 
 // the row's normaliser mcl = M c + log2 L for the block sums, and C_struct = (1/b)
 // sum over rows of the row's anchor mass / L, summed over rows in a fixed order.
 // 1024 threads.
-__global__ __launch_bounds__(1024) void est_combine(EstArgs a) {
-  __shared__ float red[128];
-  const int h = blockIdx.x, j = threadIdx.x & 7, r = threadIdx.x >> 3;
+__device__ __forceinline__ void combine_head(const EstArgs& a, int h, float* red) {
+  const int j = threadIdx.x & 7, r = threadIdx.x >> 3;
   const float4* src = a.rowstat + (size_t)h * a.splits * 128 + r;
   const bool row_ok = r < a.b;
   float M = -__builtin_inff(), L = 0.f, A = 0.f;
@@ -266,15 +265,16 @@ __global__ __launch_bounds__(1024) void est_combine(EstArgs a) {
   }
 }
 
+__global__ __launch_bounds__(1024) void est_combine(EstArgs a) {
+  __shared__ float red[128];
+  combine_head(a, blockIdx.x, red);
+}
+
 // p_v[J] = (1/b) sum_r (lo + hi)[r][J] 2^(m c - mcl_r);  p_s[J] = (1/b) sum_r (lo[r][J] +
-// hi[r][J - 1]) scaled alike.  Each wave takes kScaleRun consecutive blocks, lanes take
-// rows l and l + 64, and a block's row sum is a fixed-order butterfly.
-constexpr int kScaleRun = 2;
-__global__ __launch_bounds__(256) void est_scale(EstArgs a) {
-  const int h = blockIdx.x, l = threadIdx.x & 63;
-  const int Ja = (blockIdx.y * 4 + (threadIdx.x >> 6)) * kScaleRun;
-  if (Ja >= a.nb) return;
-  const int Jb = Ja + kScaleRun < a.nb ? Ja + kScaleRun : a.nb;
+// hi[r][J - 1]) scaled alike, for the run of blocks [Ja, Jb) of head h, by one wave:
+// lanes take rows l and l + 64, and a block's row sum is a fixed-order butterfly.
+__device__ __forceinline__ void scale_run(const EstArgs& a, int h, int Ja, int Jb) {
+  const int l = threadIdx.x & 63;
   const bool ok0 = l < a.b, ok1 = l + 64 < a.b;
   const float mcl0 = ok0 ? a.rowfinal[(size_t)h * 128 + l] : 0.f;
   const float mcl1 = ok1 ? a.rowfinal[(size_t)h * 128 + l + 64] : 0.f;
@@ -308,13 +308,34 @@ __global__ __launch_bounds__(256) void est_scale(EstArgs a) {
   }
 }
 
+// Each wave takes kScaleRun consecutive blocks.  grid (hq, ceil(runs / 4)), 256 threads.
+constexpr int kScaleRun = 2;
+__global__ __launch_bounds__(256) void est_scale(EstArgs a) {
+  const int Ja = (blockIdx.y * 4 + (threadIdx.x >> 6)) * kScaleRun;
+  if (Ja >= a.nb) return;
+  scale_run(a, blockIdx.x, Ja, Ja + kScaleRun < a.nb ? Ja + kScaleRun : a.nb);
+}
+
+// Short layers (N_b <= kFinishSmall): combine and scale of one head in one launch (the
+// 16 waves then take runs of blocks; the same sums in the same order as the two
+// kernels above).  grid hq, 1024 threads.
+constexpr int kFinishSmall = 32;
+__global__ __launch_bounds__(1024) void est_finish(EstArgs a) {
+  __shared__ float red[128];
+  const int h = blockIdx.x;
+  combine_head(a, h, red);
+  __syncthreads();  // rowfinal of every row is visible to the whole workgroup
+  for (int Ja = (threadIdx.x >> 6) * kScaleRun; Ja < a.nb; Ja += 16 * kScaleRun)
+    scale_run(a, h, Ja, Ja + kScaleRun < a.nb ? Ja + kScaleRun : a.nb);
+}
+
 }  // namespace
 
 EstSplit est_split(const Dims& d) {
   EstSplit s;
-  const int64_t want = 2048;  // target workgroups of the pass
+  const int64_t want = 1024;  // target workgroups of the pass: about one resident round (4 per CU)
   int64_t bps = ((int64_t)d.nb * d.hq + want - 1) / want;
-  if (bps < 4) bps = 4;  // short layers: fewer, longer ranges (each range loads Q_hat once)
+  if (bps < 1) bps = 1;
   s.bps = (int)bps;
   s.splits = (d.nb + s.bps - 1) / s.bps;
   if (s.splits < 1) s.splits = 1;
@@ -340,9 +361,13 @@ hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, 
   const int pairs = d.hkv * sp.splits;  // (KV group, key range) pairs, spread over the XCDs
   const int grid = kNumXcd * d.G * ((pairs + kNumXcd - 1) / kNumXcd);
   hipLaunchKernelGGL(est_pass, dim3(grid), dim3(NT), 0, stream, a);
-  hipLaunchKernelGGL(est_combine, dim3(d.hq), dim3(1024), 0, stream, a);
-  const int runs = (d.nb + kScaleRun - 1) / kScaleRun;
-  hipLaunchKernelGGL(est_scale, dim3(d.hq, (runs + 3) / 4), dim3(256), 0, stream, a);
+  if (d.nb <= kFinishSmall) {
+    hipLaunchKernelGGL(est_finish, dim3(d.hq), dim3(1024), 0, stream, a);
+  } else {
+    hipLaunchKernelGGL(est_combine, dim3(d.hq), dim3(1024), 0, stream, a);
+    const int runs = (d.nb + kScaleRun - 1) / kScaleRun;
+    hipLaunchKernelGGL(est_scale, dim3(d.hq, (runs + 3) / 4), dim3(256), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

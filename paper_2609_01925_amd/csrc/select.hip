@@ -463,20 +463,18 @@ __global__ __launch_bounds__(256) void jsd_score(JsdArgs a) {
   if (tid == 0) a.jsd[h] = (float)sqrt(fmax(0.5 * t, 0.0));
 }
 
-// Pooled logits (log2 domain) on fp32 MFMA (v_mfma_f32_32x32x2_f32): 128 x 128 tiles
-// of the block-causal triangle, grid (ntri, hq), 256 threads.  The contraction over d
-// runs in chunks of 16: each chunk of the tile's 128 Q_bar rows and 128 K_bar rows is
-// staged in LDS (two stages; the next chunk is loaded into registers while the current
-// one is multiplied), and wave w computes the 64 x 64 quarter (query blocks
-// 64 (w >> 1) .., key blocks 64 (w & 1) ..) as 2 x 2 accumulators of 32 x 32, so each
-// operand read from LDS serves two MFMAs.  Within a chunk lanes 0..31 take d = 0..7
-// and lanes 32..63 d = 8..15 (the same for Q_bar and K_bar, so the sum covers every d).
-// Output row m = 8 (i / 4) + 4 (lane / 32) + i % 4 of register i, column = lane % 32.
-constexpr int kLogitTile = 128, kLogitChunk = 16, kLogitPitch = kLogitChunk + 4;  // floats per LDS row
-
-__global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
-  __shared__ __attribute__((aligned(16))) float lq[2][kLogitTile * kLogitPitch];
-  __shared__ __attribute__((aligned(16))) float lk[2][kLogitTile * kLogitPitch];
+constexpr int kLogitDirect = 512;
+// Pooled logits for mid-size layers (kPeSmall < N_b <= kLogitDirect), where the tiles
+// are few and short and staging them in LDS costs more latency than it saves: 64 x 64
+// tiles of the block-causal triangle, grid (ntri, hq), 256 threads, operands streamed
+// from L2; wave w computes the 32 x 32 sub-tile
+// (query blocks 32 (w >> 1) .., key blocks 32 (w & 1) ..) as 64 steps of
+// v_mfma_f32_32x32x2_f32.  The contraction over d is split between the half-waves:
+// at step t, lanes 0..31 contribute d = t and lanes 32..63 d = 64 + t, for A (Q_bar
+// rows) and B (K_bar rows) alike, so each lane streams 64 consecutive floats of its
+// row with 16-byte loads.  Output row m = 8 (i / 4) + 4 (lane / 32) + i % 4 of
+// register i, column = lane % 32.
+__global__ __launch_bounds__(256) void sel_pe_logits_direct(SelArgs a) {
   const int h = blockIdx.y, tid = threadIdx.x;
   if (a.route[h] != 1) return;
   const int t = blockIdx.x;
@@ -485,17 +483,76 @@ __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
   while (qt * (qt + 1) / 2 > t) --qt;
   const int kt = t - qt * (qt + 1) / 2;
   const int w = tid >> 6, l = tid & 63;
-  const int q0 = qt * kLogitTile, k0 = kt * kLogitTile;
-  const int qs0 = q0 + 64 * (w >> 1), ks0 = k0 + 64 * (w & 1);
-  const bool work = ks0 <= qs0 + 63 && qs0 < a.nb;  // some pair of the quarter is causal
+  const int qs0 = qt * 64 + 32 * (w >> 1), ks0 = kt * 64 + 32 * (w & 1);
+  if (ks0 > qs0 + 31 || qs0 >= a.nb) return;  // sub-tile wholly above the diagonal or past N_b
+  const int qrow = qs0 + (l & 31), krow = ks0 + (l & 31);
+  const int d0 = 64 * (l >> 5);
+  const float* Qr = a.qbar + ((size_t)h * a.nb + (qrow < a.nb ? qrow : 0)) * kHeadDim + d0;
+  const float* Kr = a.kbar + ((size_t)(h / a.G) * a.nb + (krow < a.nb ? krow : 0)) * kHeadDim + d0;
+  const bool qok = qrow < a.nb, kok = krow < a.nb;
+  f32x16 acc = zero16();
+#pragma unroll 2
+  for (int c = 0; c < 64; c += 16) {
+    float4 qa[4], ka[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      qa[u] = qok ? *reinterpret_cast<const float4*>(Qr + c + 4 * u) : make_float4(0.f, 0.f, 0.f, 0.f);
+      ka[u] = kok ? *reinterpret_cast<const float4*>(Kr + c + 4 * u) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].x, ka[u].x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].y, ka[u].y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].z, ka[u].z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[u].w, ka[u].w, acc, 0, 0, 0);
+    }
+  }
+  float* At = a.atil + (size_t)h * a.cap;
+  const int kb = ks0 + (l & 31);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int qb = qs0 + 8 * (i >> 2) + 4 * (l >> 5) + (i & 3);
+    if (qb < a.nb && kb <= qb) At[(int64_t)qb * (qb + 1) / 2 + kb] = acc[i] * a.c2;
+  }
+}
+
+// Pooled logits (log2 domain) on fp32 MFMA (v_mfma_f32_32x32x2_f32): tiles of
+// 2 WT x 2 WT (query block, key block) pairs of the block-causal triangle, grid
+// (ntri, hq), 256 threads.  The contraction over d runs in chunks of 16: each chunk of
+// the tile's Q_bar and K_bar rows is staged in LDS (two stages; the next chunk is
+// loaded into registers while the current one is multiplied), and wave w computes the
+// WT x WT quarter (query blocks WT (w >> 1) .., key blocks WT (w & 1) ..) as
+// (WT / 32)^2 accumulators of 32 x 32, so with WT = 64 each operand read from LDS
+// serves two MFMAs (WT = 32, for short layers, keeps four waves busy on a small
+// triangle).  Within a chunk lanes 0..31 take d = 0..7 and lanes 32..63 d = 8..15 (the
+// same for Q_bar and K_bar, so the sum covers every d).  Output row m = 8 (i / 4) +
+// 4 (lane / 32) + i % 4 of register i, column = lane % 32.
+constexpr int kLogitChunk = 16, kLogitPitch = kLogitChunk + 4;  // floats per LDS row
+
+template <int WT>
+__global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
+  constexpr int TILE = 2 * WT, NA = WT / 32, U = TILE * 4 / 256;  // float4 per thread per tensor and chunk
+  __shared__ __attribute__((aligned(16))) float lq[2][TILE * kLogitPitch];
+  __shared__ __attribute__((aligned(16))) float lk[2][TILE * kLogitPitch];
+  const int h = blockIdx.y, tid = threadIdx.x;
+  if (a.route[h] != 1) return;
+  const int t = blockIdx.x;
+  int qt = (int)((sqrtf(8.f * (float)t + 1.f) - 1.f) * 0.5f);
+  while ((qt + 1) * (qt + 2) / 2 <= t) ++qt;
+  while (qt * (qt + 1) / 2 > t) --qt;
+  const int kt = t - qt * (qt + 1) / 2;
+  const int w = tid >> 6, l = tid & 63;
+  const int q0 = qt * TILE, k0 = kt * TILE;
+  const int qs0 = q0 + WT * (w >> 1), ks0 = k0 + WT * (w & 1);
+  const bool work = ks0 <= qs0 + WT - 1 && qs0 < a.nb;  // some pair of the quarter is causal
   const float* Qb = a.qbar + (size_t)h * a.nb * kHeadDim;
   const float* Kb = a.kbar + (size_t)(h / a.G) * a.nb * kHeadDim;
-  // staging: thread tid moves float4 number tid + 256 u of the chunk, u = 0, 1 for Q_bar
-  // (rows (tid + 256 u) / 4, columns 4 ((tid + 256 u) % 4)) and likewise for K_bar
-  float4 rq[2], rk[2];
+  // staging: thread tid moves float4 number tid + 256 u of the chunk (row (tid + 256 u) / 4,
+  // columns 4 ((tid + 256 u) % 4)) of Q_bar and likewise of K_bar
+  float4 rq[U], rk[U];
   auto load = [&](int c) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < U; ++u) {
       const int f = tid + 256 * u, row = f >> 2, col = c * kLogitChunk + 4 * (f & 3);
       rq[u] = q0 + row < a.nb ? *reinterpret_cast<const float4*>(Qb + (size_t)(q0 + row) * kHeadDim + col)
                               : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -505,17 +562,17 @@ __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
   };
   auto store = [&](int st) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < U; ++u) {
       const int f = tid + 256 * u, row = f >> 2, col = 4 * (f & 3);
       *reinterpret_cast<float4*>(&lq[st][row * kLogitPitch + col]) = rq[u];
       *reinterpret_cast<float4*>(&lk[st][row * kLogitPitch + col]) = rk[u];
     }
   };
-  f32x16 acc[2][2];
+  f32x16 acc[NA][NA];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < NA; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = zero16();
+    for (int j = 0; j < NA; ++j) acc[i][j] = zero16();
   constexpr int kChunks = kHeadDim / kLogitChunk;
   load(0);
   store(0);
@@ -524,11 +581,11 @@ __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
     if (c + 1 < kChunks) load(c + 1);
     if (work) {
       const int st = c & 1, dl = 8 * (l >> 5);
-      float av[2][8], bv[2][8];
+      float av[NA][8], bv[NA][8];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const float* qa = &lq[st][(64 * (w >> 1) + 32 * i + (l & 31)) * kLogitPitch + dl];
-        const float* kbp = &lk[st][(64 * (w & 1) + 32 * i + (l & 31)) * kLogitPitch + dl];
+      for (int i = 0; i < NA; ++i) {
+        const float* qa = &lq[st][(WT * (w >> 1) + 32 * i + (l & 31)) * kLogitPitch + dl];
+        const float* kbp = &lk[st][(WT * (w & 1) + 32 * i + (l & 31)) * kLogitPitch + dl];
         const float4 x0 = *reinterpret_cast<const float4*>(qa), x1 = *reinterpret_cast<const float4*>(qa + 4);
         const float4 y0 = *reinterpret_cast<const float4*>(kbp), y1 = *reinterpret_cast<const float4*>(kbp + 4);
         av[i][0] = x0.x; av[i][1] = x0.y; av[i][2] = x0.z; av[i][3] = x0.w;
@@ -539,9 +596,9 @@ __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
 #pragma unroll
       for (int u = 0; u < 8; ++u)
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < NA; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][u], bv[j][u], acc[i][j], 0, 0, 0);
+          for (int j = 0; j < NA; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][u], bv[j][u], acc[i][j], 0, 0, 0);
     }
     if (c + 1 < kChunks) {
       store((c + 1) & 1);  // that stage was last read in chunk c - 1, before the barrier below it
@@ -550,16 +607,85 @@ __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
   }
   if (!work) return;
   float* At = a.atil + (size_t)h * a.cap;
+  {
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int kb = ks0 + 32 * j + (l & 31);
+    for (int j = 0; j < NA; ++j) {
+      const int kb = ks0 + 32 * j + (l & 31);
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < NA; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int qb = qs0 + 32 * i + 8 * (r >> 2) + 4 * (l >> 5) + (r & 3);
-        if (qb < a.nb && kb <= qb) At[(int64_t)qb * (qb + 1) / 2 + kb] = acc[i][j][r] * a.c2;
-      }
+        for (int r = 0; r < 16; ++r) {
+          const int qb = qs0 + 32 * i + 8 * (r >> 2) + 4 * (l >> 5) + (r & 3);
+          if (qb < a.nb && kb <= qb) At[(int64_t)qb * (qb + 1) / 2 + kb] = acc[i][j][r] * a.c2;
+        }
+    }
+  }
+}
+
+// Short layers (N_b <= kPeSmall): the whole pooled triangle of one PE head in one
+// workgroup.  Q_bar and K_bar rows go to LDS once (float4 columns swizzled by row so the
+// operand reads of 32 rows spread over the banks), wave w computes the 32 x 32 quarter
+// (query blocks 32 (w >> 1) .., key blocks 32 (w & 1) ..) on fp32 MFMA with the same d
+// split as sel_pe_logits, the logits go back to LDS, and each wave takes the row softmax
+// (divided by N_b) of every fourth row from there.  grid hq, 256 threads.
+constexpr int kPeSmall = 64, kPeSmallPitch = kPeSmall + 1;
+
+__global__ __launch_bounds__(256) void sel_pe_small(SelArgs a) {
+  __shared__ __attribute__((aligned(16))) float sq[kPeSmall * kHeadDim];  // reused for the logits
+  __shared__ __attribute__((aligned(16))) float sk[kPeSmall * kHeadDim];
+  const int h = blockIdx.x, tid = threadIdx.x;
+  if (a.route[h] != 1) return;
+  const int w = tid >> 6, l = tid & 63, nb = a.nb;
+  const float* Qb = a.qbar + (size_t)h * nb * kHeadDim;
+  const float* Kb = a.kbar + (size_t)(h / a.G) * nb * kHeadDim;
+  auto phys = [](int r, int c4) { return r * kHeadDim + 4 * (c4 ^ (r & 31)); };
+  for (int f = tid; f < kPeSmall * kHeadDim / 4; f += 256) {  // kPeSmall rows x 32 float4
+    const int r = f >> 5, c4 = f & 31;
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    *reinterpret_cast<float4*>(&sq[phys(r, c4)]) =
+        r < nb ? *reinterpret_cast<const float4*>(Qb + (size_t)r * kHeadDim + 4 * c4) : z;
+    *reinterpret_cast<float4*>(&sk[phys(r, c4)]) =
+        r < nb ? *reinterpret_cast<const float4*>(Kb + (size_t)r * kHeadDim + 4 * c4) : z;
+  }
+  __syncthreads();
+  const int qs0 = 32 * (w >> 1), ks0 = 32 * (w & 1);
+  const bool work = ks0 <= qs0 && qs0 < nb;
+  f32x16 acc = zero16();
+  if (work) {
+    const int qr = qs0 + (l & 31), kr = ks0 + (l & 31);
+#pragma unroll
+    for (int c = 0; c < kHeadDim / 16; ++c) {
+      const int c4 = 4 * c + 2 * (l >> 5);  // lanes 0..31: d 16 c .. +7; lanes 32..63: d 16 c + 8 .. +15
+      const float4 x0 = *reinterpret_cast<const float4*>(&sq[phys(qr, c4)]);
+      const float4 x1 = *reinterpret_cast<const float4*>(&sq[phys(qr, c4 + 1)]);
+      const float4 y0 = *reinterpret_cast<const float4*>(&sk[phys(kr, c4)]);
+      const float4 y1 = *reinterpret_cast<const float4*>(&sk[phys(kr, c4 + 1)]);
+      const float av[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+      const float bv[8] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[u], bv[u], acc, 0, 0, 0);
+    }
+  }
+  __syncthreads();  // every operand read is done before the logits overwrite sq
+  float* lg = sq;
+  if (work) {
+    const int kb = ks0 + (l & 31);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int qb = qs0 + 8 * (r >> 2) + 4 * (l >> 5) + (r & 3);
+      lg[qb * kPeSmallPitch + kb] = acc[r] * a.c2;
+    }
+  }
+  __syncthreads();
+  float* At = a.atil + (size_t)h * a.cap;
+  const float inv_nb = 1.f / (float)nb;
+  for (int qb = w; qb < nb; qb += 4) {
+    const bool in = l <= qb;
+    const float x = in ? lg[qb * kPeSmallPitch + l] : -__builtin_inff();
+    const float mx = wave_max(x);
+    const float p = in ? fast_exp2(x - mx) : 0.f;
+    const float sum = wave_sum(p);
+    if (in) At[(int64_t)qb * (qb + 1) / 2 + l] = p / sum * inv_nb;
   }
 }
 
@@ -736,10 +862,8 @@ __global__ __launch_bounds__(1024) void sel_radix_small(SelArgs a) {
 // Per-row counts.  VS: x = row size.  PE: x = #(> t*), y = #(== t*), z = flags
 // (1: block 0 > t*, 2: block 0 == t*, 4: block qb > t*, 8: block qb == t*).
 // grid (ceil(nb / 4), hq), 256 threads, one wave per row.
-__global__ __launch_bounds__(256) void sel_csr_count(SelArgs a) {
-  const int h = blockIdx.y, w = threadIdx.x >> 6, l = threadIdx.x & 63;
-  const int qb = blockIdx.x * 4 + w;
-  if (qb >= a.nb) return;
+__device__ __forceinline__ void csr_count_row(const SelArgs& a, int h, int qb) {
+  const int l = threadIdx.x & 63;
   const int nb = a.nb;
   int4 info = make_int4(0, 0, 0, 0);
   if (a.route[h] == 0) {
@@ -774,10 +898,14 @@ __global__ __launch_bounds__(256) void sel_csr_count(SelArgs a) {
   if (l == 0) a.rowinfo[(size_t)h * nb + qb] = info;
 }
 
+__global__ __launch_bounds__(256) void sel_csr_count(SelArgs a) {
+  const int qb = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (qb < a.nb) csr_count_row(a, blockIdx.y, qb);
+}
+
 // Ties taken per PE row, row sizes and the exclusive scan into row_ptr.  grid hq, 1024 threads.
-__global__ __launch_bounds__(1024) void sel_csr_scan(SelArgs a) {
-  __shared__ long long wtot[16];
-  const int h = blockIdx.x, tid = threadIdx.x, w = tid >> 6;
+__device__ __forceinline__ void csr_scan_head(const SelArgs& a, int h, long long* wtot) {
+  const int tid = threadIdx.x, w = tid >> 6;
   const int nb = a.nb;
   const bool pe = a.route[h] == 1;
   const RState st = pe ? a.rstate[h] : RState{};
@@ -840,11 +968,14 @@ __global__ __launch_bounds__(1024) void sel_csr_scan(SelArgs a) {
   if (tid == 0) rp[nb] = (int32_t)row_carry;
 }
 
+__global__ __launch_bounds__(1024) void sel_csr_scan(SelArgs a) {
+  __shared__ long long wtot[16];
+  csr_scan_head(a, blockIdx.x, wtot);
+}
+
 // Write the block lists.  grid (ceil(nb / 4), hq), 256 threads, one wave per row.
-__global__ __launch_bounds__(256) void sel_csr_fill(SelArgs a) {
-  const int h = blockIdx.y, w = threadIdx.x >> 6, l = threadIdx.x & 63;
-  const int qb = blockIdx.x * 4 + w;
-  if (qb >= a.nb) return;
+__device__ __forceinline__ void csr_fill_row(const SelArgs& a, int h, int qb) {
+  const int l = threadIdx.x & 63;
   const int nb = a.nb;
   int32_t* out = a.col_idx + (size_t)h * a.col_cap + a.row_ptr[(size_t)h * (nb + 1) + qb];
   const uint64_t lt = lanemask_lt();
@@ -878,6 +1009,25 @@ __global__ __launch_bounds__(256) void sel_csr_fill(SelArgs a) {
       pos += __popcll(bal);
     }
   }
+}
+
+__global__ __launch_bounds__(256) void sel_csr_fill(SelArgs a) {
+  const int qb = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (qb < a.nb) csr_fill_row(a, blockIdx.y, qb);
+}
+
+// Short layers (N_b <= kCsrSmall): count, scan and fill of one head in one launch, the
+// 16 waves taking rows w, w + 16, ... (the same lists as the three kernels above).
+// grid hq, 1024 threads.
+constexpr int kCsrSmall = 64;
+__global__ __launch_bounds__(1024) void sel_csr_small(SelArgs a) {
+  __shared__ long long wtot[16];
+  const int h = blockIdx.x, w = threadIdx.x >> 6;
+  for (int qb = w; qb < a.nb; qb += 16) csr_count_row(a, h, qb);
+  __syncthreads();  // every row's counts are visible to the whole workgroup
+  csr_scan_head(a, h, wtot);
+  __syncthreads();  // row_ptr and the ties taken per row are visible
+  for (int qb = w; qb < a.nb; qb += 16) csr_fill_row(a, h, qb);
 }
 
 }  // namespace
@@ -943,9 +1093,18 @@ hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, flo
   const int nb = d.nb;
   hipLaunchKernelGGL(sel_route_vs, dim3(d.hq, 2), dim3(1024), 0, stream, a);
   hipLaunchKernelGGL(sel_pool, dim3(nb, d.hq + d.hkv), dim3(256), 0, stream, a);
-  const int nt = (nb + kLogitTile - 1) / kLogitTile;
-  hipLaunchKernelGGL(sel_pe_logits, dim3(nt * (nt + 1) / 2, d.hq), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(sel_pe_softmax, dim3(nb, d.hq), dim3(256), 0, stream, a);
+  if (nb <= kPeSmall) {  // logits and softmax of the whole triangle in one launch
+    hipLaunchKernelGGL(sel_pe_small, dim3(d.hq), dim3(256), 0, stream, a);
+  } else {
+    if (nb <= kLogitDirect) {
+      const int nt = (nb + 63) / 64;
+      hipLaunchKernelGGL(sel_pe_logits_direct, dim3(nt * (nt + 1) / 2, d.hq), dim3(256), 0, stream, a);
+    } else {
+      const int nt = (nb + 127) / 128;
+      hipLaunchKernelGGL(sel_pe_logits<64>, dim3(nt * (nt + 1) / 2, d.hq), dim3(256), 0, stream, a);
+    }
+    hipLaunchKernelGGL(sel_pe_softmax, dim3(nb, d.hq), dim3(256), 0, stream, a);
+  }
   if (d.cap <= kSmallCap) {
     hipLaunchKernelGGL(sel_radix_small, dim3(d.hq), dim3(1024), 0, stream, a);
   } else {
@@ -958,10 +1117,14 @@ hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, flo
       hipLaunchKernelGGL(sel_radix_scan, dim3(d.hq), dim3(256), 0, stream, a, pass);
     }
   }
-  const int rows_grid = (nb + 3) / 4;
-  hipLaunchKernelGGL(sel_csr_count, dim3(rows_grid, d.hq), dim3(256), 0, stream, a);
-  hipLaunchKernelGGL(sel_csr_scan, dim3(d.hq), dim3(1024), 0, stream, a);
-  hipLaunchKernelGGL(sel_csr_fill, dim3(rows_grid, d.hq), dim3(256), 0, stream, a);
+  if (nb <= kCsrSmall) {
+    hipLaunchKernelGGL(sel_csr_small, dim3(d.hq), dim3(1024), 0, stream, a);
+  } else {
+    const int rows_grid = (nb + 3) / 4;
+    hipLaunchKernelGGL(sel_csr_count, dim3(rows_grid, d.hq), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(sel_csr_scan, dim3(d.hq), dim3(1024), 0, stream, a);
+    hipLaunchKernelGGL(sel_csr_fill, dim3(rows_grid, d.hq), dim3(256), 0, stream, a);
+  }
   return hipGetLastError();
 }
 
