@@ -116,7 +116,10 @@ __global__ __launch_bounds__(NT, 4) void est_pass(EstArgs a) {
   const int tpb = a.B / BK;
   const int key_end = J1 * a.B < a.n ? J1 * a.B : a.n;
   const int T = J0 < J1 ? (key_end - J0 * a.B + BK - 1) / BK : 0;
+  // the first two tiles are loaded together (one latency for ranges of two tiles);
+  // after that each step loads the tile after the current one
   if (T > 0) fetch_tile<4, BK>(fe, rk, lds0, J0 * a.B, w);
+  if (T > 1) fetch_tile<4, BK>(fe, rk, lds0 + kTileBytes, (J0 + 1 / tpb) * a.B + (1 % tpb) * BK, w);
   float lo = 0.f, hi = 0.f;
   for (int t = 0; t < T; ++t) {
     const int J = J0 + t / tpb;
@@ -126,7 +129,7 @@ __global__ __launch_bounds__(NT, 4) void est_pass(EstArgs a) {
     const int ksplit = (J + 1) * a.B - diag_off;  // keys >= this lie on diagonals of slash block J + 1
     wait_dma();
     __syncthreads();  // tile t has landed for every wave; every wave is done with tile t - 1's stage
-    if (t + 1 < T) {
+    if (t >= 1 && t + 1 < T) {
       const int Jn = J0 + (t + 1) / tpb;
       fetch_tile<4, BK>(fe, rk, lds0 + ((t + 1) & 1) * kTileBytes, Jn * a.B + ((t + 1) % tpb) * BK, w);
     }

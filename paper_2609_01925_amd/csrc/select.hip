@@ -261,15 +261,24 @@ __device__ int gamma_prefix(const float* p, int nb, float gamma, uint32_t* t_out
   return gt + ceq;
 }
 
-// Route (Alg. 2, or App. A's pattern search when the score is D_JS) and VS selection
-// per direction (Alg. 3, or App. A's gamma coverage).  grid (hq, 2), 1024 threads.
-__global__ __launch_bounds__(1024) void sel_route_vs(SelArgs a) {
-  __shared__ uint32_t hist[256];
-  __shared__ unsigned long long hist64[2048];
-  __shared__ unsigned long long sh64[2];
-  __shared__ int wtot[16];
-  __shared__ int sh[2];
-  const int h = blockIdx.x, dir = blockIdx.y, tid = threadIdx.x;
+// Shared memory of one direction's VS selection.
+struct VsShared {
+  uint32_t hist[256];
+  unsigned long long hist64[2048];
+  unsigned long long sh64[2];
+  int wtot[16];
+  int sh[2];
+};
+
+// Route (Alg. 2, or App. A's pattern search when the score is D_JS) and VS selection of
+// direction dir (Alg. 3, or App. A's gamma coverage) of head h.  1024 threads.
+__device__ void route_vs_dir(const SelArgs& a, int h, int dir, VsShared& vsh) {
+  uint32_t* hist = vsh.hist;
+  unsigned long long* hist64 = vsh.hist64;
+  unsigned long long* sh64 = vsh.sh64;
+  int* wtot = vsh.wtot;
+  int* sh = vsh.sh;
+  const int tid = threadIdx.x;
   const bool vs = a.c_struct[h] >= a.tau;
   if (dir == 0 && tid == 0) a.route[h] = vs ? 0 : 1;
   const int nb = a.nb;
@@ -341,6 +350,12 @@ __global__ __launch_bounds__(1024) void sel_route_vs(SelArgs a) {
   select_top_k(p, nb, kd, m, dm, hist, sh, wtot);
 }
 
+// grid (hq, 2), 1024 threads.
+__global__ __launch_bounds__(1024) void sel_route_vs(SelArgs a) {
+  __shared__ VsShared vsh;
+  route_vs_dir(a, blockIdx.x, blockIdx.y, vsh);
+}
+
 // Mean of rows [r0, r1) of a [rows][128] bf16 tensor into dst[0..128) (fp32).  256 threads.
 __device__ void pool_rows(const uint16_t* src, int r0, int r1, float* dst, float (*red)[128]) {
   const int tid = threadIdx.x;
@@ -373,14 +388,14 @@ __global__ __launch_bounds__(256) void sel_pool(SelArgs a) {
   const uint16_t* src;
   float* dst;
   if (y < a.hq) {
-    if (a.route[y] != 1) return;
+    if (a.c_struct[y] >= a.tau) return;  // VS head (the route of Alg. 2, decided from its score)
     src = a.q + (size_t)y * a.n * kHeadDim;
     dst = a.qbar + ((size_t)y * a.nb + J) * kHeadDim;
   } else {
     if (a.kbar_all) return;
     const int g = y - a.hq;
     bool any = false;
-    for (int i = 0; i < a.G; ++i) any |= a.route[g * a.G + i] == 1;
+    for (int i = 0; i < a.G; ++i) any |= !(a.c_struct[g * a.G + i] >= a.tau);
     if (!any) return;
     src = a.k + (size_t)g * a.n * kHeadDim;
     dst = a.kbar + ((size_t)g * a.nb + J) * kHeadDim;
@@ -630,16 +645,13 @@ __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
 // (divided by N_b) of every fourth row from there.  grid hq, 256 threads.
 constexpr int kPeSmall = 64, kPeSmallPitch = kPeSmall + 1;
 
-__global__ __launch_bounds__(256) void sel_pe_small(SelArgs a) {
-  __shared__ __attribute__((aligned(16))) float sq[kPeSmall * kHeadDim];  // reused for the logits
-  __shared__ __attribute__((aligned(16))) float sk[kPeSmall * kHeadDim];
-  const int h = blockIdx.x, tid = threadIdx.x;
-  if (a.route[h] != 1) return;
+__device__ void pe_small_head(const SelArgs& a, int h, float* sq, float* sk) {
+  const int tid = threadIdx.x, nthr = blockDim.x, nwav = nthr >> 6;
   const int w = tid >> 6, l = tid & 63, nb = a.nb;
   const float* Qb = a.qbar + (size_t)h * nb * kHeadDim;
   const float* Kb = a.kbar + (size_t)(h / a.G) * nb * kHeadDim;
   auto phys = [](int r, int c4) { return r * kHeadDim + 4 * (c4 ^ (r & 31)); };
-  for (int f = tid; f < kPeSmall * kHeadDim / 4; f += 256) {  // kPeSmall rows x 32 float4
+  for (int f = tid; f < kPeSmall * kHeadDim / 4; f += nthr) {  // kPeSmall rows x 32 float4
     const int r = f >> 5, c4 = f & 31;
     const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
     *reinterpret_cast<float4*>(&sq[phys(r, c4)]) =
@@ -649,7 +661,7 @@ __global__ __launch_bounds__(256) void sel_pe_small(SelArgs a) {
   }
   __syncthreads();
   const int qs0 = 32 * (w >> 1), ks0 = 32 * (w & 1);
-  const bool work = ks0 <= qs0 && qs0 < nb;
+  const bool work = w < 4 && ks0 <= qs0 && qs0 < nb;  // waves 0..3 take the four quarters
   f32x16 acc = zero16();
   if (work) {
     const int qr = qs0 + (l & 31), kr = ks0 + (l & 31);
@@ -679,7 +691,7 @@ __global__ __launch_bounds__(256) void sel_pe_small(SelArgs a) {
   __syncthreads();
   float* At = a.atil + (size_t)h * a.cap;
   const float inv_nb = 1.f / (float)nb;
-  for (int qb = w; qb < nb; qb += 4) {
+  for (int qb = w; qb < nb; qb += nwav) {
     const bool in = l <= qb;
     const float x = in ? lg[qb * kPeSmallPitch + l] : -__builtin_inff();
     const float mx = wave_max(x);
@@ -687,6 +699,13 @@ __global__ __launch_bounds__(256) void sel_pe_small(SelArgs a) {
     const float sum = wave_sum(p);
     if (in) At[(int64_t)qb * (qb + 1) / 2 + l] = p / sum * inv_nb;
   }
+}
+
+__global__ __launch_bounds__(256) void sel_pe_small(SelArgs a) {
+  __shared__ __attribute__((aligned(16))) float sq[kPeSmall * kHeadDim];  // reused for the logits
+  __shared__ __attribute__((aligned(16))) float sk[kPeSmall * kHeadDim];
+  if (a.route[blockIdx.x] != 1) return;
+  pe_small_head(a, blockIdx.x, sq, sk);
 }
 
 // Row softmax of the pooled logits, divided by N_b.  grid (nb, hq), 256 threads.
@@ -808,11 +827,8 @@ __global__ __launch_bounds__(256) void sel_radix_scan(SelArgs a, int pass) {
 // with the histograms in LDS.  The masses are the same fixed-point integers, so
 // t*, the remaining mass and the count of pairs equal to t* are the same; one
 // launch replaces seven.  grid hq, 1024 threads.
-__global__ __launch_bounds__(1024) void sel_radix_small(SelArgs a) {
-  __shared__ unsigned long long bins[kRadixBins];
-  __shared__ RState sst;
-  const int h = blockIdx.x, tid = threadIdx.x;
-  if (a.route[h] != 1) return;
+__device__ void radix_small_head(const SelArgs& a, int h, unsigned long long* bins, RState& sst) {
+  const int tid = threadIdx.x;
   if (tid == 0) {
     sst.prefix = 0;
     sst.all = 0;
@@ -857,6 +873,13 @@ __global__ __launch_bounds__(1024) void sel_radix_small(SelArgs a) {
     __syncthreads();  // the search is done with the bins before the next pass clears them
   }
   if (tid == 0) a.rstate[h] = sst;
+}
+
+__global__ __launch_bounds__(1024) void sel_radix_small(SelArgs a) {
+  __shared__ unsigned long long bins[kRadixBins];
+  __shared__ RState sst;
+  if (a.route[blockIdx.x] != 1) return;
+  radix_small_head(a, blockIdx.x, bins, sst);
 }
 
 // Per-row counts.  VS: x = row size.  PE: x = #(> t*), y = #(== t*), z = flags
@@ -1020,14 +1043,42 @@ __global__ __launch_bounds__(256) void sel_csr_fill(SelArgs a) {
 // 16 waves taking rows w, w + 16, ... (the same lists as the three kernels above).
 // grid hq, 1024 threads.
 constexpr int kCsrSmall = 64;
-__global__ __launch_bounds__(1024) void sel_csr_small(SelArgs a) {
-  __shared__ long long wtot[16];
-  const int h = blockIdx.x, w = threadIdx.x >> 6;
+__device__ void csr_small_head(const SelArgs& a, int h, long long* wtot) {
+  const int w = threadIdx.x >> 6;
   for (int qb = w; qb < a.nb; qb += 16) csr_count_row(a, h, qb);
   __syncthreads();  // every row's counts are visible to the whole workgroup
   csr_scan_head(a, h, wtot);
   __syncthreads();  // row_ptr and the ties taken per row are visible
   for (int qb = w; qb < a.nb; qb += 16) csr_fill_row(a, h, qb);
+}
+
+__global__ __launch_bounds__(1024) void sel_csr_small(SelArgs a) {
+  __shared__ long long wtot[16];
+  csr_small_head(a, blockIdx.x, wtot);
+}
+
+// Short layers (N_b <= kPeSmall, so also N_b <= kCsrSmall and the PE cutoff fits one
+// workgroup): after the pooling, the whole selection of one head in one launch -- the
+// route and both VS directions, or the PE scores, softmax and gamma cutoff, then the
+// CSR lists -- the same computations as the separate kernels, phase after phase.
+// grid hq, 1024 threads.
+__global__ __launch_bounds__(1024) void sel_small(SelArgs a) {
+  __shared__ __attribute__((aligned(16))) float sbuf[2 * kPeSmall * kHeadDim];  // 64 KB, per phase
+  __shared__ RState sst;
+  const int h = blockIdx.x;
+  const bool vs = a.c_struct[h] >= a.tau;
+  VsShared& vsh = *reinterpret_cast<VsShared*>(sbuf);
+  for (int dir = 0; dir < 2; ++dir) {  // writes the route, and the direction masks (zero on a PE head)
+    route_vs_dir(a, h, dir, vsh);
+    __syncthreads();
+  }
+  if (!vs) {
+    pe_small_head(a, h, sbuf, sbuf + kPeSmall * kHeadDim);
+    __syncthreads();
+    radix_small_head(a, h, reinterpret_cast<unsigned long long*>(sbuf), sst);
+    __syncthreads();
+  }
+  csr_small_head(a, h, reinterpret_cast<long long*>(sbuf));
 }
 
 }  // namespace
@@ -1091,6 +1142,11 @@ hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, flo
   a.rstate = reinterpret_cast<RState*>(ws + L.rstate);
   a.rowinfo = reinterpret_cast<int4*>(ws + L.rowinfo);
   const int nb = d.nb;
+  if (nb <= kPeSmall) {  // short layers: pooling, then the whole selection in one launch per head
+    hipLaunchKernelGGL(sel_pool, dim3(nb, d.hq + d.hkv), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(sel_small, dim3(d.hq), dim3(1024), 0, stream, a);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(sel_route_vs, dim3(d.hq, 2), dim3(1024), 0, stream, a);
   hipLaunchKernelGGL(sel_pool, dim3(nb, d.hq + d.hkv), dim3(256), 0, stream, a);
   if (nb <= kPeSmall) {  // logits and softmax of the whole triangle in one launch
