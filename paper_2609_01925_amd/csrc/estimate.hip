@@ -63,8 +63,10 @@ __device__ __forceinline__ void scores(int kbuf, const bf16x8 (&qf)[8], int l, f
 #pragma unroll
   for (int kk = 0; kk < 8; ++kk) {
     const int d = 16 * kk + 8 * (l >> 5);
-    const bf16x8 k0 = *(const lds_bf16x8*)(uint32_t)(kbuf + lds_off(l & 31, d));
-    const bf16x8 k1 = *(const lds_bf16x8*)(uint32_t)(kbuf + lds_off(32 + (l & 31), d));
+    // rows r and r + 32 share a swizzle: the second read is the first address + 32 rows
+    const int addr = kbuf + lds_off(l & 31, d);
+    const bf16x8 k0 = *(const lds_bf16x8*)(uint32_t)addr;
+    const bf16x8 k1 = *(const lds_bf16x8*)(uint32_t)(addr + 32 * 256);
     s[0] = mfma32(k0, qf[kk], s[0]);
     s[1] = mfma32(k1, qf[kk], s[1]);
   }
@@ -178,13 +180,27 @@ __global__ __launch_bounds__(NT, 4) void est_pass(EstArgs a) {
       }
       if (all_lo) tlo = t0 + t1; else thi = t0 + t1;
     } else if (plain) {
+      // The wave's rows cross the split inside one 32-key half of the tile; the other
+      // half lies on one side of it.  Only the straddling half is tested per entry,
+      // against a per-lane limit (the lane's keys in a half are 4 (l >> 5) plus the
+      // offsets 8 (i >> 2) + (i & 3), increasing with i).
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < 2; ++mb) {
+        const int c0 = key0 + 32 * mb;
+        if (__all(c0 + 31 < ksplit) || __all(c0 >= ksplit)) {
+          float u = 0.f;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc0));
-          if (key_of(key0, mb, i, l) < ksplit) tlo += p; else thi += p;
+          for (int i = 0; i < 16; ++i) u += fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc0));
+          if (c0 < ksplit) tlo += u; else thi += u;
+        } else {
+          const int lim = ksplit - c0 - 4 * (l >> 5);
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const float p = fast_exp2(__builtin_fmaf(s[mb][i], a.c, -mc0));
+            if (8 * (i >> 2) + (i & 3) < lim) tlo += p; else thi += p;
+          }
         }
+      }
     } else {
       general(mc0);
     }
