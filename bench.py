@@ -18,6 +18,7 @@ import argparse
 import hashlib
 import json
 import math
+import statistics
 import os
 import sys
 import time
@@ -27,6 +28,10 @@ sys.path.insert(0, ROOT)
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E (published)
+# VALU issue: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz lane slots per second (the published
+# 157.3 TFLOP/s fp32 vector rate counts an FMA as two FLOPs and packs two lanes' worth per slot)
+VALU_LANE_SLOTS_PER_S = 256 * 4 * 16 * 2.4e9
+VALU_SLOTS_PER_PROXY_SCORE = 6.0  # exp2 at a quarter of the full rate (4) + fma + add
 METRIC = "CRISP prefill attention ms/layer at 128k & 512k; speedup vs dense HIP attention"
 
 
@@ -56,6 +61,9 @@ def parse():
     ap.add_argument("--label", default="crisp_kernels_llama3_8b_128k", help="file stem for --summarize")
     ap.add_argument("--command", action="append", default=[],
                     help="a profiling command, recorded by --summarize (repeatable)")
+    ap.add_argument("--clock-power", action="store_true",
+                    help="sample socket power and GFX clock (amd-smi) under several loads on the 128k layer, "
+                         "print one JSON line and exit")
     return ap.parse_args()
 
 
@@ -144,6 +152,8 @@ def layer_measure(cfg, steps, warmup, label):
     attn_flop = executed_pairs * pair_flop
     dense_flop_exec = dense_pairs * pair_flop
     dense_useful = 2.0 * cfg.n_q_heads * cfg.seq_len * cfg.seq_len * d   # causal half: 4 n^2 d / 2
+    est_scores = cfg.n_q_heads * min(block, cfg.seq_len) * cfg.seq_len
+    est_valu_ms = est_scores * VALU_SLOTS_PER_PROXY_SCORE / VALU_LANE_SLOTS_PER_S * 1e3
     res = {
         "workload": cfg.name, "seq_len": cfg.seq_len, "n_q_heads": cfg.n_q_heads, "n_kv_heads": cfg.n_kv_heads,
         "block": block, "alpha": cfg.alpha,
@@ -169,6 +179,10 @@ def layer_measure(cfg, steps, warmup, label):
         "estimate_mfma_frac": 2.0 * cfg.n_q_heads * block * cfg.seq_len * d / (est["mean"] * 1e-3) / 1e12
         / MFMA_BF16_PEAK_TFLOPS,
         "select_hbm_gbs": sel_gbs, "select_hbm_frac": sel_gbs / HBM_PEAK_GBS,
+        # the estimator's VALU floor: per proxy score one exp2 (a transcendental, a quarter of
+        # the full VALU rate, so 4 lane slots) and two full-rate ops (scale-and-subtract, sum)
+        "estimate_valu_bound_ms": est_valu_ms,
+        "estimate_valu_frac": est_valu_ms / est["mean"],
     }
     res["_attn_launch_ms"] = att["mean"]
     res["_attn_flop"] = attn_flop
@@ -619,10 +633,100 @@ def summarize(args):
     print(dst)
 
 
+def clock_power(seconds=8.0):
+    """Socket power and GFX clock while each of several loads runs for `seconds`: idle, the
+    sparse attention (on the layer's own CRISP lists) and the dense attention of the 128k
+    Llama layer, the MFMA loop of measured_peaks on toggling and on constant operands, and the
+    estimator.  amd-smi is sampled in a child process about every 0.3 s; the first second of
+    each load is left out.  The published power cap is read from rocm-smi."""
+    import ctypes
+    import re
+    import shutil
+    import subprocess
+    import threading
+    import torch
+    from paper_2609_01925_amd import crisp as C
+    from workloads import CONFIGS, make_layer
+    smi = shutil.which("amd-smi") or "/opt/rocm/bin/amd-smi"
+    samples, stop = [], threading.Event()
+
+    def sampler():
+        while not stop.is_set():
+            try:
+                r = subprocess.run([smi, "metric", "-p", "-c"], capture_output=True, text=True, timeout=10)
+            except (OSError, subprocess.SubprocessError):
+                return
+            pw = re.search(r"SOCKET_POWER:\s*(\d+)\s*W", r.stdout)
+            ck = [int(x) for x in re.findall(r"GFX_\d+:\s*\n\s*CLK:\s*(\d+)\s*MHz", r.stdout)]
+            if pw and ck:
+                samples.append((time.time(), int(pw.group(1)), sum(ck) / len(ck)))
+            stop.wait(0.2)
+
+    dev = "cuda:0"
+    cfg = CONFIGS[2]
+    q, k, v, _ = make_layer(cfg, device=dev)
+    p = C.make_params(alpha=cfg.alpha)
+    o, _, rp, ci = C.crisp_prefill_attn(q, k, v, p, cfg.block, return_lists=True)
+    ws = torch.empty(C.crisp_sparse_workspace_size(C.shape_of(q, k, cfg.block)), dtype=torch.uint8, device=dev)
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_01925_amd", "libcrisp_peaks.so"))
+    lib.crisp_peak_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p]
+    lib.crisp_peak_mfma_bf16_toggling.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                                  ctypes.c_void_p]
+    stream = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    out = torch.empty(2048 * 256, dtype=torch.float32, device=dev)
+    g = torch.Generator(device="cpu").manual_seed(20261202)
+    ops = torch.randn(64 * 16 * 8, generator=g).to(torch.bfloat16).to(dev)
+    phases = [
+        ("idle", None),
+        ("sparse_attn_128k", lambda: C.crisp_sparse_attn(q, k, v, rp, ci, cfg.block, out=o, ws=ws)),
+        ("dense_attn_128k", lambda: C.crisp_dense_attn(q, k, v, cfg.block, out=o)),
+        ("mfma_loop_toggling_operands", lambda: lib.crisp_peak_mfma_bf16_toggling(
+            2048, 80000, ctypes.c_void_p(ops.data_ptr()), ctypes.c_void_p(out.data_ptr()), stream)),
+        ("mfma_loop_constant_operands", lambda: lib.crisp_peak_mfma_bf16(
+            2048, 20000, ctypes.c_void_p(out.data_ptr()), stream)),
+        ("estimate_128k", lambda: C.crisp_estimate(q, k, p, cfg.block)),
+    ]
+    cap = None
+    try:
+        r = subprocess.run([shutil.which("rocm-smi") or "/opt/rocm/bin/rocm-smi", "--showmaxpower"],
+                           capture_output=True, text=True, timeout=30)
+        m = re.search(r"Max Graphics Package Power \(W\):\s*([0-9.]+)", r.stdout)
+        cap = float(m.group(1)) if m else None
+    except (OSError, subprocess.SubprocessError):
+        pass
+    torch.cuda.synchronize()
+    th = threading.Thread(target=sampler, daemon=True)
+    th.start()
+    rows = []
+    for name, fn in phases:
+        t0 = time.time()
+        while time.time() - t0 < seconds:
+            if fn is None:
+                time.sleep(0.25)
+            else:
+                for _ in range(4):
+                    fn()
+                torch.cuda.synchronize()
+        t1 = time.time()
+        sel = [s for s in samples if t0 + 1.0 <= s[0] <= t1]
+        row = {"load": name, "samples": len(sel),
+               "socket_power_w_median": statistics.median([s[1] for s in sel]) if sel else None,
+               "socket_power_w_max": max(s[1] for s in sel) if sel else None,
+               "gfx_clock_mhz_median": statistics.median([s[2] for s in sel]) if sel else None}
+        rows.append(row)
+        log(f"clock/power {row}")
+    stop.set()
+    th.join(timeout=15)
+    return {"power_cap_w": cap, "loads": rows, "seconds_per_load": seconds}
+
+
 def main():
     args = parse()
     if args.summarize:
         summarize(args)
+        return
+    if args.clock_power:
+        print(json.dumps({"clock_power": clock_power()}), flush=True)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
