@@ -691,6 +691,27 @@ __device__ __forceinline__ int cost_bucket(int64_t c) {
   return (int)(b < kQueueBuckets - 1 ? b : kQueueBuckets - 1);
 }
 
+// Calls f(u, row length) for the units u = tid, tid + 1024, ... in that order, the row
+// lengths of eight units loaded together (one memory latency per eight units, not
+// one per unit).
+template <typename F>
+__device__ __forceinline__ void for_units(const AttnArgs& a, int total, int tid, F f) {
+  constexpr int kBatch = 8;
+  for (int u0 = 0; u0 < total; u0 += 1024 * kBatch) {
+    int L[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int u = u0 + 1024 * j + tid;
+      L[j] = u < total ? row_len(a, u / a.nb, u % a.nb) : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int u = u0 + 1024 * j + tid;
+      if (u < total) f(u, L[j]);
+    }
+  }
+}
+
 __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
   __shared__ int hist[kCostBuckets];
   __shared__ int part[1024];
@@ -710,11 +731,10 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
   if (a.split_slots > 0) {
     unsigned long long t = 0;
     int mx = 0;
-    for (int u = tid; u < total; u += 1024) {
-      const int L = row_len(a, u / a.nb, u % a.nb);
+    for_units(a, total, tid, [&](int, int L) {
       t += (unsigned long long)L;
       mx = L > mx ? L : mx;
-    }
+    });
     atomicAdd(&s_tot, t);
     atomicMax(&s_max, mx);
     __syncthreads();
@@ -730,9 +750,8 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
   auto key = [&](int h, int len) {
     return unit_queue(a, h) * kQueueBuckets + (kQueueBuckets - 1 - cost_bucket(len));
   };
-  for (int u = tid; u < total; u += 1024) {
+  for_units(a, total, tid, [&](int u, int L) {
     const int h = u / a.nb;
-    const int L = row_len(a, h, u % a.nb);
     if (L > C) {
       const int k = (L + C - 1) / C;
       for (int c = 0; c < k; ++c) atomicAdd(&hist[key(h, L - c * C < C ? L - c * C : C)], 1);
@@ -742,7 +761,7 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
       atomicAdd(&hist[key(h, L)], 1);
       if (a.split_slots > 0) a.slot_base[u] = -1;
     }
-  }
+  });
   __syncthreads();
   // exclusive scan over the keys, 8 per thread
   constexpr int per = kCostBuckets / 1024;
@@ -790,9 +809,8 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
     a.counter[18] = s_split;
   }
   __syncthreads();
-  for (int u = tid; u < total; u += 1024) {
+  for_units(a, total, tid, [&](int u, int L) {
     const int h = u / a.nb;
-    const int L = row_len(a, h, u % a.nb);
     if (L > C) {
       const int k = (L + C - 1) / C;
       for (int c = 0; c < k; ++c) {
@@ -803,7 +821,7 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
       const int pos = atomicAdd(&hist[key(h, L)], 1);
       const_cast<int32_t*>(a.order)[pos] = u;
     }
-  }
+  });
 }
 
 // Merges the chunks of each split row in chunk order:

@@ -708,6 +708,28 @@ __global__ __launch_bounds__(256) void sel_pe_small(SelArgs a) {
   pe_small_head(a, blockIdx.x, sq, sk);
 }
 
+// Reduction of one value per thread of a 256-thread workgroup in binary-tree order
+// (t with t + 128, then t with t + 64, ..., then t with t + 1), the last six levels
+// within wave 0 by shuffles; every thread gets the result.
+template <typename Op>
+__device__ __forceinline__ float tree_reduce(float* red, float v, Op op) {
+  const int tid = threadIdx.x;
+  red[tid] = v;
+  __syncthreads();
+  if (tid < 128) red[tid] = op(red[tid], red[tid + 128]);
+  __syncthreads();
+  if (tid < 64) {
+    float x = op(red[tid], red[tid + 64]);
+#pragma unroll
+    for (int s = 32; s > 0; s >>= 1) x = op(x, __shfl_down(x, s, 64));
+    if (tid == 0) red[0] = x;
+  }
+  __syncthreads();
+  const float r = red[0];
+  __syncthreads();  // red may be reused
+  return r;
+}
+
 // Row softmax of the pooled logits, divided by N_b.  grid (nb, hq), 256 threads.
 __global__ __launch_bounds__(256) void sel_pe_softmax(SelArgs a) {
   __shared__ float red[256];
@@ -717,23 +739,10 @@ __global__ __launch_bounds__(256) void sel_pe_softmax(SelArgs a) {
   const int len = qb + 1;
   float mx = -__builtin_inff();
   for (int i = tid; i < len; i += 256) mx = fmaxf(mx, row[i]);
-  red[tid] = mx;
-  __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (tid < s) red[tid] = fmaxf(red[tid], red[tid + s]);
-    __syncthreads();
-  }
-  mx = red[0];
-  __syncthreads();
+  mx = tree_reduce(red, mx, [](float x, float y) { return fmaxf(x, y); });
   float sum = 0.f;
   for (int i = tid; i < len; i += 256) sum += fast_exp2(row[i] - mx);
-  red[tid] = sum;
-  __syncthreads();
-  for (int s = 128; s > 0; s >>= 1) {
-    if (tid < s) red[tid] += red[tid + s];
-    __syncthreads();
-  }
-  sum = red[0];
+  sum = tree_reduce(red, sum, [](float x, float y) { return x + y; });
   const float inv_nb = 1.f / (float)a.nb;
   for (int i = tid; i < len; i += 256) row[i] = fast_exp2(row[i] - mx) / sum * inv_nb;
 }
@@ -779,9 +788,31 @@ __global__ __launch_bounds__(256) void sel_radix_hist(SelArgs a, int pass) {
   const int64_t lo = (int64_t)blockIdx.x * per;
   const int64_t up = lo + per < a.cap ? lo + per : a.cap;
   const uint32_t dmask = (1u << nbits) - 1u;
-  for (int64_t i = lo + tid; i < up; i += 256) {
-    const uint32_t b = fbits(At[i]);
+  auto take = [&](float x) {
+    const uint32_t b = fbits(x);
     if (((uint64_t)b >> hi) == want) atomicAdd(&lh[(b >> shift) & dmask], fixed_mass(b));
+  };
+  // The chunk [lo, up): up to three entries before the first 16-byte aligned one, then
+  // 16-byte loads (four in flight per thread), then up to three entries after them.
+  int64_t a0 = lo + (int64_t)((4 - (((uintptr_t)(At + lo) >> 2) & 3)) & 3);
+  a0 = a0 < up ? a0 : up;
+  const int64_t n4 = (up - a0) >> 2, a1 = a0 + 4 * n4;
+  if (lo + tid < a0) take(At[lo + tid]);
+  if (a1 + tid < up) take(At[a1 + tid]);
+  const float4* A4 = reinterpret_cast<const float4*>(At + a0);
+  for (int64_t j0 = tid; j0 < n4; j0 += 4 * 256) {
+    float4 v[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+      if (j0 + 256 * x < n4) v[x] = A4[j0 + 256 * x];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+      if (j0 + 256 * x < n4) {
+        take(v[x].x);
+        take(v[x].y);
+        take(v[x].z);
+        take(v[x].w);
+      }
   }
   __syncthreads();
   for (int i = tid; i < kRadixBins; i += 256)
@@ -893,28 +924,43 @@ __device__ __forceinline__ void csr_count_row(const SelArgs& a, int h, int qb) {
     const uint8_t* vm = a.masks + (size_t)h * 2 * nb;
     const uint8_t* sm = vm + nb;
     int cnt = 0;
-    for (int base = 0; base <= qb; base += 64) {
-      const int kb = base + l;
-      const bool sel = kb <= qb && (kb == 0 || kb == qb || vm[kb] || sm[nb - 1 - qb + kb]);
-      cnt += __popcll(__ballot(sel));
+    for (int base = 0; base <= qb; base += 256) {  // four 64-entry chunks, their loads issued together
+      bool sel[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        const int kb = base + 64 * x + l;
+        sel[x] = kb <= qb && (kb == 0 || kb == qb || vm[kb] || sm[nb - 1 - qb + kb]);
+      }
+#pragma unroll
+      for (int x = 0; x < 4; ++x) cnt += __popcll(__ballot(sel[x]));
     }
     info.x = cnt;
   } else {
     const RState st = a.rstate[h];
     const float* row = a.atil + (size_t)h * a.cap + (int64_t)qb * (qb + 1) / 2;
     int ngt = 0, neq = 0, flags = 0;
-    for (int base = 0; base <= qb; base += 64) {
-      const int kb = base + l;
-      const uint32_t b = kb <= qb ? fbits(row[kb]) : 0u;
-      const bool gt = kb <= qb && (st.all || b > st.prefix);
-      const bool eq = kb <= qb && !st.all && b == st.prefix;
-      ngt += __popcll(__ballot(gt));
-      neq += __popcll(__ballot(eq));
-      int f = 0;
-      if (kb == 0) f |= (gt ? 1 : 0) | (eq ? 2 : 0);
-      if (kb == qb) f |= (gt ? 4 : 0) | (eq ? 8 : 0);
-      f = wave_sum_i(f);  // at most two lanes contribute, with disjoint bits
-      flags |= f;
+    for (int base = 0; base <= qb; base += 256) {  // four 64-entry chunks, their loads issued together
+      uint32_t bv[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        const int kb = base + 64 * x + l;
+        bv[x] = kb <= qb ? fbits(row[kb]) : 0u;
+      }
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        if (base + 64 * x > qb) break;
+        const int kb = base + 64 * x + l;
+        const uint32_t b = bv[x];
+        const bool gt = kb <= qb && (st.all || b > st.prefix);
+        const bool eq = kb <= qb && !st.all && b == st.prefix;
+        ngt += __popcll(__ballot(gt));
+        neq += __popcll(__ballot(eq));
+        int f = 0;
+        if (kb == 0) f |= (gt ? 1 : 0) | (eq ? 2 : 0);
+        if (kb == qb) f |= (gt ? 4 : 0) | (eq ? 8 : 0);
+        f = wave_sum_i(f);  // at most two lanes contribute, with disjoint bits
+        flags |= f;
+      }
     }
     info = make_int4(ngt, neq, flags, 0);
   }
@@ -1006,30 +1052,48 @@ __device__ __forceinline__ void csr_fill_row(const SelArgs& a, int h, int qb) {
   if (a.route[h] == 0) {
     const uint8_t* vm = a.masks + (size_t)h * 2 * nb;
     const uint8_t* sm = vm + nb;
-    for (int base = 0; base <= qb; base += 64) {
-      const int kb = base + l;
-      const bool sel = kb <= qb && (kb == 0 || kb == qb || vm[kb] || sm[nb - 1 - qb + kb]);
-      const uint64_t bal = __ballot(sel);
-      if (sel) out[pos + __popcll(bal & lt)] = kb;
-      pos += __popcll(bal);
+    for (int base = 0; base <= qb; base += 256) {  // four 64-entry chunks, their loads issued together
+      bool sv[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        const int kb = base + 64 * x + l;
+        sv[x] = kb <= qb && (kb == 0 || kb == qb || vm[kb] || sm[nb - 1 - qb + kb]);
+      }
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        const int kb = base + 64 * x + l;
+        const uint64_t bal = __ballot(sv[x]);
+        if (sv[x]) out[pos + __popcll(bal & lt)] = kb;
+        pos += __popcll(bal);
+      }
     }
   } else {
     const RState st = a.rstate[h];
     const int take = a.rowinfo[(size_t)h * nb + qb].w;
     const float* row = a.atil + (size_t)h * a.cap + (int64_t)qb * (qb + 1) / 2;
     int eq_seen = 0;
-    for (int base = 0; base <= qb; base += 64) {
-      const int kb = base + l;
-      const uint32_t b = kb <= qb ? fbits(row[kb]) : 0u;
-      const bool gt = kb <= qb && (st.all || b > st.prefix);
-      const bool eq = kb <= qb && !st.all && b == st.prefix;
-      const uint64_t eb = __ballot(eq);
-      const int eq_rank = eq_seen + __popcll(eb & lt);
-      eq_seen += __popcll(eb);
-      const bool sel = kb <= qb && (gt || (eq && eq_rank < take) || kb == 0 || kb == qb);
-      const uint64_t bal = __ballot(sel);
-      if (sel) out[pos + __popcll(bal & lt)] = kb;
-      pos += __popcll(bal);
+    for (int base = 0; base <= qb; base += 256) {  // four 64-entry chunks, their loads issued together
+      uint32_t bv[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        const int kb = base + 64 * x + l;
+        bv[x] = kb <= qb ? fbits(row[kb]) : 0u;
+      }
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        if (base + 64 * x > qb) break;
+        const int kb = base + 64 * x + l;
+        const uint32_t b = bv[x];
+        const bool gt = kb <= qb && (st.all || b > st.prefix);
+        const bool eq = kb <= qb && !st.all && b == st.prefix;
+        const uint64_t eb = __ballot(eq);
+        const int eq_rank = eq_seen + __popcll(eb & lt);
+        eq_seen += __popcll(eb);
+        const bool sel = kb <= qb && (gt || (eq && eq_rank < take) || kb == 0 || kb == qb);
+        const uint64_t bal = __ballot(sel);
+        if (sel) out[pos + __popcll(bal & lt)] = kb;
+        pos += __popcll(bal);
+      }
     }
   }
 }
