@@ -955,11 +955,13 @@ __device__ __forceinline__ void csr_count_row(const SelArgs& a, int h, int qb) {
         const bool eq = kb <= qb && !st.all && b == st.prefix;
         ngt += __popcll(__ballot(gt));
         neq += __popcll(__ballot(eq));
-        int f = 0;
-        if (kb == 0) f |= (gt ? 1 : 0) | (eq ? 2 : 0);
-        if (kb == qb) f |= (gt ? 4 : 0) | (eq ? 8 : 0);
-        f = wave_sum_i(f);  // at most two lanes contribute, with disjoint bits
-        flags |= f;
+        if (base + 64 * x == 0 || qb - (base + 64 * x) < 64) {  // the chunk holds block 0 or block qb
+          int f = 0;
+          if (kb == 0) f |= (gt ? 1 : 0) | (eq ? 2 : 0);
+          if (kb == qb) f |= (gt ? 4 : 0) | (eq ? 8 : 0);
+          f = wave_sum_i(f);  // at most two lanes contribute, with disjoint bits
+          flags |= f;
+        }
       }
     }
     info = make_int4(ngt, neq, flags, 0);
