@@ -31,7 +31,9 @@ HBM_PEAK_GBS = 8000.0            # MI355X HBM3E (published)
 # VALU issue: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz lane slots per second (the published
 # 157.3 TFLOP/s fp32 vector rate counts an FMA as two FLOPs and packs two lanes' worth per slot)
 VALU_LANE_SLOTS_PER_S = 256 * 4 * 16 * 2.4e9
-VALU_SLOTS_PER_PROXY_SCORE = 6.0  # exp2 at a quarter of the full rate (4) + fma + add
+# per proxy score: exp2, which issues at half the full rate on this chip (measured_peaks:
+# 9.0 SIMD cycles per wave-wide v_exp_f32 against 3.75 for v_fma_f32), so 2 slots, + fma + add
+VALU_SLOTS_PER_PROXY_SCORE = 4.0
 METRIC = "CRISP prefill attention ms/layer at 128k & 512k; speedup vs dense HIP attention"
 
 
@@ -179,8 +181,8 @@ def layer_measure(cfg, steps, warmup, label):
         "estimate_mfma_frac": 2.0 * cfg.n_q_heads * block * cfg.seq_len * d / (est["mean"] * 1e-3) / 1e12
         / MFMA_BF16_PEAK_TFLOPS,
         "select_hbm_gbs": sel_gbs, "select_hbm_frac": sel_gbs / HBM_PEAK_GBS,
-        # the estimator's VALU floor: per proxy score one exp2 (a transcendental, a quarter of
-        # the full VALU rate, so 4 lane slots) and two full-rate ops (scale-and-subtract, sum)
+        # the estimator's VALU floor: per proxy score one exp2 (half the full VALU rate, so 2
+        # lane slots) and two full-rate ops (scale-and-subtract, sum)
         "estimate_valu_bound_ms": est_valu_ms,
         "estimate_valu_frac": est_valu_ms / est["mean"],
     }
@@ -201,6 +203,15 @@ def add_measured_fracs(res, peaks):
     res["estimate_frac_of_measured_mfma"] = res["estimate_tflops"] / m
     res["estimate_frac_of_measured_copy"] = res["estimate_hbm_gbs"] / c
     res["select_frac_of_measured_copy"] = res["select_hbm_gbs"] / c
+    # the same VALU floor from this GPU's measured issue costs: per 64 scores one exp2 and
+    # two FMA-class instructions on one SIMD, 1024 SIMDs at 2.4 GHz
+    v = peaks.get("valu_cycles_per_wave_instruction")
+    if v and res.get("estimate_valu_bound_ms"):
+        per64 = v["exp2_f32"] + 2.0 * v["fma_f32"]
+        scores = res["estimate_valu_bound_ms"] * 1e-3 * VALU_LANE_SLOTS_PER_S / VALU_SLOTS_PER_PROXY_SCORE
+        ms = scores / 64.0 * per64 / (1024 * 2.4e9) * 1e3
+        res["estimate_valu_bound_ms_measured_issue"] = ms
+        res["estimate_valu_frac_measured_issue"] = ms / res["stage_ms"]["estimate"]
 
 
 def comparator_measure(cfg, res, steps, warmup, label, mixes=True):
@@ -435,14 +446,50 @@ def measured_peaks():
     torch.cuda.empty_cache()
     log(f"peaks: bf16 MFMA {mfma_tflops:.0f} TFLOP/s (constant operands), {tog_tflops:.0f} TFLOP/s "
         f"(toggling operands), copy {copy_gbs:.0f} GB/s")
+    # LDS read rates in the attention kernel's operand patterns and the VALU issue cost of
+    # exp2 against a full-rate FMA, clocked by the waves themselves (s_memtime, core cycles)
+    lib.crisp_peak_lds_bytes_per_wave.restype = ctypes.c_double
+    lib.crisp_peak_lds_bytes_per_wave.argtypes = [ctypes.c_int, ctypes.c_int]
+    lib.crisp_peak_lds_read.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                        ctypes.c_void_p]
+    lib.crisp_peak_valu.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_void_p]
+    wg_c, it_c = 512, 20000  # two workgroups (eight waves) per CU, two waves per SIMD
+    cyc = torch.empty(wg_c * 4, dtype=torch.int64, device=dev)
+    sink = torch.empty(wg_c * 256, dtype=torch.int32, device=dev)
+
+    def median_cycles(launch):
+        for _ in range(2):
+            assert launch() == 0
+        torch.cuda.synchronize()
+        v = sorted(cyc.cpu().tolist())
+        return v[len(v) // 2]
+
+    lds = {}
+    for kind, name in ((0, "b128_k_operand"), (1, "b64_tr_b16_v_operand"), (2, "b64")):
+        c = median_cycles(lambda: lib.crisp_peak_lds_read(kind, wg_c, it_c, ctypes.c_void_p(cyc.data_ptr()),
+                                                          ctypes.c_void_p(sink.data_ptr()), stream))
+        lds[name] = 8 * lib.crisp_peak_lds_bytes_per_wave(kind, it_c) / c  # bytes per clock per CU (8 waves)
+    valu = {}
+    for kind, name in ((0, "exp2_f32"), (1, "fma_f32")):
+        c = median_cycles(lambda: lib.crisp_peak_valu(kind, wg_c, it_c, ctypes.c_void_p(cyc.data_ptr()),
+                                                      ctypes.c_void_p(sink.data_ptr()), stream))
+        valu[name] = c / (2 * it_c * 8)  # SIMD cycles per wave-wide instruction (two waves per SIMD)
+    log(f"peaks: LDS read B/clk/CU {', '.join(f'{k} {v:.0f}' for k, v in lds.items())}; VALU cycles per "
+        f"wave instruction {', '.join(f'{k} {v:.2f}' for k, v in valu.items())}")
     return {"mfma_bf16_tflops": tog_tflops, "mfma_bf16_constant_operand_tflops": mfma_tflops,
+            "lds_read_bytes_per_clk_per_cu": lds, "valu_cycles_per_wave_instruction": valu,
             "mfma_bf16_published_tflops": MFMA_BF16_PEAK_TFLOPS,
             "copy_gbs": copy_gbs, "hbm_published_gbs": HBM_PEAK_GBS,
             "method": ("MFMA: 2048 workgroups x 4 waves, 4 independent v_mfma_f32_32x32x16_bf16 chains per wave, "
                        f"median of 10 launches; mfma_bf16_tflops: operands cycling through 16 random normal "
                        f"bf16 registers per lane ({iters_t} rounds, launches about as long as the 128k attention's); "
                        f"constant_operand: the same registers every MFMA ({iters} rounds); copy: 1 GiB device to "
-                       "device, 16-byte loads and stores, read + written bytes, median of 10 launches")}
+                       "device, 16-byte loads and stores, read + written bytes, median of 10 launches; LDS: "
+                       "512 workgroups (8 waves per CU) x 20000 rounds of 8 reads in the attention kernel's K and "
+                       "V operand patterns, bytes per core clock per CU from each wave's s_memtime cycles "
+                       "(median wave); VALU: 8 independent chains of v_exp_f32 or v_fma_f32 per wave, two waves "
+                       "per SIMD, SIMD cycles per wave-wide instruction")}
 
 
 def config_records(steps, warmup, skip_cpu, peaks):

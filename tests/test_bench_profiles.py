@@ -39,6 +39,17 @@ def test_peaks_library_exports_and_validates():
     assert lib.crisp_peak_mfma_bf16_toggling(8, 16, ctypes.c_void_p(8), ctypes.c_void_p(16), None) != 0   # misaligned
     assert lib.crisp_peak_copy(ctypes.c_void_p(16), ctypes.c_void_p(32), 15, 1, None) != 0   # not 16-byte words
     assert lib.crisp_peak_copy(ctypes.c_void_p(8), ctypes.c_void_p(32), 16, 1, None) != 0    # misaligned
+    lib.crisp_peak_lds_bytes_per_wave.restype = ctypes.c_double
+    lib.crisp_peak_lds_bytes_per_wave.argtypes = [ctypes.c_int, ctypes.c_int]
+    assert lib.crisp_peak_lds_bytes_per_wave(0, 10) == 10 * 8 * 64 * 16.0   # ds_read_b128
+    assert lib.crisp_peak_lds_bytes_per_wave(1, 10) == 10 * 8 * 64 * 8.0    # ds_read_b64_tr_b16
+    six = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    lib.crisp_peak_lds_read.argtypes = six
+    lib.crisp_peak_valu.argtypes = six
+    assert lib.crisp_peak_lds_read(3, 8, 10, ctypes.c_void_p(16), ctypes.c_void_p(16), None) != 0   # no such kind
+    assert lib.crisp_peak_lds_read(0, 8, 10, None, ctypes.c_void_p(16), None) != 0                  # no output
+    assert lib.crisp_peak_valu(2, 8, 10, ctypes.c_void_p(16), ctypes.c_void_p(16), None) != 0       # no such kind
+    assert lib.crisp_peak_valu(0, 0, 10, ctypes.c_void_p(16), ctypes.c_void_p(16), None) != 0       # no workgroups
 
 
 def _write_csv(path, rows):
