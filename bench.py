@@ -542,6 +542,7 @@ def attn_traffic(kernel_src_hash, workload):
 
 
 COPY_BYTES = 1 << 30
+SIMDS = 256 * 4  # MI355X: 256 CUs x 4 SIMDs
 
 
 def copy_calibration():
@@ -663,11 +664,45 @@ def summarize(args):
                 d["L2_hit"] = med[(k, "TCC_HIT_sum")] / tot if tot else None
             if (k, "GRBM_GUI_ACTIVE") in med and (k, "GRBM_GUI_ACTIVE") in dur:
                 d["clock_ghz"] = med[(k, "GRBM_GUI_ACTIVE")] / 8.0 / statistics.median(dur[(k, "GRBM_GUI_ACTIVE")]) / 1e9
+            # Issue and overlap of the SIMDs, in SIMD-cycles over GRBM_GUI_ACTIVE / 8 XCDs x 1024
+            # SIMDs: SQ_VALU_MFMA_BUSY_CYCLES and SQ_VALU_MFMA_COEXEC_CYCLES count SIMD-cycles,
+            # SQ_ACTIVE_INST_VALU quad-cycles (x 4; it includes the issue of MFMAs, 4 cycles each,
+            # taken out below), SQ_WAIT_INST_ANY and SQ_WAVE_CYCLES wave quad-cycles.
+            if (k, "GRBM_GUI_ACTIVE") in med:
+                simd_cycles = med[(k, "GRBM_GUI_ACTIVE")] / 8.0 * SIMDS
+                if (k, "SQ_VALU_MFMA_BUSY_CYCLES") in med:
+                    d["mfma_busy"] = med[(k, "SQ_VALU_MFMA_BUSY_CYCLES")] / simd_cycles
+                if (k, "SQ_VALU_MFMA_COEXEC_CYCLES") in med:
+                    d["coexec"] = med[(k, "SQ_VALU_MFMA_COEXEC_CYCLES")] / simd_cycles
+                if (k, "SQ_ACTIVE_INST_VALU") in med and (k, "SQ_INSTS_MFMA") in med:
+                    d["valu_busy"] = (4.0 * med[(k, "SQ_ACTIVE_INST_VALU")] - 4.0 * med[(k, "SQ_INSTS_MFMA")]) / simd_cycles
+                if "mfma_busy" in d and "coexec" in d and "valu_busy" in d:
+                    d["valu_only"] = d["valu_busy"] - d["coexec"]
+                    d["neither"] = 1.0 - d["mfma_busy"] - d["valu_only"]
+            if (k, "SQ_WAIT_INST_ANY") in med and (k, "SQ_WAVE_CYCLES") in med:
+                d["wait_inst_frac"] = med[(k, "SQ_WAIT_INST_ANY")] / med[(k, "SQ_WAVE_CYCLES")]
             rec["kernels"][k] = d
             f = lambda key, sc=1.0, fmt="{:.3g}": fmt.format(d[key] / sc) if d.get(key) is not None else ""
             out.append(f"| {k} | {f('counter_run_ms')} | {f('FETCH_bytes', 1e9)} | {f('WRITE_bytes', 1e9)} | "
                        f"{f('bf16_mfma_flop', 1e12)} | {f('f32_mfma_flop', 1e12)} | {f('MfmaUtil')} | {f('LdsUtil')} | "
                        f"{f('L2_hit', 0.01)} | {f('clock_ghz')} |\n")
+        if any("mfma_busy" in d or "valu_busy" in d for d in rec["kernels"].values()):
+            out.append("\n## SIMD issue and overlap per dispatch\n\n")
+            out.append("| kernel | MFMA busy % | VALU busy % (no MFMA issue) | MFMA and VALU together % "
+                       "| VALU with MFMA idle % | neither % | waves waiting on an instruction % |\n"
+                       "|---|---|---|---|---|---|---|\n")
+            for k in kernels:
+                d = rec["kernels"][k]
+                if not any(x in d for x in ("mfma_busy", "valu_busy", "coexec")):
+                    continue
+                g = lambda key: f"{100 * d[key]:.1f}" if d.get(key) is not None else ""
+                out.append(f"| {k} | {g('mfma_busy')} | {g('valu_busy')} | {g('coexec')} | {g('valu_only')} | "
+                           f"{g('neither')} | {g('wait_inst_frac')} |\n")
+            out.append("\nFractions of SIMD-cycles (GRBM_GUI_ACTIVE / 8 XCDs x 1024 SIMDs): MFMA busy = "
+                       "SQ_VALU_MFMA_BUSY_CYCLES; VALU busy = 4 x SQ_ACTIVE_INST_VALU (quad-cycles) less 4 cycles "
+                       "per MFMA issued (SQ_INSTS_MFMA); together = SQ_VALU_MFMA_COEXEC_CYCLES; VALU with MFMA "
+                       "idle = VALU busy - together; neither = the rest (waits on LDS, memory, barriers, "
+                       "dependences).  The last column is SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES.\n")
         out.append("\nMfmaUtil = 100 * (sum of SQ_VALU_MFMA_BUSY_CYCLES) / (GRBM_GUI_ACTIVE * SIMD count), "
                    "rocprofv3's own derived metric; clock = GRBM_GUI_ACTIVE / 8 XCDs / dispatch duration "
                    "in the counter run (counter runs serialise dispatches, so their durations are close to, "
