@@ -392,6 +392,14 @@ def cpu_baseline(cfg, res, budget_s=25.0, full=False):
     }
 
 
+def manifest_id():
+    """Generator version and sha256[:16] of tests/golden/manifests.json (the seeded workloads'
+    realised per-head statistics: C_struct, sink mass, route, k_v, k_s, density)."""
+    from workloads import GEN_VERSION
+    path = os.path.join(ROOT, "tests", "golden", "manifests.json")
+    return {"gen_version": GEN_VERSION, "manifests_sha": src_hash(path) if os.path.exists(path) else None}
+
+
 def measured_peaks():
     """The rates this GPU sustains, beside the published peaks: bf16 MFMA from a register-only
     loop of independent v_mfma_f32_32x32x16_bf16 (2048 workgroups, the chip's clock under
@@ -897,6 +905,9 @@ def main():
                     for f in sorted(os.listdir(os.path.join(ROOT, "paper_2609_01925_amd", "csrc")))
                     if f.endswith((".hip", ".cpp", ".h"))},
         "attn_src_sha": attn_src,
+        # the workload generator's version and the hash of the committed workload manifests
+        # (per-head statistics the generator realises), so that drift in the inputs is visible
+        "workload_manifest": manifest_id(),
     }
     if sweep is not None:
         record["pe_sweep"] = sweep

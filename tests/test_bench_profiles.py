@@ -92,3 +92,36 @@ def test_summary_scales_counters_and_feeds_the_traffic_field(tmp_path, monkeypat
     h = b.src_hash(str(tmp_path / "paper_2609_01925_amd" / "csrc" / "attn.hip"))
     assert b.attn_traffic(h, "test-layer") == pytest.approx(want)
     assert b.attn_traffic("0" * 16, "test-layer") is None      # taken on another kernel source
+
+
+def test_summary_splits_simd_cycles_into_mfma_and_valu_overlap(tmp_path, monkeypatch):
+    """MFMA busy, VALU busy (issue of MFMAs taken out), both at once, VALU with the MFMA idle and
+    neither, as fractions of GRBM_GUI_ACTIVE / 8 XCDs x 1024 SIMDs."""
+    b = _bench()
+    attn = "void crisp::(anonymous namespace)::attn_kernel<128, false>(crisp::(anonymous namespace)::AttnArgs)"
+    grbm = 8 * 1000.0                      # 1000 cycles per XCD -> 1.024e6 SIMD-cycles
+    simd = 1000.0 * 1024
+    vals = {"GRBM_GUI_ACTIVE": grbm, "SQ_VALU_MFMA_BUSY_CYCLES": 0.7 * simd, "SQ_VALU_MFMA_COEXEC_CYCLES": 0.25 * simd,
+            # quad-cycles: 0.4 of the SIMD-cycles of VALU work plus the issue of 1000 MFMAs (4 cycles each)
+            "SQ_ACTIVE_INST_VALU": (0.4 * simd + 4 * 1000.0) / 4, "SQ_INSTS_MFMA": 1000.0,
+            "SQ_WAIT_INST_ANY": 30.0, "SQ_WAVE_CYCLES": 100.0}
+    d = tmp_path / "stall"
+    d.mkdir()
+    rows = [{"Kernel_Name": attn, "Counter_Name": c, "Counter_Value": v, "Start_Timestamp": 0,
+             "End_Timestamp": 1000000} for c, v in vals.items()]
+    _write_csv(d / "pmc_counter_collection.csv", rows)
+    monkeypatch.setattr(b, "ROOT", str(tmp_path))
+    os.makedirs(tmp_path / "paper_2609_01925_amd" / "csrc")
+    args = types.SimpleNamespace(summarize=str(tmp_path), label="crisp_kernels_overlap", command=["cmd"])
+    b.summarize(args)
+    text = open(tmp_path / "profiles" / "crisp_kernels_overlap.md").read()
+    # MFMA 70, VALU 40, together 25, VALU alone 15, neither 100 - 70 - 15 = 15, waiting 30
+    assert "| attn_kernel<128, false> | 70.0 | 40.0 | 25.0 | 15.0 | 15.0 | 30.0 |" in text
+
+
+def test_record_names_the_workload_manifest():
+    b = _bench()
+    m = b.manifest_id()
+    from workloads import GEN_VERSION
+    assert m["gen_version"] == GEN_VERSION
+    assert m["manifests_sha"] == b.src_hash(os.path.join(ROOT, "tests", "golden", "manifests.json"))
