@@ -479,7 +479,7 @@ def measured_peaks():
                                                           ctypes.c_void_p(sink.data_ptr()), stream))
         lds[name] = 8 * lib.crisp_peak_lds_bytes_per_wave(kind, it_c) / c  # bytes per clock per CU (8 waves)
     valu = {}
-    for kind, name in ((0, "exp2_f32"), (1, "fma_f32")):
+    for kind, name in ((0, "exp2_f32"), (1, "fma_f32"), (2, "exp2_f16")):
         c = median_cycles(lambda: lib.crisp_peak_valu(kind, wg_c, it_c, ctypes.c_void_p(cyc.data_ptr()),
                                                       ctypes.c_void_p(sink.data_ptr()), stream))
         valu[name] = c / (2 * it_c * 8)  # SIMD cycles per wave-wide instruction (two waves per SIMD)
@@ -496,7 +496,7 @@ def measured_peaks():
                        "device, 16-byte loads and stores, read + written bytes, median of 10 launches; LDS: "
                        "512 workgroups (8 waves per CU) x 20000 rounds of 8 reads in the attention kernel's K and "
                        "V operand patterns, bytes per core clock per CU from each wave's s_memtime cycles "
-                       "(median wave); VALU: 8 independent chains of v_exp_f32 or v_fma_f32 per wave, two waves "
+                       "(median wave); VALU: 8 independent chains of v_exp_f32, v_fma_f32 or v_exp_f16 per wave, two waves "
                        "per SIMD, SIMD cycles per wave-wide instruction")}
 
 

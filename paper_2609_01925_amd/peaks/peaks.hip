@@ -165,12 +165,31 @@ __global__ __launch_bounds__(256) void peak_lds_read(int iters, unsigned long lo
 
 // VALU issue cost: each wave runs `iters` rounds of 8 independent chains of one
 // instruction each, kind 0: x = exp2(-x) (v_exp_f32; values stay in [0.5, 1]), kind 1:
-// x = fma(x, 0.5, 0.25) (v_fma_f32, full rate).  cycles[wave] as above.  The launch
-// reserves 64 KiB of LDS (unused), so two workgroups share a CU and 512 workgroups give
-// two waves per SIMD.
+// x = fma(x, 0.5, 0.25) (v_fma_f32, full rate), kind 2: x = exp2(-x) in half precision
+// (v_exp_f16 on the low 16 bits; values stay in [0.5, 1]).  cycles[wave] as above.  The
+// launch reserves 64 KiB of LDS (unused), so two workgroups share a CU and 512 workgroups
+// give two waves per SIMD.
 template <int KIND>
 __global__ __launch_bounds__(256) void peak_valu(int iters, unsigned long long* cycles, float* sink) {
   const int tid = threadIdx.x, l = tid & 63;
+  if constexpr (KIND == 2) {
+    unsigned h[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) h[k] = 0x3800u + ((l + k) & 63);  // 0.5 + a few ulp, as half bits
+    __syncthreads();
+    const unsigned long long t0 = __builtin_amdgcn_s_memtime();
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) asm volatile("v_exp_f16 %0, -%0" : "+v"(h[k]));
+    }
+    unsigned sh = 0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) sh += h[k] & 0xffffu;
+    const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+    if (l == 0) cycles[(size_t)blockIdx.x * 4 + (tid >> 6)] = t1 - t0;
+    sink[(size_t)blockIdx.x * 256 + tid] = (float)sh;
+    return;
+  }
   float x[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) x[k] = 0.5f + 0.001f * (float)((l + k) & 63);
@@ -245,11 +264,13 @@ int crisp_peak_lds_read(int kind, int workgroups, int iters, unsigned long long*
 // Instructions one wave issues in a crisp_peak_valu call: iters x 8.
 // cycles: uint64[workgroups * 4], sink: float[workgroups * 256], both on the device.
 int crisp_peak_valu(int kind, int workgroups, int iters, unsigned long long* cycles, float* sink, void* stream) {
-  if (workgroups <= 0 || iters <= 0 || !cycles || !sink || kind < 0 || kind > 1) return (int)hipErrorInvalidValue;
+  if (workgroups <= 0 || iters <= 0 || !cycles || !sink || kind < 0 || kind > 2) return (int)hipErrorInvalidValue;
   if (kind == 0)
     hipLaunchKernelGGL(peak_valu<0>, dim3(workgroups), dim3(256), kLdsAlloc, (hipStream_t)stream, iters, cycles, sink);
-  else
+  else if (kind == 1)
     hipLaunchKernelGGL(peak_valu<1>, dim3(workgroups), dim3(256), kLdsAlloc, (hipStream_t)stream, iters, cycles, sink);
+  else
+    hipLaunchKernelGGL(peak_valu<2>, dim3(workgroups), dim3(256), kLdsAlloc, (hipStream_t)stream, iters, cycles, sink);
   return (int)hipGetLastError();
 }
 

@@ -48,7 +48,7 @@ def test_peaks_library_exports_and_validates():
     lib.crisp_peak_valu.argtypes = six
     assert lib.crisp_peak_lds_read(3, 8, 10, ctypes.c_void_p(16), ctypes.c_void_p(16), None) != 0   # no such kind
     assert lib.crisp_peak_lds_read(0, 8, 10, None, ctypes.c_void_p(16), None) != 0                  # no output
-    assert lib.crisp_peak_valu(2, 8, 10, ctypes.c_void_p(16), ctypes.c_void_p(16), None) != 0       # no such kind
+    assert lib.crisp_peak_valu(3, 8, 10, ctypes.c_void_p(16), ctypes.c_void_p(16), None) != 0       # no such kind
     assert lib.crisp_peak_valu(0, 0, 10, ctypes.c_void_p(16), ctypes.c_void_p(16), None) != 0       # no workgroups
 
 
