@@ -39,7 +39,10 @@
 // no longer meet in L2: there the grid has one workgroup per unit, and every
 // workgroup takes the next unit of the group lists in order (one KV group after
 // the other, longest first within a group), so units that start together
-// advance together over the same group's K/V.
+// advance together over the same group's K/V.  Up to 8192 tokens (a few short units
+// per workgroup, K/V of the whole layer within the caches) the persistent grid takes
+// its units without atomics: one longest-first list of all units, workgroup i taking
+// items i, i + grid, i + 2 grid, ...
 #include <atomic>
 #include <type_traits>
 
@@ -63,6 +66,7 @@ struct Tile {
 constexpr float kSumLimit = 256.0f;          // a lane's tile sum of P above this forces a rescale
 constexpr int kCostBuckets = 8192;
 constexpr int kOneShotMinLen = 1 << 19;  // from this length on, sparse lists run one unit per workgroup
+constexpr int kStaticListMaxLen = 8192;  // up to this length, one list taken in a fixed stride (no atomics)
 constexpr int kMinChunk = 8;             // shortest chunk of a split row, in list entries
 constexpr int kItemUnitBits = 21;        // work item = unit | chunk << 21
 
@@ -77,6 +81,7 @@ struct AttnArgs {
   const int32_t* order;  // persistent mode: units sorted longest first
   int* counter;          // persistent mode: next position in `order`
   int one_shot;          // 1: one unit per workgroup, all units in one queue
+  int static_list;       // 1: all units in queue 0, workgroup i takes items i, i + grid, ...
   int* slot_base;        // split rows: first partial slot of the row's chunks, else -1
   int* split_rows;       // the split rows (any order)
   float* parts;          // partial results per slot: O[BQ][128], m[BQ], l[BQ] (fp32)
@@ -618,9 +623,17 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
   // A queue whose counter already reads past its end is skipped without an atomic
   // (a stale read only costs an extra atomic: counters never decrease).
   unsigned dry = 0u;
+  int spos = blockIdx.x;  // static list: the next item of this workgroup
   for (;;) {
     __syncthreads();  // the previous unit is done with LDS and the unit slot
-    if (tid == 0) {
+    if (a.static_list) {
+      // Short layers: the pop's atomic and the wait for it cost about as much as a unit's
+      // tiles; a fixed stride over one longest-first list balances as well (each round of
+      // grid items is no longer than the previous one).  Every wave computes the same item.
+      const int item = spos < start[1] - start[0] ? a.order[start[0] + spos] : -1;
+      spos += gridDim.x;
+      if (tid == 0) *s_unit = item;
+    } else if (tid == 0) {
       int unit = -1;
       for (int t = 0; t < kNumXcd && unit < 0; ++t) {
         const int x = (x0 + t) % kNumXcd;
@@ -665,8 +678,9 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
 // for them (separate queues let the XCDs of a group drift apart over a long
 // layer, and each then streams K/V from HBM on its own).  Within an XCD the
 // group's heads share its L2.  One-unit-per-workgroup mode empties the slots in
-// order.  Items are ordered longest first within a queue (a counting sort of
-// list lengths: exact up to 768 entries, then in steps of 16).
+// order; static-list mode (short layers) puts every unit in slot 0.  Items are
+// ordered longest first within a queue (a counting sort of list lengths: exact up to
+// 768 entries, then in steps of 16).
 //
 // Split rows (persistent mode): a workgroup runs a row's tiles one after the
 // other, so when the longest row holds more entries than the layer's work per
@@ -771,7 +785,7 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
     if (s_max > c) C = (int)c;
   }
   auto key = [&](int h, int len) {
-    return unit_queue(a, h) * kQueueBuckets + (kQueueBuckets - 1 - cost_bucket(len));
+    return (a.static_list ? 0 : unit_queue(a, h)) * kQueueBuckets + (kQueueBuckets - 1 - cost_bucket(len));
   };
   each_unit([&](int u, int L) {
     const int h = u / a.nb;
@@ -992,7 +1006,7 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
   AttnArgs a;
   a.q = q; a.k = k; a.v = v; a.o = o;
   a.row_ptr = row_ptr; a.col_idx = col_idx; a.col_cap = col_cap;
-  a.order = nullptr; a.counter = nullptr; a.one_shot = 0;
+  a.order = nullptr; a.counter = nullptr; a.one_shot = 0; a.static_list = 0;
   a.slot_base = nullptr; a.split_rows = nullptr; a.parts = nullptr; a.split_slots = 0; a.grid = 0;
   a.n = d.n; a.nb = d.nb; a.hq = d.hq; a.hkv = d.hkv; a.G = d.G;
   a.c = scale * kLog2e;
@@ -1013,6 +1027,7 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
     a.counter = reinterpret_cast<int*>(sc);
     a.order = reinterpret_cast<const int32_t*>(sc) + 64;
     a.one_shot = d.n >= kOneShotMinLen ? 1 : 0;
+    a.static_list = d.n <= kStaticListMaxLen ? 1 : 0;
     a.split_slots = sl.slots;
     if (sl.slots > 0) {
       a.slot_base = reinterpret_cast<int*>(sc + sl.slot_base);
