@@ -772,8 +772,17 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
       t += (unsigned long long)L;
       mx = L > mx ? L : mx;
     });
-    atomicAdd(&s_tot, t);
-    atomicMax(&s_max, mx);
+    // one LDS atomic per wave, not per thread
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      t += (unsigned long long)__shfl_xor((long long)t, o);
+      const int m2 = __shfl_xor(mx, o);
+      mx = m2 > mx ? m2 : mx;
+    }
+    if ((tid & 63) == 0) {
+      atomicAdd(&s_tot, t);
+      atomicMax(&s_max, mx);
+    }
     __syncthreads();
     long long gp = a.split_slots / 2;
     gp = a.grid < gp ? a.grid : gp;
