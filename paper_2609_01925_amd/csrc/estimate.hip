@@ -355,8 +355,8 @@ EstSplit est_split(const Dims& d) {
   // Target: one resident round of workgroups (4 per CU), never more.  Each head gets at
   // most want / hq ranges, so the (head, range) pairs fit one round; rounding the
   // blocks per range over all heads at once (ceil(nb hq / want)) could leave a few
-  // pairs to a second round that then runs almost alone (36 extra at 512k tokens, 28
-  // heads: 0.80 -> 0.72 ms).
+  // pairs to a second round that then runs almost alone (12 of 1036 at 512k tokens,
+  // 28 heads: 0.80 -> 0.72 ms).
   const int64_t want = 1024;
   int64_t per_head = want / (d.hq > 0 ? d.hq : 1);
   if (per_head < 1) per_head = 1;
