@@ -23,6 +23,8 @@
 //            (in flat order qb * N_b + kb) complete the gamma mass.
 // CSR: count per row -> per-head scan -> fill, one wave per row, ballots for
 // compaction; rows always hold the sink block 0 and the diagonal block qb.
+// Short layers (N_b <= 64): after the pooling, one workgroup per head takes all of the
+// above with every intermediate in LDS and the VS directions one wave each (sel_small).
 #include "crisp_device.h"
 #include "crisp_internal.h"
 
@@ -114,19 +116,27 @@ __device__ int block_sum_1024(int x, int* wtot) {
 }
 
 // Digit search of a radix select, by one whole wave: bins[0 .. nbins) (nbins a
-// multiple of 64) hold non-negative weights (counts or fixed-point masses) of the
-// candidates whose higher digits match, visited from bin nbins - 1 down.  Returns
-// the first bin at which the cumulative weight reaches need (>= 1), with *before
-// the weight of the bins above it, or -1 when the total stays below need.  Lane l
-// sums its own run of nbins / 64 bins; a prefix scan over the lanes finds the run
-// that crosses need, and only that lane walks its run.
+// power of two from 64 to 4096) hold non-negative weights (counts or fixed-point
+// masses) of the candidates whose higher digits match, visited from bin nbins - 1
+// down.  Returns the first bin at which the cumulative weight reaches need (>= 1), with
+// *before the weight of the bins above it, or -1 when the total stays below need.
+// Lane l sums its own run of nbins / 64 bins (starting at a lane-dependent offset in
+// the run, so that the lanes' reads fall in different LDS banks: the sums are of
+// integers, so the order does not matter); a prefix scan over the lanes finds the run
+// that crosses need, and the wave then scans that run, one bin per lane.
 template <typename T>
 __device__ int wave_descend_find(const T* bins, int nbins, T need, T* before) {
   const int l = lane_id();
   const int per = nbins / 64;
   const int top = nbins - 1 - per * l;
   T own = 0;
-  for (int i = 0; i < per; ++i) own += bins[top - i];
+  for (int i0 = 0; i0 < per; i0 += 8) {  // eight reads in flight, then their sum
+    T v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = i0 + j < per ? bins[top - ((i0 + j + l) & (per - 1))] : (T)0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) own += v[j];
+  }
   T incl = own;
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
@@ -136,17 +146,31 @@ __device__ int wave_descend_find(const T* bins, int nbins, T need, T* before) {
   const uint64_t hit = __ballot(incl >= need);
   if (hit == 0) return -1;
   const int lw = __builtin_ctzll(hit);
+  const T base = __shfl(incl - own, lw, 64);  // weight of the runs above run lw
+  const int top_w = nbins - 1 - per * lw;
+  T v = 0;
   int d = 0;
-  T cum = incl - own;
-  if (l == lw) {
-    d = top;
-    for (int i = 0; i < per - 1; ++i, --d) {
-      if (cum + bins[d] >= need) break;
-      cum += bins[d];
+  T cum = 0;
+  for (int j0 = 0; j0 < per; j0 += 64) {  // the run, 64 bins at a time from its top
+    const int j = j0 + l;
+    v = j < per ? bins[top_w - j] : (T)0;
+    T c = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const T y = __shfl_up(c, o, 64);
+      if (l >= o) c += y;
     }
+    const uint64_t cross = __ballot(j < per && base + cum + c >= need);
+    if (cross) {
+      const int lj = __builtin_ctzll(cross);
+      d = top_w - (j0 + lj);
+      cum = base + cum + __shfl(c - v, lj, 64);
+      break;
+    }
+    cum += __shfl(c, 63, 64);
   }
-  *before = __shfl(cum, lw, 64);
-  return __shfl(d, lw, 64);
+  *before = cum;
+  return d;
 }
 
 // k-th largest bit pattern (k >= 1) among fbits(p[0..nb)).
@@ -638,74 +662,81 @@ __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
 }
 
 // Short layers (N_b <= kPeSmall): the whole pooled triangle of one PE head in one
-// workgroup.  Q_bar and K_bar rows go to LDS once (float4 columns swizzled by row so the
-// operand reads of 32 rows spread over the banks), wave w computes the 32 x 32 quarter
-// (query blocks 32 (w >> 1) .., key blocks 32 (w & 1) ..) on fp32 MFMA with the same d
-// split as sel_pe_logits, the logits go back to LDS, and each wave takes the row softmax
-// (divided by N_b) of every fourth row from there.  grid hq, 256 threads.
-constexpr int kPeSmall = 64, kPeSmallPitch = kPeSmall + 1;
+// workgroup of 16 waves.  Q_bar and K_bar rows go to LDS once (float4 columns swizzled by
+// row so the operand reads of 32 rows spread over the banks).  Each of the triangle's
+// three non-empty 32 x 32 quarters (query blocks 32 i .., key blocks 32 j .., j <= i) is
+// split over d into four runs of 32: wave w < 12 computes quarter w / 4 over run w % 4
+// on fp32 MFMA (within the run, the d split of sel_pe_logits), the twelve partial
+// products go back to LDS, and the row softmax (divided by N_b) adds the four runs of
+// each logit in run order.  The waves take the rows in turn, writing row qb at
+// At[qb (qb + 1) / 2 ..] (global memory or LDS).  buf holds 2 kPeSmall kHeadDim floats.
+constexpr int kPeSmall = 64, kPartPitch = 33;
 
-__device__ void pe_small_head(const SelArgs& a, int h, float* sq, float* sk) {
+__device__ void pe_small_head(const SelArgs& a, int h, float* buf, float* At) {
   const int tid = threadIdx.x, nthr = blockDim.x, nwav = nthr >> 6;
   const int w = tid >> 6, l = tid & 63, nb = a.nb;
+  float* sq = buf;
+  float* sk = buf + kPeSmall * kHeadDim;
   const float* Qb = a.qbar + (size_t)h * nb * kHeadDim;
   const float* Kb = a.kbar + (size_t)(h / a.G) * nb * kHeadDim;
   auto phys = [](int r, int c4) { return r * kHeadDim + 4 * (c4 ^ (r & 31)); };
   for (int f = tid; f < kPeSmall * kHeadDim / 4; f += nthr) {  // kPeSmall rows x 32 float4
     const int r = f >> 5, c4 = f & 31;
-    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
-    *reinterpret_cast<float4*>(&sq[phys(r, c4)]) =
-        r < nb ? *reinterpret_cast<const float4*>(Qb + (size_t)r * kHeadDim + 4 * c4) : z;
-    *reinterpret_cast<float4*>(&sk[phys(r, c4)]) =
-        r < nb ? *reinterpret_cast<const float4*>(Kb + (size_t)r * kHeadDim + 4 * c4) : z;
+    float4 x = make_float4(0.f, 0.f, 0.f, 0.f), y = x;
+    if (r < nb) {
+      x = *reinterpret_cast<const float4*>(Qb + (size_t)r * kHeadDim + 4 * c4);
+      y = *reinterpret_cast<const float4*>(Kb + (size_t)r * kHeadDim + 4 * c4);
+    }
+    *reinterpret_cast<float4*>(&sq[phys(r, c4)]) = x;
+    *reinterpret_cast<float4*>(&sk[phys(r, c4)]) = y;
   }
   __syncthreads();
-  const int qs0 = 32 * (w >> 1), ks0 = 32 * (w & 1);
-  const bool work = w < 4 && ks0 <= qs0 && qs0 < nb;  // waves 0..3 take the four quarters
+  const int quarter = w >> 2, run = w & 3;
+  const int qs0 = quarter == 0 ? 0 : 32, ks0 = quarter == 2 ? 32 : 0;
+  const bool work = w < 12 && qs0 < nb;
   f32x16 acc = zero16();
   if (work) {
     const int qr = qs0 + (l & 31), kr = ks0 + (l & 31);
 #pragma unroll
-    for (int c = 0; c < kHeadDim / 16; ++c) {
+    for (int c = 2 * run; c < 2 * run + 2; ++c) {
       const int c4 = 4 * c + 2 * (l >> 5);  // lanes 0..31: d 16 c .. +7; lanes 32..63: d 16 c + 8 .. +15
       const float4 x0 = *reinterpret_cast<const float4*>(&sq[phys(qr, c4)]);
       const float4 x1 = *reinterpret_cast<const float4*>(&sq[phys(qr, c4 + 1)]);
       const float4 y0 = *reinterpret_cast<const float4*>(&sk[phys(kr, c4)]);
       const float4 y1 = *reinterpret_cast<const float4*>(&sk[phys(kr, c4 + 1)]);
-      const float av[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-      const float bv[8] = {y0.x, y0.y, y0.z, y0.w, y1.x, y1.y, y1.z, y1.w};
-#pragma unroll
-      for (int u = 0; u < 8; ++u) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[u], bv[u], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x0.x, y0.x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x0.y, y0.y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x0.z, y0.z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x0.w, y0.w, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x1.x, y1.x, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x1.y, y1.y, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x1.z, y1.z, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(x1.w, y1.w, acc, 0, 0, 0);
     }
   }
-  __syncthreads();  // every operand read is done before the logits overwrite sq
-  float* lg = sq;
+  __syncthreads();  // every operand read is done before the partial products overwrite buf
+  // partial products: [run][quarter][32 rows][kPartPitch]
+  constexpr int kQuarter = 32 * kPartPitch, kRun = 3 * kQuarter;
   if (work) {
-    const int kb = ks0 + (l & 31);
+    float* P = buf + run * kRun + quarter * kQuarter + (l & 31);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int qb = qs0 + 8 * (r >> 2) + 4 * (l >> 5) + (r & 3);
-      lg[qb * kPeSmallPitch + kb] = acc[r] * a.c2;
-    }
+    for (int r = 0; r < 16; ++r) P[(8 * (r >> 2) + 4 * (l >> 5) + (r & 3)) * kPartPitch] = acc[r];
   }
   __syncthreads();
-  float* At = a.atil + (size_t)h * a.cap;
   const float inv_nb = 1.f / (float)nb;
   for (int qb = w; qb < nb; qb += nwav) {
     const bool in = l <= qb;
-    const float x = in ? lg[qb * kPeSmallPitch + l] : -__builtin_inff();
+    float x = -__builtin_inff();
+    if (in) {
+      const int qd = qb < 32 ? 0 : (l < 32 ? 1 : 2);
+      const float* P = buf + qd * kQuarter + (qb & 31) * kPartPitch + (l & 31);
+      x = (((P[0] + P[kRun]) + P[2 * kRun]) + P[3 * kRun]) * a.c2;
+    }
     const float mx = wave_max(x);
     const float p = in ? fast_exp2(x - mx) : 0.f;
     const float sum = wave_sum(p);
     if (in) At[(int64_t)qb * (qb + 1) / 2 + l] = p / sum * inv_nb;
   }
-}
-
-__global__ __launch_bounds__(256) void sel_pe_small(SelArgs a) {
-  __shared__ __attribute__((aligned(16))) float sq[kPeSmall * kHeadDim];  // reused for the logits
-  __shared__ __attribute__((aligned(16))) float sk[kPeSmall * kHeadDim];
-  if (a.route[blockIdx.x] != 1) return;
-  pe_small_head(a, blockIdx.x, sq, sk);
 }
 
 // Reduction of one value per thread of a 256-thread workgroup in binary-tree order
@@ -857,9 +888,11 @@ __global__ __launch_bounds__(256) void sel_radix_scan(SelArgs a, int pass) {
 // workgroup per head: the three digit passes of sel_radix_hist / sel_radix_scan
 // with the histograms in LDS.  The masses are the same fixed-point integers, so
 // t*, the remaining mass and the count of pairs equal to t* are the same; one
-// launch replaces seven.  grid hq, 1024 threads.
-__device__ void radix_small_head(const SelArgs& a, int h, unsigned long long* bins, RState& sst) {
-  const int tid = threadIdx.x;
+// launch replaces seven.  At holds the head's cap scores (global memory or LDS); the
+// state ends in sst (LDS) and, when out is given, in *out.
+__device__ void radix_small_head(const SelArgs& a, const float* At, unsigned long long* bins, RState& sst,
+                                 RState* out) {
+  const int tid = threadIdx.x, nthr = blockDim.x;
   if (tid == 0) {
     sst.prefix = 0;
     sst.all = 0;
@@ -868,18 +901,17 @@ __device__ void radix_small_head(const SelArgs& a, int h, unsigned long long* bi
     sst.ceq = 0;
     sst.pad = 0;
   }
-  const float* At = a.atil + (size_t)h * a.cap;
   for (int pass = 0; pass < 3; ++pass) {
     int shift, nbits;
     radix_digit(pass, shift, nbits);
     const int nbins = 1 << nbits;
-    for (int i = tid; i < nbins; i += 1024) bins[i] = 0ull;
+    for (int i = tid; i < nbins; i += nthr) bins[i] = 0ull;
     __syncthreads();  // bins cleared; sst of the previous pass visible
     if (sst.all) break;
     const int hi = shift + nbits;
     const uint64_t want = (uint64_t)sst.prefix >> hi;
     const uint32_t dmask = (uint32_t)nbins - 1u;
-    for (int64_t i = tid; i < a.cap; i += 1024) {
+    for (int64_t i = tid; i < a.cap; i += nthr) {
       const uint32_t b = fbits(At[i]);
       if (((uint64_t)b >> hi) == want) atomicAdd(&bins[(b >> shift) & dmask], fixed_mass(b));
     }
@@ -903,14 +935,16 @@ __device__ void radix_small_head(const SelArgs& a, int h, unsigned long long* bi
     }
     __syncthreads();  // the search is done with the bins before the next pass clears them
   }
-  if (tid == 0) a.rstate[h] = sst;
+  if (tid == 0 && out) *out = sst;
 }
 
+// grid hq, 1024 threads.
 __global__ __launch_bounds__(1024) void sel_radix_small(SelArgs a) {
   __shared__ unsigned long long bins[kRadixBins];
   __shared__ RState sst;
-  if (a.route[blockIdx.x] != 1) return;
-  radix_small_head(a, blockIdx.x, bins, sst);
+  const int h = blockIdx.x;
+  if (a.route[h] != 1) return;
+  radix_small_head(a, a.atil + (size_t)h * a.cap, bins, sst, a.rstate + h);
 }
 
 // Per-row counts.  VS: x = row size.  PE: x = #(> t*), y = #(== t*), z = flags
@@ -1105,46 +1139,224 @@ __global__ __launch_bounds__(256) void sel_csr_fill(SelArgs a) {
   if (qb < a.nb) csr_fill_row(a, blockIdx.y, qb);
 }
 
-// Short layers (N_b <= kCsrSmall): count, scan and fill of one head in one launch, the
-// 16 waves taking rows w, w + 16, ... (the same lists as the three kernels above).
-// grid hq, 1024 threads.
-constexpr int kCsrSmall = 64;
-__device__ void csr_small_head(const SelArgs& a, int h, long long* wtot) {
-  const int w = threadIdx.x >> 6;
-  for (int qb = w; qb < a.nb; qb += 16) csr_count_row(a, h, qb);
-  __syncthreads();  // every row's counts are visible to the whole workgroup
-  csr_scan_head(a, h, wtot);
-  __syncthreads();  // row_ptr and the ties taken per row are visible
-  for (int qb = w; qb < a.nb; qb += 16) csr_fill_row(a, h, qb);
+// ---------------------------------------------------------------------------
+// Short layers (N_b <= kPeSmall): after the pooling, the route, the selection and the
+// lists of one head in one workgroup, with every intermediate in LDS (the direction
+// masks as 64-bit words, the pooled scores, the radix bins, the per-row counts and
+// offsets), so no phase waits on a round trip through global memory.  With at most 64
+// blocks a VS direction fits one wave, one block per lane, and both directions run at
+// once on waves 0 and 1.  Their decisions are those of route_vs_dir, reached with
+// ballots and shuffles instead of histogram passes: the k-th largest bit pattern is
+// found bit by bit from the top as the largest t with #{b >= t} >= k, and the gamma cut
+// as the largest t whose mass at or above t (the same 2^-60 fixed-point integers)
+// reaches gamma -- the values the digit passes settle on, since both counts only fall
+// as t grows.  The PE scores, softmax and cutoff are pe_small_head and
+// radix_small_head on LDS, and the lists follow the rules of csr_count_row,
+// csr_scan_head and csr_fill_row, one wave per row.  grid hq, kSmallThreads threads.
+constexpr int kSmallThreads = 1024;
+
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
 }
 
-__global__ __launch_bounds__(1024) void sel_csr_small(SelArgs a) {
-  __shared__ long long wtot[16];
-  csr_small_head(a, blockIdx.x, wtot);
+// k-th largest (k >= 1) of the bit patterns b of the lanes with `in` set (k of them at least).
+__device__ __forceinline__ uint32_t wave_kth_largest(uint32_t b, bool in, int k) {
+  uint32_t t = 0;
+  for (int bit = 31; bit >= 0; --bit) {
+    const uint32_t c = t | (1u << bit);
+    if (__popcll(__ballot(in && b >= c)) >= k) t = c;
+  }
+  return t;
 }
 
-// Short layers (N_b <= kPeSmall, so also N_b <= kCsrSmall and the PE cutoff fits one
-// workgroup): after the pooling, the whole selection of one head in one launch -- the
-// route and both VS directions, or the PE scores, softmax and gamma cutoff, then the
-// CSR lists -- the same computations as the separate kernels, phase after phase.
-// grid hq, 1024 threads.
-__global__ __launch_bounds__(1024) void sel_small(SelArgs a) {
-  __shared__ __attribute__((aligned(16))) float sbuf[2 * kPeSmall * kHeadDim];  // 64 KB, per phase
-  __shared__ RState sst;
-  const int h = blockIdx.x;
+// select_top_k for one block per lane: the kd largest patterns of the lanes below nb,
+// ties at the k-th taken in block order.
+__device__ __forceinline__ bool wave_top_k(uint32_t b, bool in, int kd) {
+  const uint32_t t = wave_kth_largest(b, in, kd);
+  const int ngt = __popcll(__ballot(in && b > t));
+  const bool eq = in && b == t;
+  const int rank = __popcll(__ballot(eq) & lanemask_lt());
+  return in && (b > t || (eq && rank < kd - ngt));
+}
+
+// Direction dir's block set of a VS head with nb > 2 blocks (route_vs_dir), lane = block.
+__device__ bool small_vs_dir(const SelArgs& a, int h, int dir) {
+  const int l = lane_id(), nb = a.nb;
+  const bool in = l < nb;
+  const float p = in ? (dir == 0 ? a.p_v : a.p_s)[(size_t)h * nb + l] : 0.f;
+  const uint32_t b = in ? fbits(p) : 0u;
+  if (a.vs_mode == 1) {
+    const unsigned long long need = (unsigned long long)ceil((double)a.gamma * kFix);
+    const unsigned long long m = in ? fixed_mass(b) : 0ull;
+    int c = nb, ceq = 0;
+    uint32_t t = 0;
+    const bool all = wave_sum_u64(m) < need;  // the total mass never reaches gamma
+    if (!all) {
+      for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t x = t | (1u << bit);
+        if (wave_sum_u64(b >= x ? m : 0ull) >= need) t = x;
+      }
+      const unsigned long long rest = need - wave_sum_u64(b > t ? m : 0ull);
+      const unsigned long long mt = fixed_mass(t);  // > 0: t carries mass
+      ceq = (int)((rest + mt - 1) / mt);
+      c = __popcll(__ballot(in && b > t)) + ceq;
+    }
+    int kd = c > a.k_min ? c : a.k_min;
+    kd = kd < nb ? kd : nb;
+    if (kd != c) return wave_top_k(b, in, kd);
+    const bool eq = in && b == t;
+    const int rank = __popcll(__ballot(eq) & lanemask_lt());
+    return in && (all || b > t || (eq && rank < ceq));
+  }
+  float mu;
+  if (a.floor_mode == 1) {  // median of p[1 .. nb-2]
+    const int m = nb - 2;
+    const bool mid = l >= 1 && l <= nb - 2;
+    const float hi = __uint_as_float(wave_kth_largest(b, mid, m / 2 + (m & 1)));
+    if (m & 1) {
+      mu = hi;
+    } else {
+      const float lo = __uint_as_float(wave_kth_largest(b, mid, m / 2 + 1));
+      mu = (lo + hi) * 0.5f;
+    }
+  } else {
+    const float r = fmaxf((1.0f - __shfl(p, 0, 64)) - __shfl(p, nb - 1, 64), 0.0f);
+    mu = r / (float)(nb - 2);
+  }
+  const float thr = a.alpha * mu;
+  const bool above = in && p > thr;
+  const int c = __popcll(__ballot(above));
+  int kd = c > a.k_min ? c : a.k_min;
+  kd = kd < nb ? kd : nb;
+  return kd == c ? above : wave_top_k(b, in, kd);
+}
+
+struct SmallShared {
+  float ops[2 * kPeSmall * kHeadDim];  // Q_bar and K_bar rows, the partial products, then the radix bins
+  float at[kPeSmall * (kPeSmall + 1) / 2];  // the head's pooled scores, row qb at qb (qb + 1) / 2
+  uint64_t sel[kPeSmall];  // per row: VS the blocks taken; PE those above t*
+  uint64_t eqm[kPeSmall];  // PE, per row: the blocks equal to t*
+  int4 info[kPeSmall];     // per row: (#above t* or row size, #equal, flags, ties taken)
+  int rp[kPeSmall];
+  uint64_t dmask[2];
+  RState st;
+};
+
+__global__ __launch_bounds__(kSmallThreads) void sel_small(SelArgs a) {
+  __shared__ __attribute__((aligned(16))) SmallShared sm;
+  const int h = blockIdx.x, tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+  const int nb = a.nb;
   const bool vs = a.c_struct[h] >= a.tau;
-  VsShared& vsh = *reinterpret_cast<VsShared*>(sbuf);
-  for (int dir = 0; dir < 2; ++dir) {  // writes the route, and the direction masks (zero on a PE head)
-    route_vs_dir(a, h, dir, vsh);
-    __syncthreads();
+  if (tid == 0) a.route[h] = vs ? 0 : 1;
+  if (w < 2) {  // wave w: direction w (no blocks on a PE head or with N_b <= 2)
+    const bool s = vs && nb > 2 && small_vs_dir(a, h, w);
+    const uint64_t bits = __ballot(s);
+    if (l == 0) sm.dmask[w] = bits;
+    if (a.dir_mask && l < nb) a.dir_mask[((size_t)h * 2 + w) * nb + l] = s;
   }
   if (!vs) {
-    pe_small_head(a, h, sbuf, sbuf + kPeSmall * kHeadDim);
-    __syncthreads();
-    radix_small_head(a, h, reinterpret_cast<unsigned long long*>(sbuf), sst);
-    __syncthreads();
+    pe_small_head(a, h, sm.ops, sm.at);
+    __syncthreads();  // every score is in sm.at; sm.ops is free
+    radix_small_head(a, sm.at, reinterpret_cast<unsigned long long*>(sm.ops), sm.st, nullptr);
   }
-  csr_small_head(a, h, reinterpret_cast<long long*>(sbuf));
+  __syncthreads();  // the direction masks, or the PE state
+  const uint64_t lt = lanemask_lt();
+  // per-row counts (csr_count_row); a wave's rows are w + 16 i, their scores read together
+  constexpr int kRowsPerWave = kPeSmall / (kSmallThreads / 64);
+  uint32_t rb[kRowsPerWave];
+#pragma unroll
+  for (int i = 0; i < kRowsPerWave; ++i) {
+    const int qb = w + (kSmallThreads / 64) * i;
+    rb[i] = !vs && qb < nb && l <= qb ? fbits(sm.at[qb * (qb + 1) / 2 + l]) : 0u;
+  }
+#pragma unroll
+  for (int i = 0; i < kRowsPerWave; ++i) {
+    const int qb = w + (kSmallThreads / 64) * i;
+    if (qb >= nb) break;
+    const bool on = l <= qb;
+    int4 info;
+    if (vs) {
+      const uint64_t vm = sm.dmask[0], smk = sm.dmask[1];
+      const bool sel = on && (l == 0 || l == qb || ((vm >> l) & 1) || ((smk >> (nb - 1 - qb + l)) & 1));
+      const uint64_t bal = __ballot(sel);
+      if (l == 0) sm.sel[qb] = bal;
+      info = make_int4(__popcll(bal), 0, 0, 0);
+    } else {
+      const RState st = sm.st;
+      const uint32_t b = rb[i];
+      const uint64_t gt = __ballot(on && (st.all || b > st.prefix));
+      const uint64_t eq = __ballot(on && !st.all && b == st.prefix);
+      if (l == 0) {
+        sm.sel[qb] = gt;
+        sm.eqm[qb] = eq;
+      }
+      const int flags = (int)(gt & 1) | (int)((eq & 1) << 1) | (int)(((gt >> qb) & 1) << 2) |
+                        (int)(((eq >> qb) & 1) << 3);
+      info = make_int4(__popcll(gt), __popcll(eq), flags, 0);
+    }
+    if (l == 0) sm.info[qb] = info;
+  }
+  __syncthreads();
+  // ties taken per PE row and the row offsets (csr_scan_head), wave 0, lane = row
+  if (w == 0) {
+    int4 in = l < nb ? sm.info[l] : make_int4(0, 0, 0, 0);
+    int cnt = in.x;
+    if (!vs) {
+      int incl = in.y;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(incl, o, 64);
+        if (l >= o) incl += y;
+      }
+      const unsigned long long tie_prefix = (unsigned long long)(incl - in.y);
+      const unsigned long long ceq = sm.st.ceq;
+      int take = 0;
+      if (ceq > tie_prefix) {
+        const unsigned long long left = ceq - tie_prefix;
+        take = left < (unsigned long long)in.y ? (int)left : in.y;
+      }
+      const bool z_sel = (in.z & 1) || ((in.z & 2) && take >= 1);
+      const bool d_sel = (in.z & 4) || ((in.z & 8) && take == in.y);
+      cnt = in.x + take + (z_sel ? 0 : 1) + ((l > 0 && !d_sel) ? 1 : 0);
+      in.w = take;
+      if (l < nb) sm.info[l] = in;
+    }
+    if (l >= nb) cnt = 0;
+    int incl = cnt;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int y = __shfl_up(incl, o, 64);
+      if (l >= o) incl += y;
+    }
+    int32_t* rp = a.row_ptr + (size_t)h * (nb + 1);
+    if (l < nb) {
+      sm.rp[l] = incl - cnt;
+      rp[l] = incl - cnt;
+    }
+    if (l == nb - 1) rp[nb] = incl;
+  }
+  __syncthreads();
+  // the lists (csr_fill_row)
+  int32_t* out = a.col_idx + (size_t)h * a.col_cap;
+#pragma unroll
+  for (int i = 0; i < kRowsPerWave; ++i) {
+    const int qb = w + (kSmallThreads / 64) * i;
+    if (qb >= nb) break;
+    const bool on = l <= qb;
+    bool sel;
+    if (vs) {
+      sel = (sm.sel[qb] >> l) & 1;
+    } else {
+      const uint64_t eq = sm.eqm[qb];
+      const bool e = (eq >> l) & 1;
+      const int eq_rank = __popcll(eq & lt);
+      sel = on && (((sm.sel[qb] >> l) & 1) || (e && eq_rank < sm.info[qb].w) || l == 0 || l == qb);
+    }
+    const uint64_t bal = __ballot(sel);
+    if (sel) out[sm.rp[qb] + __popcll(bal & lt)] = l;
+  }
 }
 
 }  // namespace
@@ -1210,23 +1422,19 @@ hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, flo
   const int nb = d.nb;
   if (nb <= kPeSmall) {  // short layers: pooling, then the whole selection in one launch per head
     hipLaunchKernelGGL(sel_pool, dim3(nb, d.hq + d.hkv), dim3(256), 0, stream, a);
-    hipLaunchKernelGGL(sel_small, dim3(d.hq), dim3(1024), 0, stream, a);
+    hipLaunchKernelGGL(sel_small, dim3(d.hq), dim3(kSmallThreads), 0, stream, a);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(sel_route_vs, dim3(d.hq, 2), dim3(1024), 0, stream, a);
   hipLaunchKernelGGL(sel_pool, dim3(nb, d.hq + d.hkv), dim3(256), 0, stream, a);
-  if (nb <= kPeSmall) {  // logits and softmax of the whole triangle in one launch
-    hipLaunchKernelGGL(sel_pe_small, dim3(d.hq), dim3(256), 0, stream, a);
+  if (nb <= kLogitDirect) {
+    const int nt = (nb + 63) / 64;
+    hipLaunchKernelGGL(sel_pe_logits_direct, dim3(nt * (nt + 1) / 2, d.hq), dim3(256), 0, stream, a);
   } else {
-    if (nb <= kLogitDirect) {
-      const int nt = (nb + 63) / 64;
-      hipLaunchKernelGGL(sel_pe_logits_direct, dim3(nt * (nt + 1) / 2, d.hq), dim3(256), 0, stream, a);
-    } else {
-      const int nt = (nb + 127) / 128;
-      hipLaunchKernelGGL(sel_pe_logits<64>, dim3(nt * (nt + 1) / 2, d.hq), dim3(256), 0, stream, a);
-    }
-    hipLaunchKernelGGL(sel_pe_softmax, dim3(nb, d.hq), dim3(256), 0, stream, a);
+    const int nt = (nb + 127) / 128;
+    hipLaunchKernelGGL(sel_pe_logits<64>, dim3(nt * (nt + 1) / 2, d.hq), dim3(256), 0, stream, a);
   }
+  hipLaunchKernelGGL(sel_pe_softmax, dim3(nb, d.hq), dim3(256), 0, stream, a);
   if (d.cap <= kSmallCap) {
     hipLaunchKernelGGL(sel_radix_small, dim3(d.hq), dim3(1024), 0, stream, a);
   } else {
@@ -1239,14 +1447,10 @@ hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, flo
       hipLaunchKernelGGL(sel_radix_scan, dim3(d.hq), dim3(256), 0, stream, a, pass);
     }
   }
-  if (nb <= kCsrSmall) {
-    hipLaunchKernelGGL(sel_csr_small, dim3(d.hq), dim3(1024), 0, stream, a);
-  } else {
-    const int rows_grid = (nb + 3) / 4;
-    hipLaunchKernelGGL(sel_csr_count, dim3(rows_grid, d.hq), dim3(256), 0, stream, a);
-    hipLaunchKernelGGL(sel_csr_scan, dim3(d.hq), dim3(1024), 0, stream, a);
-    hipLaunchKernelGGL(sel_csr_fill, dim3(rows_grid, d.hq), dim3(256), 0, stream, a);
-  }
+  const int rows_grid = (nb + 3) / 4;
+  hipLaunchKernelGGL(sel_csr_count, dim3(rows_grid, d.hq), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(sel_csr_scan, dim3(d.hq), dim3(1024), 0, stream, a);
+  hipLaunchKernelGGL(sel_csr_fill, dim3(rows_grid, d.hq), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 
