@@ -439,14 +439,17 @@ crisp_status crisp_prefill_attn(const crisp_shape* shape, const crisp_params* pa
   int32_t* ci = given ? col_idx_or_null : (int32_t*)(ws + e.colidx);
   const float scale = scale_of(params->softmax_scale);
   hipStream_t st = (hipStream_t)stream;
-  CHECK(hip_status(launch_estimate(d, scale, params->w_sink, params->w_local, q, k, cs, pv, ps, ws, st),
-                   "crisp_prefill_attn estimate launch"));
   const bool by_jsd = params->route_mode == CRISP_ROUTE_BY_JSD;
+  // Short layers: the selection forms p_v and p_s itself from the estimator's sums (one
+  // launch fewer); the pattern search reads p_v, so it keeps the estimator's own step.
+  const bool fold = !by_jsd && d.nb <= kSmallSelectBlocks;
+  CHECK(hip_status(launch_estimate(d, scale, params->w_sink, params->w_local, q, k, cs, pv, ps, ws, st, fold),
+                   "crisp_prefill_attn estimate launch"));
   if (by_jsd)  // the route score slot then holds D_JS instead of C_struct
     CHECK(hip_status(launch_jsd(d, scale, q, k, pv, cs, ws, st), "crisp_prefill_attn pattern search launch"));
   CHECK(hip_status(launch_select(d, scale, params->alpha, route_tau(params), params->gamma, kmin_of(params, d.B),
                                  params->vs_mode, params->floor_mode, by_jsd, q, k, cs, pv, ps, route, rp, ci,
-                                 d.cap, nullptr, ws, st),
+                                 d.cap, nullptr, ws, st, fold),
                    "crisp_prefill_attn select launch"));
   return hip_status(launch_attn(d, scale, q, k, v, rp, ci, d.cap, false, o, ws + L.sched, st),
                     "crisp_prefill_attn attention launch");

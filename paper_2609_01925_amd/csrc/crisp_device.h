@@ -129,6 +129,31 @@ __device__ __forceinline__ int wave_sum_i(int x) {
   return x;
 }
 
+// The proxy's mass in key block J summed over the b proxy rows (the vertical and slash
+// scores of Alg. 3 before the 1/b): P holds one head's per-(block, row) pairs (lo, hi,
+// max m they were summed under, -), and lane l takes rows l and l + 64 (ok0 / ok1: the
+// row exists) with their normalisers mcl = M c + log2 L.  *slo and *shi get the sums of
+// lo and hi, each a fixed-order butterfly over the wave, scaled by 2^(m c - mcl).
+__device__ __forceinline__ void proxy_block_sums(const float4* P, int J, float c, float mcl0, float mcl1, bool ok0,
+                                                 bool ok1, float* slo, float* shi) {
+  const int l = __lane_id();
+  float lo0 = 0.f, hi0 = 0.f, lo1 = 0.f, hi1 = 0.f;
+  if (ok0) {
+    const float4 e = P[(size_t)J * 128 + l];
+    const float f = e.z == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(e.z * c - mcl0);
+    lo0 = e.x * f;
+    hi0 = e.y * f;
+  }
+  if (ok1) {
+    const float4 e = P[(size_t)J * 128 + l + 64];
+    const float f = e.z == -__builtin_inff() ? 0.f : __builtin_amdgcn_exp2f(e.z * c - mcl1);
+    lo1 = e.x * f;
+    hi1 = e.y * f;
+  }
+  *slo = wave_sum(lo0 + lo1);
+  *shi = wave_sum(hi0 + hi1);
+}
+
 #if defined(__HIP_DEVICE_COMPILE__)
 
 // Tile fetch: a 64-key x 128-dim tile goes straight from global memory into an

@@ -49,17 +49,24 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
                        const int32_t* row_ptr, const int32_t* col_idx, int64_t col_cap, bool dense,
                        uint16_t* o, void* sched, hipStream_t stream, int max_slots = kWorkspaceSlots);
 
+// combine_only: C_struct and the per-row normalisers only; p_v and p_s stay unwritten
+// (launch_select with scores_from_ws forms them from the workspace instead).
 hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, const uint16_t* q,
                            const uint16_t* k, float* c_struct, float* p_v, float* p_s, char* ws,
-                           hipStream_t stream);
+                           hipStream_t stream, bool combine_only = false);
+
+// Layers of at most this many blocks take the one-launch-per-head selection.
+constexpr int kSmallSelectBlocks = 64;
 
 // route_score is C_struct (tau = tau_proxy) or D_JS (tau = tau_jsd); vs_mode 0 is the
 // noise floor (floor_mode 0: mean, 1: median), 1 gamma coverage; kbar_all: K_bar of
-// every KV group is already in ws.
+// every KV group is already in ws.  scores_from_ws (layers of at most kSmallSelectBlocks
+// blocks, after launch_estimate with combine_only on the same ws): p_v and p_s are not
+// read; the selection forms them from the estimator's sums in ws.
 hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, float gamma, int k_min, int vs_mode,
                          int floor_mode, bool kbar_all, const uint16_t* q, const uint16_t* k, const float* route_score,
                          const float* p_v, const float* p_s, int8_t* route, int32_t* row_ptr, int32_t* col_idx,
-                         int64_t col_cap, uint8_t* dir_mask, char* ws, hipStream_t stream);
+                         int64_t col_cap, uint8_t* dir_mask, char* ws, hipStream_t stream, bool scores_from_ws = false);
 
 // route = dense and full causal CSR lists (col_cap >= nb (nb + 1) / 2).
 hipError_t launch_dense_lists(const Dims& d, int8_t* route, int32_t* row_ptr, int32_t* col_idx, int64_t col_cap,

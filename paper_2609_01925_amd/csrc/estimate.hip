@@ -298,27 +298,15 @@ __device__ __forceinline__ void scale_run(const EstArgs& a, int h, int Ja, int J
   const float mcl0 = ok0 ? a.rowfinal[(size_t)h * 128 + l] : 0.f;
   const float mcl1 = ok1 ? a.rowfinal[(size_t)h * 128 + l + 64] : 0.f;
   const float4* P = a.parts + (size_t)h * a.nb * 128;
-  auto row = [&](int J, int rr, float mcl, bool ok, float& lo, float& hi) {
-    lo = hi = 0.f;
-    if (!ok) return;
-    const float4 e = P[(size_t)J * 128 + rr];
-    const float f = e.z == -__builtin_inff() ? 0.f : fast_exp2(e.z * a.c - mcl);
-    lo = e.x * f;
-    hi = e.y * f;
-  };
   float prev_hi = 0.f;
   if (Ja > 0) {
-    float lo0, hi0, lo1, hi1;
-    row(Ja - 1, l, mcl0, ok0, lo0, hi0);
-    row(Ja - 1, l + 64, mcl1, ok1, lo1, hi1);
-    prev_hi = wave_sum(hi0 + hi1);
+    float slo;
+    proxy_block_sums(P, Ja - 1, a.c, mcl0, mcl1, ok0, ok1, &slo, &prev_hi);
   }
   const float invb = 1.f / (float)a.b;
   for (int J = Ja; J < Jb; ++J) {
-    float lo0, hi0, lo1, hi1;
-    row(J, l, mcl0, ok0, lo0, hi0);
-    row(J, l + 64, mcl1, ok1, lo1, hi1);
-    const float slo = wave_sum(lo0 + lo1), shi = wave_sum(hi0 + hi1);
+    float slo, shi;
+    proxy_block_sums(P, J, a.c, mcl0, mcl1, ok0, ok1, &slo, &shi);
     if (l == 0) {
       a.p_v[(size_t)h * a.nb + J] = (slo + shi) * invb;
       a.p_s[(size_t)h * a.nb + J] = (slo + prev_hi) * invb;
@@ -370,7 +358,7 @@ EstSplit est_split(const Dims& d) {
 
 hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, const uint16_t* q,
                            const uint16_t* k, float* c_struct, float* p_v, float* p_s, char* ws,
-                           hipStream_t stream) {
+                           hipStream_t stream, bool combine_only) {
   if (d.n == 0 || d.hq == 0) return hipSuccess;
   const WsLayout L = ws_layout(d);
   const EstSplit sp = est_split(d);
@@ -387,7 +375,9 @@ hipError_t launch_estimate(const Dims& d, float scale, int w_sink, int w_local, 
   const int pairs = d.hkv * sp.splits;  // (KV group, key range) pairs, spread over the XCDs
   const int grid = kNumXcd * d.G * ((pairs + kNumXcd - 1) / kNumXcd);
   hipLaunchKernelGGL(est_pass, dim3(grid), dim3(NT), 0, stream, a);
-  if (d.nb <= kFinishSmall) {
+  if (combine_only) {  // p_v and p_s are left to the caller's next launch (from parts and rowfinal)
+    hipLaunchKernelGGL(est_combine, dim3(d.hq), dim3(1024), 0, stream, a);
+  } else if (d.nb <= kFinishSmall) {
     hipLaunchKernelGGL(est_finish, dim3(d.hq), dim3(1024), 0, stream, a);
   } else {
     hipLaunchKernelGGL(est_combine, dim3(d.hq), dim3(1024), 0, stream, a);

@@ -66,6 +66,9 @@ struct SelArgs {
   unsigned long long* rhist;
   RState* rstate;
   int4* rowinfo;
+  const float4* parts;     // short layers from prefill: the estimator's per-(block, row) sums, else null
+  const float* rowfinal;   // their per-row normalisers
+  int b;                   // proxy rows
 };
 
 constexpr int kRadixBins = 2048;
@@ -670,7 +673,7 @@ __global__ __launch_bounds__(256) void sel_pe_logits(SelArgs a) {
 // products go back to LDS, and the row softmax (divided by N_b) adds the four runs of
 // each logit in run order.  The waves take the rows in turn, writing row qb at
 // At[qb (qb + 1) / 2 ..] (global memory or LDS).  buf holds 2 kPeSmall kHeadDim floats.
-constexpr int kPeSmall = 64, kPartPitch = 33;
+constexpr int kPeSmall = kSmallSelectBlocks, kPartPitch = 33;
 
 __device__ void pe_small_head(const SelArgs& a, int h, float* buf, float* At) {
   const int tid = threadIdx.x, nthr = blockDim.x, nwav = nthr >> 6;
@@ -1181,11 +1184,12 @@ __device__ __forceinline__ bool wave_top_k(uint32_t b, bool in, int kd) {
   return in && (b > t || (eq && rank < kd - ngt));
 }
 
-// Direction dir's block set of a VS head with nb > 2 blocks (route_vs_dir), lane = block.
-__device__ bool small_vs_dir(const SelArgs& a, int h, int dir) {
+// The block set of one direction of a VS head with nb > 2 blocks (route_vs_dir), lane =
+// block; P: the direction's scores (p_v or p_s) of the head.
+__device__ bool small_vs_dir(const SelArgs& a, const float* P) {
   const int l = lane_id(), nb = a.nb;
   const bool in = l < nb;
-  const float p = in ? (dir == 0 ? a.p_v : a.p_s)[(size_t)h * nb + l] : 0.f;
+  const float p = in ? P[l] : 0.f;
   const uint32_t b = in ? fbits(p) : 0u;
   if (a.vs_mode == 1) {
     const unsigned long long need = (unsigned long long)ceil((double)a.gamma * kFix);
@@ -1242,6 +1246,8 @@ struct SmallShared {
   int rp[kPeSmall];
   uint64_t dmask[2];
   RState st;
+  float bsum[2][kPeSmall];  // per block: the proxy's lo and hi mass summed over rows
+  float pvs[2][kPeSmall];   // p_v and p_s of the head
 };
 
 __global__ __launch_bounds__(kSmallThreads) void sel_small(SelArgs a) {
@@ -1250,8 +1256,34 @@ __global__ __launch_bounds__(kSmallThreads) void sel_small(SelArgs a) {
   const int nb = a.nb;
   const bool vs = a.c_struct[h] >= a.tau;
   if (tid == 0) a.route[h] = vs ? 0 : 1;
+  const float* pdir[2] = {a.p_v + (size_t)h * nb, a.p_s + (size_t)h * nb};
+  if (vs && a.parts) {
+    // p_v and p_s from the estimator's sums, as its scale step forms them: p_v[J] = (lo[J] +
+    // hi[J]) / b, p_s[J] = (lo[J] + hi[J - 1]) / b, every sum in the same order
+    const bool ok0 = l < a.b, ok1 = l + 64 < a.b;
+    const float mcl0 = ok0 ? a.rowfinal[(size_t)h * 128 + l] : 0.f;
+    const float mcl1 = ok1 ? a.rowfinal[(size_t)h * 128 + l + 64] : 0.f;
+    const float4* P = a.parts + (size_t)h * nb * 128;
+    for (int J = w; J < nb; J += kSmallThreads / 64) {
+      float slo, shi;
+      proxy_block_sums(P, J, a.c2, mcl0, mcl1, ok0, ok1, &slo, &shi);
+      if (l == 0) {
+        sm.bsum[0][J] = slo;
+        sm.bsum[1][J] = shi;
+      }
+    }
+    __syncthreads();
+    const float invb = 1.f / (float)a.b;
+    if (tid < nb) {
+      sm.pvs[0][tid] = (sm.bsum[0][tid] + sm.bsum[1][tid]) * invb;
+      sm.pvs[1][tid] = (sm.bsum[0][tid] + (tid > 0 ? sm.bsum[1][tid - 1] : 0.f)) * invb;
+    }
+    __syncthreads();
+    pdir[0] = sm.pvs[0];
+    pdir[1] = sm.pvs[1];
+  }
   if (w < 2) {  // wave w: direction w (no blocks on a PE head or with N_b <= 2)
-    const bool s = vs && nb > 2 && small_vs_dir(a, h, w);
+    const bool s = vs && nb > 2 && small_vs_dir(a, pdir[w]);
     const uint64_t bits = __ballot(s);
     if (l == 0) sm.dmask[w] = bits;
     if (a.dir_mask && l < nb) a.dir_mask[((size_t)h * 2 + w) * nb + l] = s;
@@ -1401,7 +1433,7 @@ hipError_t launch_jsd(const Dims& d, float scale, const uint16_t* q, const uint1
 hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, float gamma, int k_min, int vs_mode,
                          int floor_mode, bool kbar_all, const uint16_t* q, const uint16_t* k, const float* route_score,
                          const float* p_v, const float* p_s, int8_t* route, int32_t* row_ptr, int32_t* col_idx,
-                         int64_t col_cap, uint8_t* dir_mask, char* ws, hipStream_t stream) {
+                         int64_t col_cap, uint8_t* dir_mask, char* ws, hipStream_t stream, bool scores_from_ws) {
   if (d.n == 0 || d.hq == 0) return hipSuccess;
   const WsLayout L = ws_layout(d);
   SelArgs a;
@@ -1420,6 +1452,10 @@ hipError_t launch_select(const Dims& d, float scale, float alpha, float tau, flo
   a.rstate = reinterpret_cast<RState*>(ws + L.rstate);
   a.rowinfo = reinterpret_cast<int4*>(ws + L.rowinfo);
   const int nb = d.nb;
+  const bool from_ws = scores_from_ws && nb <= kPeSmall;
+  a.parts = from_ws ? reinterpret_cast<const float4*>(ws + L.parts) : nullptr;
+  a.rowfinal = from_ws ? reinterpret_cast<const float*>(ws + L.rowfinal) : nullptr;
+  a.b = d.b;
   if (nb <= kPeSmall) {  // short layers: pooling, then the whole selection in one launch per head
     hipLaunchKernelGGL(sel_pool, dim3(nb, d.hq + d.hkv), dim3(256), 0, stream, a);
     hipLaunchKernelGGL(sel_small, dim3(d.hq), dim3(kSmallThreads), 0, stream, a);

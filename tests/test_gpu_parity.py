@@ -805,21 +805,35 @@ def test_flexprefill_prefill_matches_stagewise():
     assert torch.equal(o1, o2)
 
 
-def test_prefill_lists_match_stagewise():
-    """crisp_prefill_attn with caller lists reproduces the stage-by-stage calls exactly."""
+def _stagewise_cases():
+    # (name, layer, parameters); up to 64 blocks prefill's selection forms p_v and p_s from
+    # the estimator's sums itself, past that it reads the estimator's own p_v and p_s
+    return [("5000 4/1", lambda: custom_config(5000, 4, 1, block=128, config_id=140), {}),
+            ("pe8k 32/8 nb64", lambda: structured_pe_config(8192), {}),
+            ("4000 8/2 B64 median kmin3", lambda: custom_config(4000, 8, 2, block=64, config_id=142),
+             dict(floor_mode=1, k_min_blocks=3)),
+            ("3000 6/3 gamma VS", lambda: custom_config(3000, 6, 3, block=128, config_id=143), dict(vs_mode=1)),
+            ("8320 4/2 nb65", lambda: custom_config(8320, 4, 2, block=128, config_id=144), {})]
+
+
+@pytest.mark.parametrize("name,make_cfg,kw", _stagewise_cases(), ids=[c[0] for c in _stagewise_cases()])
+def test_prefill_lists_match_stagewise(name, make_cfg, kw):
+    """crisp_prefill_attn with caller lists reproduces the stage-by-stage calls exactly, on
+    either side of the short-layer selection's 64 blocks."""
     C = _crisp()
-    _say("prefill lists == stages")
-    cfg = custom_config(5000, 4, 1, block=128, config_id=140)
+    _say(f"prefill lists == stages: {name}")
+    cfg = make_cfg()
+    block = cfg.block
     q, k, v, _ = make_layer(cfg, device=DEV)
-    params = C.make_params()
-    cs, pv, ps, route, rp, ci, _ = _run_stages(C, q, k, v, params, 128)
-    o1, r2, rp2, ci2 = C.crisp_prefill_attn(q, k, v, params, 128, return_lists=True)
-    o2 = C.crisp_sparse_attn(q, k, v, torch.from_numpy(rp).to(DEV), torch.from_numpy(ci).to(DEV), 128)
-    o3 = C.crisp_prefill_attn(q, k, v, params, 128)
+    params = C.make_params(**kw)
+    cs, pv, ps, route, rp, ci, _ = _run_stages(C, q, k, v, params, block)
+    o1, r2, rp2, ci2 = C.crisp_prefill_attn(q, k, v, params, block, return_lists=True)
+    o2 = C.crisp_sparse_attn(q, k, v, torch.from_numpy(rp).to(DEV), torch.from_numpy(ci).to(DEV), block)
+    o3 = C.crisp_prefill_attn(q, k, v, params, block)
     torch.cuda.synchronize()
     assert np.array_equal(r2.cpu().numpy(), route) and np.array_equal(rp2.cpu().numpy(), rp)
-    nb = O.n_blocks(cfg.seq_len, 128)
-    for h in range(4):
+    nb = O.n_blocks(cfg.seq_len, block)
+    for h in range(cfg.n_q_heads):
         assert PR.csr_to_sets(rp2.cpu().numpy(), ci2.cpu().numpy(), h, nb) == PR.csr_to_sets(rp, ci, h, nb)
     assert torch.equal(o1, o2) and torch.equal(o1, o3)
 
