@@ -1149,19 +1149,20 @@ __global__ __launch_bounds__(256) void sel_csr_fill(SelArgs a) {
 // offsets), so no phase waits on a round trip through global memory.  With at most 64
 // blocks a VS direction fits one wave, one block per lane, and both directions run at
 // once on waves 0 and 1.  Their decisions are those of route_vs_dir, reached with
-// ballots and shuffles instead of histogram passes: the k-th largest bit pattern is
+// ballots and lane reads instead of histogram passes: the k-th largest bit pattern is
 // found bit by bit from the top as the largest t with #{b >= t} >= k, and the gamma cut
-// as the largest t whose mass at or above t (the same 2^-60 fixed-point integers)
-// reaches gamma -- the values the digit passes settle on, since both counts only fall
-// as t grows.  The PE scores, softmax and cutoff are pe_small_head and
+// as the largest block value t whose mass at or above t (the same 2^-60 fixed-point
+// integers) reaches gamma -- the values the digit passes settle on, since both counts
+// only fall as t grows.  The PE scores, softmax and cutoff are pe_small_head and
 // radix_small_head on LDS, and the lists follow the rules of csr_count_row,
 // csr_scan_head and csr_fill_row, one wave per row.  grid hq, kSmallThreads threads.
 constexpr int kSmallThreads = 1024;
 
-__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
-  return x;
+// Lane j's value of x (j uniform).
+__device__ __forceinline__ unsigned long long readlane_u64(unsigned long long x, int j) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, j);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), j);
+  return ((unsigned long long)hi << 32) | lo;
 }
 
 // k-th largest (k >= 1) of the bit patterns b of the lanes with `in` set (k of them at least).
@@ -1194,16 +1195,32 @@ __device__ bool small_vs_dir(const SelArgs& a, const float* P) {
   if (a.vs_mode == 1) {
     const unsigned long long need = (unsigned long long)ceil((double)a.gamma * kFix);
     const unsigned long long m = in ? fixed_mass(b) : 0ull;
+    // the mass at or above each lane's own value, summed over the blocks in lane order
+    unsigned long long ge = 0ull, total = 0ull;
+    for (int j = 0; j < nb; ++j) {
+      const uint32_t bj = (uint32_t)__builtin_amdgcn_readlane((int)b, j);
+      const unsigned long long mj = readlane_u64(m, j);
+      total += mj;
+      ge += bj >= b ? mj : 0ull;
+    }
     int c = nb, ceq = 0;
     uint32_t t = 0;
-    const bool all = wave_sum_u64(m) < need;  // the total mass never reaches gamma
+    const bool all = total < need;  // the total mass never reaches gamma
     if (!all) {
-      for (int bit = 31; bit >= 0; --bit) {
-        const uint32_t x = t | (1u << bit);
-        if (wave_sum_u64(b >= x ? m : 0ull) >= need) t = x;
+      // mass(>= x) only falls as x grows, and t* carries mass, so t* is the largest
+      // block value whose mass at or above it reaches need
+      uint32_t cand = in && ge >= need ? b : 0u;
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) {
+        const uint32_t y = __shfl_xor(cand, o, 64);
+        cand = y > cand ? y : cand;
       }
-      const unsigned long long rest = need - wave_sum_u64(b > t ? m : 0ull);
+      t = cand;
+      const uint64_t eqm = __ballot(in && b == t);
+      const int first = __builtin_ctzll(eqm);
+      const unsigned long long ge_t = readlane_u64(ge, first);
       const unsigned long long mt = fixed_mass(t);  // > 0: t carries mass
+      const unsigned long long rest = need - (ge_t - (unsigned long long)__popcll(eqm) * mt);
       ceq = (int)((rest + mt - 1) / mt);
       c = __popcll(__ballot(in && b > t)) + ceq;
     }
