@@ -84,10 +84,10 @@ __device__ __forceinline__ int key_of(int key0, int mb, int i, int l) {
 // block ends).  K tiles go straight from global memory into a two-stage LDS ring
 // (LDS-DMA; keys at or past n read as 0), the next tile's load issued as the current
 // one is scored.  The running max is raised lazily: a tile's terms are formed against
-// the current max, and only when some lane's tile sum exceeds 2^8 (or is not finite,
-// or the row has no max yet) is the tile's true row max taken, the open sums scaled
-// down to it and the terms formed again -- until then every term is at most 2^8, which
-// float32 holds as exactly as terms below 1.  A block's (lo, hi) is written with the
+// the current max, and only when some lane's tile sum exceeds 2^8 (or is not finite)
+// is the tile's true row max taken, the open sums scaled down to it and the terms
+// formed again -- until then every term is at most 2^8, which float32 holds as exactly
+// as terms below 1; while a row of the wave has no max yet, the max is taken first.  A block's (lo, hi) is written with the
 // max it was summed under when the block ends, and the range's (max, l, anchor) when
 // the range ends.
 __global__ __launch_bounds__(NT, 4) void est_pass(EstArgs a) {
@@ -170,8 +170,13 @@ __global__ __launch_bounds__(NT, 4) void est_pass(EstArgs a) {
           if (key < a.w_sink || key >= a.n - a.w_local) tanc += p;
         }
     };
+    // A wave with a row that has no running max yet (its first tiles) goes straight to
+    // the raise below: terms formed against no max would only be dropped there.
+    const bool fresh = __ballot(row_ok && m_run == -__builtin_inff()) != 0;
     const float mc0 = m_run == -__builtin_inff() ? 0.f : m_run * a.c;
-    if (plain && (all_lo || all_hi)) {
+    if (fresh) {
+      // the raise forms this tile's terms
+    } else if (plain && (all_lo || all_hi)) {
       float t0 = 0.f, t1 = 0.f;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
@@ -205,7 +210,7 @@ __global__ __launch_bounds__(NT, 4) void est_pass(EstArgs a) {
       general(mc0);
     }
     const float tsum = tlo + thi;
-    if (__ballot(row_ok && (!(tsum <= kSumLimit) || m_run == -__builtin_inff()))) {
+    if (fresh || __ballot(row_ok && !(tsum <= kSumLimit))) {
       float mx = vmax(s[0][0], s[1][0]);
 #pragma unroll
       for (int i = 1; i < 16; ++i) mx = vmax(mx, vmax(s[0][i], s[1][i]));
