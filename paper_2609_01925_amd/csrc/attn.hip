@@ -873,40 +873,61 @@ __global__ __launch_bounds__(1024) void attn_schedule(AttnArgs a) {
 // Merges the chunks of each split row in chunk order:
 //   O = sum_c w_c O_c / sum_c w_c l_c,  w_c = 2^((m_c - M) c),  M = max_c m_c
 // (chunks whose keys are all masked have m_c = -inf and weigh nothing).  grid
-// slots / 2 (workgroups past the number of split rows exit), 256 threads: BQ
-// query rows x 256 / BQ lanes, each lane 128 * BQ / 256 dims.
+// slots / 2 (workgroups past the number of split rows exit), kCombineThreads threads:
+// BQ query rows x kCombineThreads / BQ lanes, each lane 128 BQ / kCombineThreads dims.
+// The chunks' row statistics and partial rows are loaded kCombineBatch chunks at a
+// time (one memory latency per batch, not per chunk) and summed in chunk order.
+constexpr int kCombineThreads = 1024, kCombineBatch = 4;
 template <int BQ>
-__global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
+__global__ __launch_bounds__(kCombineThreads) void attn_combine(AttnArgs a) {
   const int i = blockIdx.x;
   if (i >= a.counter[18]) return;
   const int C = a.counter[17];
   const int u = a.split_rows[i];
   const int head = u / a.nb, qb = u % a.nb;
   const int k = (row_len(a, head, qb) + C - 1) / C;
-  constexpr int TPR = 256 / BQ, DPT = kHeadDim / TPR;
+  constexpr int TPR = kCombineThreads / BQ, DPT = kHeadDim / TPR, NB = kCombineBatch;
   constexpr size_t kSlotFloats = (size_t)BQ * (kHeadDim + 2);
   const int r = threadIdx.x / TPR, d0 = (threadIdx.x % TPR) * DPT;
   const float* base = a.parts + (size_t)a.slot_base[u] * kSlotFloats;
   float M = -__builtin_inff();
-  for (int c = 0; c < k; ++c) M = fmaxf(M, base[c * kSlotFloats + BQ * kHeadDim + r]);
+  for (int c0 = 0; c0 < k; c0 += NB) {
+    float mv[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      mv[j] = c0 + j < k ? base[(c0 + j) * kSlotFloats + BQ * kHeadDim + r] : -__builtin_inff();
+#pragma unroll
+    for (int j = 0; j < NB; ++j) M = fmaxf(M, mv[j]);
+  }
   float acc[DPT];
 #pragma unroll
   for (int e = 0; e < DPT; ++e) acc[e] = 0.f;
   float lsum = 0.f;
-  for (int c = 0; c < k; ++c) {
-    const float* sl = base + c * kSlotFloats;
-    const float m = sl[BQ * kHeadDim + r];
-    if (m == -__builtin_inff()) continue;
-    const float w = fast_exp2((m - M) * a.c);
-    lsum += w * sl[BQ * kHeadDim + BQ + r];
-    const float4* po = reinterpret_cast<const float4*>(sl + (size_t)r * kHeadDim + d0);
+  for (int c0 = 0; c0 < k; c0 += NB) {
+    float mv[NB], lv[NB];
+    float4 pv[NB][DPT / 4];
 #pragma unroll
-    for (int e = 0; e < DPT / 4; ++e) {
-      const float4 v = po[e];
-      acc[4 * e] += w * v.x;
-      acc[4 * e + 1] += w * v.y;
-      acc[4 * e + 2] += w * v.z;
-      acc[4 * e + 3] += w * v.w;
+    for (int j = 0; j < NB; ++j) {
+      const bool in = c0 + j < k;
+      const float* sl = base + (size_t)(in ? c0 + j : 0) * kSlotFloats;
+      mv[j] = in ? sl[BQ * kHeadDim + r] : -__builtin_inff();
+      lv[j] = in ? sl[BQ * kHeadDim + BQ + r] : 0.f;
+      const float4* po = reinterpret_cast<const float4*>(sl + (size_t)r * kHeadDim + d0);
+#pragma unroll
+      for (int e = 0; e < DPT / 4; ++e) pv[j][e] = in ? po[e] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      if (mv[j] == -__builtin_inff()) continue;  // also every slot past the last chunk
+      const float w = fast_exp2((mv[j] - M) * a.c);
+      lsum += w * lv[j];
+#pragma unroll
+      for (int e = 0; e < DPT / 4; ++e) {
+        acc[4 * e] += w * pv[j][e].x;
+        acc[4 * e + 1] += w * pv[j][e].y;
+        acc[4 * e + 2] += w * pv[j][e].z;
+        acc[4 * e + 3] += w * pv[j][e].w;
+      }
     }
   }
   const int q = qb * BQ + r;
@@ -1057,9 +1078,9 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
     e = launch_t<64, false>(a, grid, stream);  // dense 64-row layers run as 128-row ones (above)
   if (e != hipSuccess || a.split_slots == 0) return e;
   if (d.B == 128)
-    hipLaunchKernelGGL(attn_combine<128>, dim3(a.split_slots / 2), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(attn_combine<128>, dim3(a.split_slots / 2), dim3(kCombineThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL(attn_combine<64>, dim3(a.split_slots / 2), dim3(256), 0, stream, a);
+    hipLaunchKernelGGL(attn_combine<64>, dim3(a.split_slots / 2), dim3(kCombineThreads), 0, stream, a);
   return hipGetLastError();
 }
 
