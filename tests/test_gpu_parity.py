@@ -163,17 +163,18 @@ def _csr_from_rows(rows, nb):
 def test_split_rows(case):
     """Rows far longer than the layer's work per workgroup are split into chunks whose
     partial results are merged (online-softmax merge of (O, m, l) in chunk order).  Few heads
-    with full causal lists force it; the merged rows match the oracle, runs are bitwise
-    repeatable, and the split rows round differently from the unsplit fixed-order launch
-    (which shows the split path ran).  junk-first-chunk: a row's first chunk holds only
-    invalid entries (m = -inf, weighing nothing in the merge)."""
+    with full causal lists force it (on the persistent grid, above 8192 tokens); the merged
+    rows match the oracle, runs are bitwise repeatable, and the split rows round differently
+    from the unsplit fixed-order launch (which shows the split path ran).  junk-first-chunk:
+    a row's first chunk holds only invalid entries (m = -inf, weighing nothing in the
+    merge)."""
     C = _crisp()
     _say(f"split rows {case}")
     if case == "junk-first-chunk":
         # rows from N_b / 2 on: even ones [-5] * 60 + [0, qb] (first chunk all invalid, then
         # merged with weight exactly 1), odd ones ten valid blocks at each end around 40
-        # invalid entries (both chunks count)
-        n, block, hq = 8192, 128, 1
+        # invalid entries (both chunks count; 32 entries per chunk)
+        n, block, hq = 16384, 128, 1
         nb = n // block
         rows, sets = [], []
         for qb in range(nb):
@@ -188,7 +189,7 @@ def test_split_rows(case):
         rp, ci = _csr_from_rows(rows, nb)
         long_rows = [qb for qb in range(nb // 2, nb) if qb % 2]
     else:
-        n, block, hq = (16384, 128, 1) if case == "full-b128" else (8000, 64, 2)
+        n, block, hq = (16384, 128, 1) if case == "full-b128" else (16000, 64, 2)
         nb = O.n_blocks(n, block)
         sets = O.dense_causal_sets(nb)
         rp = np.zeros((hq, nb + 1), np.int32)
@@ -1019,24 +1020,30 @@ def test_golden_manifests_on_gpu():
         del q, k, v, o
 
 
-@pytest.mark.parametrize("layer", ["config0", "ragged-b64", "pe-8k-split-rows", "one-shot-512k"])
+@pytest.mark.parametrize("layer", ["config0", "ragged-b64", "pe-8k", "16k-split-rows", "one-shot-512k"])
 def test_debug_build_race_check(layer):
     """The debug build's attention runs the same arithmetic with its tile pipeline
     serialised (each tile load waited for, a barrier after every LDS phase): its outputs
     equal the pipelined kernel's bit for bit, so the overlapped loads and reads of the
-    LDS rings never race.  Layers: the 4k tiny layer, a ragged B = 64 layer, an 8k
-    layer whose long rows are split (persistent grid, partial results merged), and a
-    512k layer (one unit per workgroup)."""
+    LDS rings never race.  Layers: the 4k tiny layer, a ragged B = 64 layer, the 8k
+    structured layer (one unit per workgroup from one list), a 16k two-head layer whose
+    long PE rows are split (persistent grid, partial results merged: checked against the
+    unsplit fixed-order launch), and a 512k layer (one unit per workgroup)."""
     C = _crisp()
     _say(f"debug race check {layer}")
     cfg, block = {"config0": (CONFIGS[0], 128), "ragged-b64": (custom_config(3001, 4, 2, block=64, config_id=154), 64),
-                  "pe-8k-split-rows": (structured_pe_config(8192), 128),
+                  "pe-8k": (structured_pe_config(8192), 128),
+                  "16k-split-rows": (custom_config(16384, 2, 1, block=128, config_id=156, tiny=True), 128),
                   "one-shot-512k": (custom_config(1 << 19, 2, 1, block=128, config_id=155), 128)}[layer]
     q, k, v, _ = make_layer(cfg, device=DEV)
     params = C.make_params(alpha=cfg.alpha)
     release = C.lib
     o_rel, _, rp, ci = C.crisp_prefill_attn(q, k, v, params, block, return_lists=True)
     d_rel = C.crisp_dense_attn(q, k, v, block)
+    if layer == "16k-split-rows":
+        o_fixed = C.crisp_sparse_attn(q, k, v, rp, ci, block, balance=False)
+        torch.cuda.synchronize()
+        assert not torch.equal(o_rel, o_fixed), "no row was split"
     torch.cuda.synchronize()
     try:
         C.lib = C._load(C.DEBUG_LIB_PATH)

@@ -39,17 +39,27 @@ def _agree(a, b, where):
 
 def test_no_alloc_matches_workspace_entry_point_twice():
     from paper_2609_01925_amd import crisp as C
-    # first call: an 8k layer whose long PE rows are split (persistent grid, partial slots)
-    big = structured_pe_config(8192)
+    # first call: a 16k two-head layer whose long PE rows the workspace entry point splits
+    # (persistent grid, partial slots; the area's fewer slots split fewer rows)
+    big = custom_config(16384, 2, 1, block=128, config_id=156, tiny=True)
     _say(f"no-alloc sparse attention, first call: {big.name}")
     q, k, v, rp, ci = _layer(C, big)
     o_ws = C.crisp_sparse_attn(q, k, v, rp, ci, big.block)
     o_na = C.crisp_sparse_attn_noalloc(q, k, v, rp, ci, big.block)
-    _agree(o_na, o_ws, "8k layer")
+    _agree(o_na, o_ws, "16k layer")
     del q, k, v, rp, ci
-    # second call, smaller: ragged B = 64 layer
+    # the 8k structured layer: one unit per workgroup from one list in both, bit for bit
+    mid = structured_pe_config(8192)
+    _say(f"no-alloc sparse attention, second call: {mid.name}")
+    q, k, v, rp, ci = _layer(C, mid)
+    o_ws = C.crisp_sparse_attn(q, k, v, rp, ci, mid.block)
+    o_na = C.crisp_sparse_attn_noalloc(q, k, v, rp, ci, mid.block)
+    torch.cuda.synchronize()
+    assert torch.equal(o_na, o_ws)
+    del q, k, v, rp, ci
+    # third call, smaller: ragged B = 64 layer
     small = custom_config(3001, 4, 2, block=64, config_id=154)
-    _say(f"no-alloc sparse attention, second call: {small.name}")
+    _say(f"no-alloc sparse attention, third call: {small.name}")
     q, k, v, rp, ci = _layer(C, small)
     o_ws = C.crisp_sparse_attn(q, k, v, rp, ci, small.block)
     o_na = C.crisp_sparse_attn_noalloc(q, k, v, rp, ci, small.block)
