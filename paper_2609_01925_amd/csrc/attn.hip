@@ -29,7 +29,7 @@
 //
 // Sparse lists are processed longest first from work lists that attn_schedule
 // builds from the list lengths, so long PE rows start first and short VS rows
-// fill the tail.  Above 8192 and below 512k tokens a persistent grid pulls units from one list
+// fill the tail.  Below 512k tokens a persistent grid pulls units from one list
 // per KV group, and the K/V tiles of a group stay in the caches of the XCDs that
 // serve it; rows much longer than the layer's work per workgroup are split into
 // chunks whose partial results attn_combine merges.  From 512k tokens on, rows
@@ -39,13 +39,15 @@
 // no longer meet in L2: there the grid has one workgroup per unit, and every
 // workgroup takes the next unit of the group lists in order (one KV group after
 // the other, longest first within a group), so units that start together
-// advance together over the same group's K/V.  Up to 8192 tokens (a few short units
-// per workgroup of a persistent grid, K/V of the whole layer within the caches) the
-// grid also has one workgroup per unit, workgroup i taking item i of one longest-first
-// list of all units without atomics: the dispatcher starts the workgroups in order, so
-// the longest units start first and later ones fill the CUs as they free up, with no
-// loop, queue or split rows around each unit (2k-4k layers 11-12% faster than the
-// persistent grid with split rows, 8k a little faster, 16k 14% slower).
+// advance together over the same group's K/V.  Up to 8192 tokens (K/V of the whole
+// layer within the caches) the units come from one longest-first list of all units
+// without atomics; when there are at least as many units as a persistent grid has
+// workgroups, the grid has one workgroup per unit, workgroup i taking item i: the
+// dispatcher starts the workgroups in order, so the longest units start first and later
+// ones fill the CUs as they free up, with no loop, queue or split rows around each unit
+// (2k-4k layers of 32 heads 11-12% faster than the persistent grid with split rows, 8k
+// 3-10% faster, 16k 14% slower).  With fewer units (few heads) the persistent grid takes
+// items i, i + grid, ... of that list and splits long rows.
 #include <atomic>
 #include <type_traits>
 
@@ -84,7 +86,7 @@ struct AttnArgs {
   const int32_t* order;  // persistent mode: units sorted longest first
   int* counter;          // persistent mode: next position in `order`
   int one_shot;          // 1: one unit per workgroup, all units in one queue
-  int static_list;       // 1: all units in queue 0, workgroup i takes item i (one per workgroup)
+  int static_list;       // 1: all units in queue 0, workgroup i takes items i, i + grid, ...
   int* slot_base;        // split rows: first partial slot of the row's chunks, else -1
   int* split_rows;       // the split rows (any order)
   float* parts;          // partial results per slot: O[BQ][128], m[BQ], l[BQ] (fp32)
@@ -626,12 +628,17 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
   // A queue whose counter already reads past its end is skipped without an atomic
   // (a stale read only costs an extra atomic: counters never decrease).
   unsigned dry = 0u;
+  int spos = blockIdx.x;  // static list: the next item of this workgroup
   for (;;) {
     __syncthreads();  // the previous unit is done with LDS and the unit slot
     if (a.static_list) {
-      // Short layers, one unit per workgroup: item blockIdx.x of one longest-first list,
-      // no atomic (the workgroups start in index order).  Every wave computes the same item.
-      const int item = (int)blockIdx.x < start[1] - start[0] ? a.order[start[0] + blockIdx.x] : -1;
+      // Short layers: items i, i + grid, ... of one longest-first list, no atomic (with one
+      // unit per workgroup, item i alone; the workgroups start in index order).  On a
+      // persistent grid the pop's atomic and the wait for it cost about as much as a unit's
+      // tiles, and a fixed stride balances as well (each round of grid items is no longer
+      // than the previous one).  Every wave computes the same item.
+      const int item = spos < start[1] - start[0] ? a.order[start[0] + spos] : -1;
+      spos += gridDim.x;
       if (tid == 0) *s_unit = item;
     } else if (tid == 0) {
       int unit = -1;
@@ -678,14 +685,13 @@ __global__ __launch_bounds__(Geo<BQ>::kThreads, Geo<BQ>::kWavesPerEU) void attn_
 // for them (separate queues let the XCDs of a group drift apart over a long
 // layer, and each then streams K/V from HBM on its own).  Within an XCD the
 // group's heads share its L2.  One-unit-per-workgroup mode empties the slots in
-// order; static-list mode (short layers, also one unit per workgroup) puts every unit
-// in slot 0.  Items are
+// order; static-list mode (short layers) puts every unit in slot 0.  Items are
 // ordered longest first within a queue (a counting sort of list lengths: exact up to
 // 768 entries, then in steps of 16).
 //
 // Split rows (persistent mode): a workgroup runs a row's tiles one after the
 // other, so when the longest row holds more entries than the layer's work per
-// workgroup (few heads), that row alone would set the kernel's
+// workgroup (short layers, few heads), that row alone would set the kernel's
 // time.  With G' = min(grid, slots / 2) and T the total of all rows' entries,
 // rows longer than C = max(ceil(T / G'), 8, ceil(N_b / 1024)) are cut into
 // ceil(L / C) chunks, each a work item of its own that leaves a partial result
@@ -981,7 +987,7 @@ struct SchedLayout {
 SchedLayout sched_layout(const Dims& d, int max_slots) {
   SchedLayout s;
   const size_t units = (size_t)d.hq * d.nb;
-  const bool split = d.n < kOneShotMinLen && d.n > kStaticListMaxLen && units < ((size_t)1 << kItemUnitBits);
+  const bool split = d.n < kOneShotMinLen && units < ((size_t)1 << kItemUnitBits);
   s.slots = split ? (int)(2 * units < (size_t)max_slots ? 2 * units : (size_t)max_slots) : 0;
   size_t off = (64 + units + (size_t)s.slots) * sizeof(int32_t);
   s.slot_base = off;
@@ -1057,15 +1063,17 @@ hipError_t launch_attn(const Dims& d, float scale, const uint16_t* q, const uint
     const SchedLayout sl = sched_layout(d, max_slots);
     a.counter = reinterpret_cast<int*>(sc);
     a.order = reinterpret_cast<const int32_t*>(sc) + 64;
-    a.one_shot = d.n >= kOneShotMinLen || d.n <= kStaticListMaxLen ? 1 : 0;
+    const int pg = d.B == 128 ? persistent_grid<128>() : persistent_grid<64>();
+    // short layers with at least a persistent grid's worth of units: one unit per workgroup
+    const bool short_one = d.n <= kStaticListMaxLen && (size_t)d.hq * d.nb >= (size_t)pg;
+    a.one_shot = d.n >= kOneShotMinLen || short_one ? 1 : 0;
     a.static_list = d.n <= kStaticListMaxLen ? 1 : 0;
-    a.split_slots = sl.slots;
-    if (sl.slots > 0) {
+    a.split_slots = short_one ? 0 : sl.slots;  // the slots stay reserved, unused
+    if (a.split_slots > 0) {
       a.slot_base = reinterpret_cast<int*>(sc + sl.slot_base);
       a.split_rows = reinterpret_cast<int*>(sc + sl.split_rows);
       a.parts = reinterpret_cast<float*>(sc + sl.parts);
     }
-    const int pg = d.B == 128 ? persistent_grid<128>() : persistent_grid<64>();
     grid = a.one_shot || pg > d.hq * d.nb ? d.hq * d.nb : pg;
     a.grid = grid;
     hipLaunchKernelGGL(attn_schedule, dim3(1), dim3(1024), 0, stream, a);

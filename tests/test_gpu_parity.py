@@ -159,12 +159,12 @@ def _csr_from_rows(rows, nb):
     return rp, ci
 
 
-@pytest.mark.parametrize("case", ["full-b128", "full-b64-ragged", "junk-first-chunk"])
+@pytest.mark.parametrize("case", ["full-b128", "full-b128-8k", "full-b64-ragged", "junk-first-chunk"])
 def test_split_rows(case):
     """Rows far longer than the layer's work per workgroup are split into chunks whose
     partial results are merged (online-softmax merge of (O, m, l) in chunk order).  Few heads
-    with full causal lists force it (on the persistent grid, above 8192 tokens); the merged
-    rows match the oracle, runs are bitwise repeatable, and the split rows round differently
+    with full causal lists force it (on the persistent grid); the merged rows match the
+    oracle, runs are bitwise repeatable, and the split rows round differently
     from the unsplit fixed-order launch (which shows the split path ran).  junk-first-chunk:
     a row's first chunk holds only invalid entries (m = -inf, weighing nothing in the
     merge)."""
@@ -189,7 +189,10 @@ def test_split_rows(case):
         rp, ci = _csr_from_rows(rows, nb)
         long_rows = [qb for qb in range(nb // 2, nb) if qb % 2]
     else:
-        n, block, hq = (16384, 128, 1) if case == "full-b128" else (16000, 64, 2)
+        # 8k: a short layer (units from one list in a fixed stride) with too few units for
+        # one workgroup each
+        n, block, hq = {"full-b128": (16384, 128, 1), "full-b128-8k": (8192, 128, 1),
+                        "full-b64-ragged": (16000, 64, 2)}[case]
         nb = O.n_blocks(n, block)
         sets = O.dense_causal_sets(nb)
         rp = np.zeros((hq, nb + 1), np.int32)
