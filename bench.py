@@ -55,6 +55,9 @@ def parse():
     ap.add_argument("--skip-comparators", action="store_true",
                     help="skip the FlexPrefill comparator, ablation and noise-floor variant timings")
     ap.add_argument("--config", type=int, default=2, help="headline config id (2 = 128k Llama GQA layer)")
+    ap.add_argument("--structured", type=int, default=0, metavar="N",
+                    help="headline layer: the structured-PE layer of N tokens (Llama-3-8B shape) instead of "
+                         "--config (for profiling the length sweep's layers)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain 1 GiB device copy, the reference for rocprofv3 byte counters")
     ap.add_argument("--summarize", metavar="ROCPROF_DIR",
@@ -826,7 +829,11 @@ def main():
     from workloads import CONFIGS
 
     assert torch.cuda.is_available(), "no GPU visible"
-    cfg = CONFIGS[args.config]
+    if args.structured:
+        from workloads import structured_pe_config
+        cfg = structured_pe_config(args.structured)
+    else:
+        cfg = CONFIGS[args.config]
     if args.copy_calibration:
         copy_calibration()
     peaks = None if args.skip_peaks else measured_peaks()
@@ -849,7 +856,7 @@ def main():
     for r_ in (res,):
         add_measured_fracs(r_, peaks)
     extra = {}
-    if not args.skip_512k and args.config != 3:
+    if not args.skip_512k and args.config != 3 and not args.structured:
         try:
             r3 = layer_measure(CONFIGS[3], args.steps_512k, 1, "512k")
             if not args.skip_comparators:
