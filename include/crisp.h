@@ -209,7 +209,9 @@ crisp_status crisp_sparse_workspace_size(const crisp_shape* shape, size_t* bytes
  * work list that balances rows of very different lengths over the GPU and, for
  * layers shorter than 512k tokens, slots for partial results: a row far longer
  * than the layer's work per workgroup is split into chunks whose softmax partials
- * are merged in chunk order.  Results are repeatable for given lists; a split row
+ * are merged in chunk order (up to 8192 tokens, a layer with at least as many
+ * (head, query block) units as the GPU holds workgroups at once runs one workgroup
+ * per unit and splits nothing).  Results are repeatable for given lists; a split row
  * differs from an unsplit one by floating-point rounding only.  With NULL the rows
  * are processed whole, in a fixed order. */
 crisp_status crisp_sparse_attn(const crisp_shape* shape, float softmax_scale,
