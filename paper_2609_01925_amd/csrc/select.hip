@@ -118,6 +118,41 @@ __device__ int block_sum_1024(int x, int* wtot) {
   return s;
 }
 
+// Inclusive prefix sum over the 64 lanes in lane order, on DPP lane moves: within each
+// row of 16 lanes by shifts of 1, 2, 4 and 8 (lanes shifted in from outside the row read
+// 0), then the last lane of rows 0 and 2 broadcast into rows 1 and 3, and lane 31 into
+// rows 2 and 3.  Integer sums, so the result is that of any other order.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROW_MASK, 0xf, true);
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ unsigned long long dpp_move(unsigned long long x) {
+  return ((unsigned long long)dpp_u32<CTRL, ROW_MASK>((uint32_t)(x >> 32)) << 32) | dpp_u32<CTRL, ROW_MASK>((uint32_t)x);
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_move(uint32_t x) {
+  return dpp_u32<CTRL, ROW_MASK>(x);
+}
+template <typename T>
+__device__ __forceinline__ T wave_inclusive_scan(T x) {
+  x += dpp_move<0x111, 0xf>(x);  // row_shr:1
+  x += dpp_move<0x112, 0xf>(x);  // row_shr:2
+  x += dpp_move<0x114, 0xf>(x);  // row_shr:4
+  x += dpp_move<0x118, 0xf>(x);  // row_shr:8
+  x += dpp_move<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
+  x += dpp_move<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
+  return x;
+}
+
+// Lane j's value of x (j uniform).
+__device__ __forceinline__ uint32_t lane_value(uint32_t x, int j) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)x, j);
+}
+__device__ __forceinline__ unsigned long long lane_value(unsigned long long x, int j) {
+  return ((unsigned long long)lane_value((uint32_t)(x >> 32), j) << 32) | lane_value((uint32_t)x, j);
+}
+
 // Digit search of a radix select, by one whole wave: bins[0 .. nbins) (nbins a
 // power of two from 64 to 4096) hold non-negative weights (counts or fixed-point
 // masses) of the candidates whose higher digits match, visited from bin nbins - 1
@@ -140,37 +175,26 @@ __device__ int wave_descend_find(const T* bins, int nbins, T need, T* before) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) own += v[j];
   }
-  T incl = own;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const T y = __shfl_up(incl, o, 64);
-    if (l >= o) incl += y;
-  }
+  const T incl = wave_inclusive_scan(own);
   const uint64_t hit = __ballot(incl >= need);
   if (hit == 0) return -1;
   const int lw = __builtin_ctzll(hit);
-  const T base = __shfl(incl - own, lw, 64);  // weight of the runs above run lw
+  const T base = lane_value(incl, lw) - lane_value(own, lw);  // weight of the runs above run lw
   const int top_w = nbins - 1 - per * lw;
-  T v = 0;
   int d = 0;
   T cum = 0;
   for (int j0 = 0; j0 < per; j0 += 64) {  // the run, 64 bins at a time from its top
     const int j = j0 + l;
-    v = j < per ? bins[top_w - j] : (T)0;
-    T c = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const T y = __shfl_up(c, o, 64);
-      if (l >= o) c += y;
-    }
+    const T v = j < per ? bins[top_w - j] : (T)0;
+    const T c = wave_inclusive_scan(v);
     const uint64_t cross = __ballot(j < per && base + cum + c >= need);
     if (cross) {
       const int lj = __builtin_ctzll(cross);
       d = top_w - (j0 + lj);
-      cum = base + cum + __shfl(c - v, lj, 64);
+      cum = base + cum + lane_value(c, lj) - lane_value(v, lj);
       break;
     }
-    cum += __shfl(c, 63, 64);
+    cum += lane_value(c, 63);
   }
   *before = cum;
   return d;
