@@ -1182,13 +1182,6 @@ __global__ __launch_bounds__(256) void sel_csr_fill(SelArgs a) {
 // csr_scan_head and csr_fill_row, one wave per row.  grid hq, kSmallThreads threads.
 constexpr int kSmallThreads = 1024;
 
-// Lane j's value of x (j uniform).
-__device__ __forceinline__ unsigned long long readlane_u64(unsigned long long x, int j) {
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, j);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(x >> 32), j);
-  return ((unsigned long long)hi << 32) | lo;
-}
-
 // k-th largest (k >= 1) of the bit patterns b of the lanes with `in` set (k of them at least).
 __device__ __forceinline__ uint32_t wave_kth_largest(uint32_t b, bool in, int k) {
   uint32_t t = 0;
@@ -1222,8 +1215,8 @@ __device__ bool small_vs_dir(const SelArgs& a, const float* P) {
     // the mass at or above each lane's own value, summed over the blocks in lane order
     unsigned long long ge = 0ull, total = 0ull;
     for (int j = 0; j < nb; ++j) {
-      const uint32_t bj = (uint32_t)__builtin_amdgcn_readlane((int)b, j);
-      const unsigned long long mj = readlane_u64(m, j);
+      const uint32_t bj = lane_value(b, j);
+      const unsigned long long mj = lane_value(m, j);
       total += mj;
       ge += bj >= b ? mj : 0ull;
     }
@@ -1242,7 +1235,7 @@ __device__ bool small_vs_dir(const SelArgs& a, const float* P) {
       t = cand;
       const uint64_t eqm = __ballot(in && b == t);
       const int first = __builtin_ctzll(eqm);
-      const unsigned long long ge_t = readlane_u64(ge, first);
+      const unsigned long long ge_t = lane_value(ge, first);
       const unsigned long long mt = fixed_mass(t);  // > 0: t carries mass
       const unsigned long long rest = need - (ge_t - (unsigned long long)__popcll(eqm) * mt);
       ceq = (int)((rest + mt - 1) / mt);
