@@ -769,6 +769,25 @@ def test_median_floor_stress_config4():
                  where="med stress")
 
 
+@pytest.mark.parametrize("n,hq,hkv,block", [(8192, 16, 4, 64), (6000, 24, 8, 128)])
+def test_short_layer_one_workgroup_per_unit(n, hq, hkv, block):
+    """Short layers with at least as many (head, query block) units as the persistent grid
+    holds run one workgroup per unit from one longest-first list (B = 64: 2048 units; B =
+    128: 1128 units, ragged tail): every head's selection and sampled attention rows
+    against the oracle, and the balanced launch equal to the fixed-order one bit for bit
+    (no row is split)."""
+    C = _crisp()
+    _say(f"short layer, one workgroup per unit: n={n} {hq}/{hkv} B={block}")
+    cfg = custom_config(n, hq, hkv, block=block, config_id=157 + block)
+    qsel = lambda h, nb: sorted({0, 1, nb // 2, nb - 2, nb - 1})
+    _check_layer(C, cfg, C.make_params(), qbs_per_head=qsel, where=f"one-per-unit n{n} B{block}")
+    q, k, v, _ = make_layer(cfg, device=DEV)
+    o, _, rp, ci = C.crisp_prefill_attn(q, k, v, C.make_params(), block, return_lists=True)
+    o_fixed = C.crisp_sparse_attn(q, k, v, rp, ci, block, balance=False)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o_fixed)
+
+
 @pytest.mark.parametrize("n,block", [(4000, 128), (777, 64)])
 def test_context_length_gate_is_dense(n, block):
     """Below the gate, prefill equals the dense kernel bit for bit and reports dense routes and
